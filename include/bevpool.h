@@ -1,0 +1,173 @@
+/*
+ * bevpool.h -- C ABI of the BEVPoolv2 view-transformation path for AMD
+ * Instinct MI355X (gfx950).
+ *
+ * BEVPoolv2 (section 2.1) turns the Lift-Splat-Shoot view transformer into
+ * two stages:
+ *   1. an offline preprocessing of the voxel index of every frustum point:
+ *      drop points outside the scope of all voxels and sort the rest by
+ *      voxel index, carrying each point's frustum index along as a trace;
+ *   2. an online pooling that, for every voxel, reads the depth score and the
+ *      image feature of each of its points through that trace and sums their
+ *      products, so the (N, D, H, W, C) frustum feature is never formed.
+ * bevpool_prepare is stage 1, bevpool_forward is stage 2 and
+ * bevpool_backward gives the gradients of stage 2 (which the paper does not
+ * describe; they follow from the chain rule).
+ *
+ * Shapes and layouts (all arrays dense, row-major, no padding):
+ *   depth     (B, N, D, H, W)   depth score, element type in_dtype
+ *   feat      (B, N, H, W, C)   image feature, channels last, in_dtype
+ *   coor      (P, 3) int32      voxel index (x, y, z) of every frustum point
+ *   out       (B, Z, Y, X, C)   BEV feature, channels last, out_dtype
+ * with P = B*N*D*H*W frustum points enumerated
+ *   p = (((b*N + n)*D + d)*H + h)*W + w,
+ * the same order as the depth score.  A point is kept when
+ * 0 <= x < X, 0 <= y < Y and 0 <= z < Z.  For a kept point
+ *   depth rank   = p
+ *   feature rank = ((b*N + n)*H + h)*W + w          (row of feat)
+ *   BEV rank     = ((b*Z + z)*Y + y)*X + x          (row of out)
+ *
+ * Conventions shared by every call:
+ *   - All array pointers are device pointers (hipMalloc'd or equivalent),
+ *     owned by the caller.  The library never allocates or frees device
+ *     memory and never synchronises the stream, except where stated.
+ *   - `stream` is a hipStream_t passed as void*; NULL is the default stream.
+ *     Work is enqueued asynchronously; results are visible after the stream
+ *     is synchronised.
+ *   - Every call validates its arguments before any HIP call and returns
+ *     BEVPOOL_OK (0) or a negative bevpool_status.  No C++ exception crosses
+ *     the ABI.  bevpool_last_error() gives a message for the calling thread.
+ *   - Limits: every dimension >= 1; P < 2^31; B*Z*Y*X*C < 2^31;
+ *     B*N*H*W*C < 2^31; C <= 1024.
+ *   - 16-byte aligned depth/feat/out/grad pointers with C a multiple of the
+ *     vector width (4 for f32, 8 for f16) take the vectorised kernels; any
+ *     other alignment or C takes the scalar kernels (not an error).
+ *   - Accumulation is always in float32.
+ *   - Kernels bounds-check every index they read from a plan, so a plan that
+ *     does not satisfy the documented invariants cannot cause out-of-bounds
+ *     accesses; the numerical result is then unspecified.
+ */
+#ifndef BEVPOOL_H
+#define BEVPOOL_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define BEVPOOL_VERSION 1
+
+typedef struct bevpool_shape {
+  int32_t B; /* samples */
+  int32_t N; /* camera views */
+  int32_t D; /* depth classes */
+  int32_t H; /* feature-map height */
+  int32_t W; /* feature-map width */
+  int32_t C; /* feature channels */
+  int32_t X; /* BEV cells along ego x */
+  int32_t Y; /* BEV cells along ego y */
+  int32_t Z; /* BEV cells along ego z */
+} bevpool_shape;
+
+enum bevpool_dtype {
+  BEVPOOL_F32 = 0, /* IEEE binary32 */
+  BEVPOOL_F16 = 1  /* IEEE binary16 */
+};
+
+enum bevpool_status {
+  BEVPOOL_OK = 0,
+  BEVPOOL_EINVAL = -1,     /* null pointer, non-positive dimension, bad count */
+  BEVPOOL_EOVERFLOW = -2,  /* a size exceeds the int32 index range or C > 1024 */
+  BEVPOOL_EDTYPE = -3,     /* unknown dtype or unsupported dtype combination */
+  BEVPOOL_EWORKSPACE = -4, /* workspace pointer NULL or smaller than required */
+  BEVPOOL_ELAUNCH = -5     /* a HIP call or kernel launch failed */
+};
+
+/* Library version (BEVPOOL_VERSION of the build). */
+int bevpool_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* bevpool_strerror(int status);
+
+/* Message describing the last failure of a call on this thread (for
+ * BEVPOOL_ELAUNCH it includes the HIP error string); "" if none. */
+const char* bevpool_last_error(void);
+
+/*
+ * Preprocessing (section 2.1, paragraphs 1-2): filter, sort, intervals.
+ *
+ * bevpool_prepare_workspace_size writes to *bytes the device scratch size
+ * bevpool_prepare needs for `shape` (radix ping-pong buffers, tile counts,
+ * digit histograms).
+ *
+ * bevpool_prepare reads coor (P x 3 int32) and writes:
+ *   ranks_depth, ranks_feat, ranks_bev   capacity P each; the first n_valid
+ *       entries hold the kept points sorted by BEV rank, ties in ascending
+ *       frustum index (a stable sort), so the order is unique;
+ *   interval_starts, interval_lengths    capacity min(P, B*Z*Y*X) each; the
+ *       first n_intervals entries give, for every occupied BEV cell in
+ *       ascending cell order, the position of its first point in the sorted
+ *       ranks and its number of points;
+ *   counts[0] = n_valid, counts[1] = n_intervals  (device int32[2]).
+ * Points outside the grid are filtered, not errors.  The caller reads
+ * `counts` after synchronising the stream.  Entries beyond the counts are
+ * left unspecified.  The workspace must stay untouched until the stream has
+ * executed the call.  Deterministic: the same coor always gives the same
+ * bytes.
+ */
+int bevpool_prepare_workspace_size(const bevpool_shape* shape, size_t* bytes);
+int bevpool_prepare(const bevpool_shape* shape, const int32_t* coor,
+                    int32_t* ranks_depth, int32_t* ranks_feat, int32_t* ranks_bev,
+                    int32_t* interval_starts, int32_t* interval_lengths,
+                    int32_t* counts, void* workspace, size_t workspace_bytes,
+                    void* stream);
+
+/*
+ * Pooling (section 2.1, paragraph 2): for every occupied cell j,
+ *   out[cell_j, c] = sum over i in [start_j, start_j + length_j) of
+ *                    depth[ranks_depth[i]] * feat[ranks_feat[i], c],
+ * with cell_j = ranks_bev[start_j]; every other cell of out is +0.0.
+ * The plan arrays are those of bevpool_prepare (or any plan with the same
+ * invariants: ranks_bev non-decreasing, intervals covering maximal runs of
+ * equal ranks_bev in ascending order); n_valid is the number of entries of
+ * the ranks arrays and n_intervals that of the interval arrays.  out is
+ * written in full, exactly once per element, without atomics; results are
+ * bitwise reproducible.  out must not alias any input.  in_dtype applies to depth and feat, out_dtype to
+ * out; both F32 or both F16, or F16 in with F32 out.  n_intervals == 0
+ * writes an all-zero out.
+ */
+int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                    const void* depth, const void* feat,
+                    const int32_t* ranks_depth, const int32_t* ranks_feat,
+                    const int32_t* ranks_bev, const int32_t* interval_starts,
+                    const int32_t* interval_lengths, int32_t n_valid,
+                    int32_t n_intervals, void* out, void* stream);
+
+/*
+ * Gradients of bevpool_forward (not in the paper; chain rule):
+ *   grad_depth[p]  = sum_c grad_out[rank_bev(p), c] * feat[rank_feat(p), c]
+ *                    for a kept point p, and +0.0 for a dropped point;
+ *   grad_feat[f,c] = sum over kept points p of pixel f of
+ *                    depth[p] * grad_out[rank_bev(p), c], +0.0 if none.
+ * grad_out has out's shape and out_dtype; grad_depth and grad_feat have the
+ * shapes and in_dtype of depth and feat.  The backward reads ranks_depth and
+ * ranks_bev (first n_valid entries) to map every frustum point to its cell;
+ * a point's feature row is its pixel, as bevpool_prepare's ranks_feat
+ * records.  Both gradients are written in full, exactly once per element,
+ * without atomics (deterministic).  Workspace: bevpool_backward_workspace_size
+ * bytes (one int32 per frustum point).
+ */
+int bevpool_backward_workspace_size(const bevpool_shape* shape, size_t* bytes);
+int bevpool_backward(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                     const void* grad_out, const void* depth, const void* feat,
+                     const int32_t* ranks_depth, const int32_t* ranks_bev,
+                     int32_t n_valid, void* grad_depth, void* grad_feat,
+                     void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+} /* extern "C" */
+#endif
+
+#endif /* BEVPOOL_H */

@@ -1,0 +1,288 @@
+"""Python binding of libbevpool.so (the C ABI declared in include/bevpool.h).
+
+The functions named ``bevpool_*`` mirror the C entry points one to one and
+only marshal arguments: tensors become device pointers, the shape becomes a
+``bevpool_shape`` struct and the current HIP stream is passed along.  The
+lower-case helpers (``prepare``, ``forward``, ``backward``) additionally
+allocate the output tensors with PyTorch.  Every step of the computation runs
+in the library's HIP kernels; if the library cannot be loaded, every call
+raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+import re
+from dataclasses import dataclass
+
+import torch
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libbevpool.so")
+HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "bevpool.h")
+
+BEVPOOL_F32 = 0
+BEVPOOL_F16 = 1
+
+_DTYPE_CODE = {torch.float32: BEVPOOL_F32, torch.float16: BEVPOOL_F16}
+_CODE_DTYPE = {BEVPOOL_F32: torch.float32, BEVPOOL_F16: torch.float16}
+
+
+class BevpoolError(RuntimeError):
+    def __init__(self, status: int, func: str, message: str):
+        super().__init__(f"{func} failed with status {status}: {message}")
+        self.status = status
+
+
+class bevpool_shape(ctypes.Structure):
+    _fields_ = [(k, ctypes.c_int32) for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z")]
+
+
+_lib = None
+
+
+def load_library(path: str | None = None) -> ctypes.CDLL:
+    """Load libbevpool.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None and path is None:
+        return _lib
+    p = path or LIB_PATH
+    if not os.path.exists(p):
+        raise RuntimeError(f"{p} not found: build it with paper_2211_17111_amd.build.build()")
+    lib = ctypes.CDLL(p)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    shp = ctypes.POINTER(bevpool_shape)
+    lib.bevpool_version.restype = ctypes.c_int
+    lib.bevpool_version.argtypes = []
+    lib.bevpool_strerror.restype = ctypes.c_char_p
+    lib.bevpool_strerror.argtypes = [ctypes.c_int]
+    lib.bevpool_last_error.restype = ctypes.c_char_p
+    lib.bevpool_last_error.argtypes = []
+    lib.bevpool_prepare_workspace_size.restype = ctypes.c_int
+    lib.bevpool_prepare_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
+    lib.bevpool_prepare.restype = ctypes.c_int
+    lib.bevpool_prepare.argtypes = [shp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
+    lib.bevpool_forward.restype = ctypes.c_int
+    lib.bevpool_forward.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp,
+                                    i32, i32, vp, vp]
+    lib.bevpool_backward_workspace_size.restype = ctypes.c_int
+    lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
+    lib.bevpool_backward.restype = ctypes.c_int
+    lib.bevpool_backward.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, i32,
+                                     vp, vp, vp, sz, vp]
+    if path is None:
+        _lib = lib
+    return lib
+
+
+def declared_symbols(header: str = HEADER_PATH) -> list[str]:
+    """Names of the functions declared in include/bevpool.h."""
+    with open(header) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bevpool_\w+)\s*\(", text)))
+
+
+# ----------------------------------------------------------------- marshalling
+
+def make_shape(shape) -> bevpool_shape:
+    if isinstance(shape, bevpool_shape):
+        return shape
+    get = (lambda k: shape[k]) if isinstance(shape, dict) else (lambda k: getattr(shape, k))
+    return bevpool_shape(*(int(get(k)) for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z")))
+
+
+def _ptr(x) -> int | None:
+    if x is None:
+        return None
+    if isinstance(x, torch.Tensor):
+        return x.data_ptr()
+    return int(x)
+
+
+def _stream(stream) -> int | None:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream if torch.cuda.is_available() else None
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _check(lib, status: int, func: str):
+    if status != 0:
+        msg = lib.bevpool_last_error().decode() or lib.bevpool_strerror(status).decode()
+        raise BevpoolError(status, func, msg)
+
+
+def bevpool_version() -> int:
+    return load_library().bevpool_version()
+
+
+def bevpool_strerror(status: int) -> str:
+    return load_library().bevpool_strerror(status).decode()
+
+
+def bevpool_last_error() -> str:
+    return load_library().bevpool_last_error().decode()
+
+
+def bevpool_prepare_workspace_size(shape) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib, lib.bevpool_prepare_workspace_size(ctypes.byref(make_shape(shape)), ctypes.byref(n)),
+           "bevpool_prepare_workspace_size")
+    return n.value
+
+
+def bevpool_prepare(shape, coor, ranks_depth, ranks_feat, ranks_bev, interval_starts,
+                    interval_lengths, counts, workspace, workspace_bytes, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_prepare(ctypes.byref(s), _ptr(coor), _ptr(ranks_depth), _ptr(ranks_feat),
+                                    _ptr(ranks_bev), _ptr(interval_starts), _ptr(interval_lengths),
+                                    _ptr(counts), _ptr(workspace), int(workspace_bytes),
+                                    _stream(stream)),
+           "bevpool_prepare")
+
+
+def bevpool_forward(shape, in_dtype, out_dtype, depth, feat, ranks_depth, ranks_feat, ranks_bev,
+                    interval_starts, interval_lengths, n_valid, n_intervals, out,
+                    stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_forward(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
+                                    _ptr(feat), _ptr(ranks_depth), _ptr(ranks_feat), _ptr(ranks_bev),
+                                    _ptr(interval_starts), _ptr(interval_lengths), int(n_valid),
+                                    int(n_intervals), _ptr(out), _stream(stream)),
+           "bevpool_forward")
+
+
+def bevpool_backward_workspace_size(shape) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib, lib.bevpool_backward_workspace_size(ctypes.byref(make_shape(shape)), ctypes.byref(n)),
+           "bevpool_backward_workspace_size")
+    return n.value
+
+
+def bevpool_backward(shape, in_dtype, out_dtype, grad_out, depth, feat, ranks_depth, ranks_bev,
+                     n_valid, grad_depth, grad_feat, workspace, workspace_bytes, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_backward(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(grad_out),
+                                     _ptr(depth), _ptr(feat), _ptr(ranks_depth), _ptr(ranks_bev),
+                                     int(n_valid), _ptr(grad_depth), _ptr(grad_feat),
+                                     _ptr(workspace), int(workspace_bytes), _stream(stream)),
+           "bevpool_backward")
+
+
+# ------------------------------------------------------------ allocating helpers
+
+@dataclass
+class Plan:
+    """Output of prepare: the sorted ranks and the interval table."""
+    shape: dict
+    ranks_depth: torch.Tensor
+    ranks_feat: torch.Tensor
+    ranks_bev: torch.Tensor
+    interval_starts: torch.Tensor
+    interval_lengths: torch.Tensor
+    n_valid: int
+    n_intervals: int
+
+
+def _shape_dict(shape) -> dict:
+    s = make_shape(shape)
+    return {k: getattr(s, k) for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z")}
+
+
+def _require(t: torch.Tensor, name: str, dtype=None):
+    if not isinstance(t, torch.Tensor) or not t.is_cuda:
+        raise ValueError(f"{name} must be a CUDA (HIP) tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+
+
+def prepare(coor: torch.Tensor, shape, stream=None) -> Plan:
+    """Filter, sort and find intervals on the GPU; reads the two counts back."""
+    sd = _shape_dict(shape)
+    _require(coor, "coor", torch.int32)
+    P = sd["B"] * sd["N"] * sd["D"] * sd["H"] * sd["W"]
+    if coor.shape != (P, 3):
+        raise ValueError(f"coor must be ({P}, 3), got {tuple(coor.shape)}")
+    cells = sd["B"] * sd["Z"] * sd["Y"] * sd["X"]
+    dev = coor.device
+    i32 = dict(dtype=torch.int32, device=dev)
+    rd = torch.empty(P, **i32)
+    rf = torch.empty(P, **i32)
+    rb = torch.empty(P, **i32)
+    cap = min(P, cells)
+    st = torch.empty(cap, **i32)
+    ln = torch.empty(cap, **i32)
+    counts = torch.zeros(2, **i32)
+    ws_bytes = bevpool_prepare_workspace_size(sd)
+    ws = torch.empty(max(ws_bytes, 1), dtype=torch.uint8, device=dev)
+    bevpool_prepare(sd, coor, rd, rf, rb, st, ln, counts, ws, ws_bytes, stream)
+    nv, ni = (int(v) for v in counts.cpu().tolist())
+    return Plan(sd, rd[:nv], rf[:nv], rb[:nv], st[:ni], ln[:ni], nv, ni)
+
+
+def forward(depth: torch.Tensor, feat: torch.Tensor, plan: Plan, out_dtype=None,
+            out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    sd = plan.shape
+    B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
+    _require(depth, "depth")
+    _require(feat, "feat", depth.dtype)
+    if depth.dtype not in _DTYPE_CODE:
+        raise ValueError(f"unsupported dtype {depth.dtype}")
+    if tuple(depth.shape) != (B, N, D, H, W) or tuple(feat.shape) != (B, N, H, W, C):
+        raise ValueError("depth/feat shapes do not match the plan")
+    odt = out_dtype or depth.dtype
+    if out is None:
+        out = torch.empty((B, Z, Y, X, C), dtype=odt, device=depth.device)
+    _require(out, "out", odt)
+    bevpool_forward(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, plan.ranks_depth,
+                    plan.ranks_feat, plan.ranks_bev, plan.interval_starts, plan.interval_lengths,
+                    plan.n_valid, plan.n_intervals, out, stream)
+    return out
+
+
+def backward(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor, plan: Plan,
+             workspace: torch.Tensor | None = None, stream=None):
+    sd = plan.shape
+    B, N, D, H, W, C = (sd[k] for k in ("B", "N", "D", "H", "W", "C"))
+    _require(grad_out, "grad_out")
+    _require(depth, "depth")
+    _require(feat, "feat", depth.dtype)
+    gd = torch.empty_like(depth)
+    gf = torch.empty_like(feat)
+    ws_bytes = bevpool_backward_workspace_size(sd)
+    if workspace is None:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=depth.device)
+    bevpool_backward(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[grad_out.dtype], grad_out, depth, feat,
+                     plan.ranks_depth, plan.ranks_bev, plan.n_valid, gd, gf, workspace,
+                     workspace.numel() * workspace.element_size(), stream)
+    return gd, gf
+
+
+class BevPoolFunction(torch.autograd.Function):
+    """Autograd wrapper: forward pools, backward returns grad_depth, grad_feat."""
+
+    @staticmethod
+    def forward(ctx, depth, feat, plan: Plan, out_dtype=None):
+        ctx.plan = plan
+        ctx.save_for_backward(depth, feat)
+        return forward(depth, feat, plan, out_dtype)
+
+    @staticmethod
+    def backward(ctx, grad_out):
+        depth, feat = ctx.saved_tensors
+        gd, gf = backward(grad_out.contiguous(), depth, feat, ctx.plan)
+        return gd, gf, None, None
+
+
+def bev_pool(depth, feat, plan: Plan, out_dtype=None):
+    return BevPoolFunction.apply(depth, feat, plan, out_dtype)

@@ -1,0 +1,200 @@
+// Gradients of the BEVPoolv2 pooling (the paper gives none; chain rule):
+//   grad_depth[p]  = <grad_out[cell(p), :], feat[pixel(p), :]>   (0 if p dropped)
+//   grad_feat[f,:] = sum over kept p of pixel f of depth[p] * grad_out[cell(p), :]
+//
+// Both are produced by one pixel-major pass so every output element is
+// written exactly once, without atomics:
+//   1. k_fill + k_point_map scatter the plan back into frustum-index order,
+//      map[p] = BEV rank of p, or -1 when p was dropped;
+//   2. k_backward gives each feature-map pixel to a group of GS lanes (GS a
+//      power of two covering the row's 16-byte vectors).  The group keeps the
+//      pixel's feature row in registers, walks its D depth points, gathers the
+//      upstream-gradient row of each kept point's cell, reduces the dot
+//      product across the group for grad_depth and accumulates
+//      depth * grad_out for grad_feat.
+
+#include "device_utils.h"
+#include "internal.h"
+#include "vec.h"
+
+namespace bevpool {
+
+namespace {
+
+constexpr int kBwdThreads = 256;
+constexpr int kBwdWaves = kBwdThreads / kWave;
+constexpr int kBwdUnroll = 4;
+
+__global__ __launch_bounds__(256) void k_fill(int32_t* __restrict__ map, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) map[i] = v;
+}
+
+__global__ __launch_bounds__(256) void k_point_map(const int32_t* __restrict__ rd,
+                                                   const int32_t* __restrict__ rb, int64_t n_valid,
+                                                   int32_t* __restrict__ map, int64_t P,
+                                                   int64_t cells) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n_valid) {
+    const int32_t p = rd[i];
+    const int32_t c = rb[i];
+    if (p >= 0 && p < P) map[p] = (c >= 0 && c < cells) ? c : -1;
+  }
+}
+
+template <typename TIn, typename TG, int VEC, int NV>
+__global__ __launch_bounds__(kBwdThreads) void k_backward(
+    const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
+    const int32_t* __restrict__ map, TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat,
+    int32_t C, int32_t D, int64_t hw, int64_t rows, int GS) {
+  const int lane = lane_id();
+  const int G = kWave / GS;
+  const int g = lane / GS;
+  const int vi = lane - g * GS;
+  const int64_t f = ((int64_t)blockIdx.x * kBwdWaves + threadIdx.x / kWave) * G + g;
+  const bool pix_ok = f < rows;
+  const int CV = C / VEC;
+
+  float fv[NV][VEC];
+  float acc[NV][VEC];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int v = vi + k * GS;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[k][e] = 0.f;
+    if (pix_ok && v < CV) {
+      Vec<TIn, VEC>::load(feat + f * C + (int64_t)v * VEC, fv[k]);
+    } else {
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) fv[k][e] = 0.f;
+    }
+  }
+
+  const int64_t bn = pix_ok ? f / hw : 0;
+  const int64_t p0 = bn * D * hw + (pix_ok ? f % hw : 0);  // point at depth 0
+
+  for (int d0 = 0; d0 < D; d0 += GS) {
+    // one depth point per lane: cell and depth score, zero grad for drops
+    const int dl = d0 + vi;
+    int my_cell = -1;
+    float my_dep = 0.f;
+    if (pix_ok && dl < D) {
+      const int64_t p = p0 + (int64_t)dl * hw;
+      my_cell = map[p];
+      if (my_cell >= 0) {
+        my_dep = to_float(depth[p]);
+      } else {
+        grad_depth[p] = (TIn)0.f;
+      }
+    }
+    const int nd = min(GS, D - d0);
+    for (int k0 = 0; k0 < nd; k0 += kBwdUnroll) {
+      int cell[kBwdUnroll];
+      float dep[kBwdUnroll];
+      float gv[kBwdUnroll][NV][VEC];
+#pragma unroll
+      for (int u = 0; u < kBwdUnroll; ++u) {
+        const int src = g * GS + ((k0 + u) & (GS - 1));
+        cell[u] = __shfl(my_cell, src);
+        dep[u] = __shfl(my_dep, src);
+        if (k0 + u >= nd) cell[u] = -1;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const int v = vi + k * GS;
+          if (cell[u] >= 0 && v < CV) {
+            Vec<TG, VEC>::load(grad_out + (int64_t)cell[u] * C + (int64_t)v * VEC, gv[u][k]);
+          } else {
+#pragma unroll
+            for (int e = 0; e < VEC; ++e) gv[u][k][e] = 0.f;
+          }
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kBwdUnroll; ++u) {
+        float part = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            part = fmaf(gv[u][k][e], fv[k][e], part);
+            acc[k][e] = fmaf(dep[u], gv[u][k][e], acc[k][e]);
+          }
+        for (int o = GS >> 1; o > 0; o >>= 1) part += __shfl_xor(part, o);
+        if (vi == 0 && cell[u] >= 0)
+          grad_depth[p0 + (int64_t)(d0 + k0 + u) * hw] = (TIn)part;
+      }
+    }
+  }
+
+  if (pix_ok) {
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+      const int v = vi + k * GS;
+      if (v < CV) Vec<TIn, VEC>::store(grad_feat + f * C + (int64_t)v * VEC, acc[k]);
+    }
+  }
+}
+
+template <typename TIn, typename TG, int VEC, int NV>
+hipError_t run(const Dims& d, const void* grad_out, const void* depth, const void* feat,
+               const int32_t* map, void* grad_depth, void* grad_feat, hipStream_t stream) {
+  const int CV = (int)d.C / VEC;
+  const int per_lane = (CV + NV - 1) / NV;
+  int GS = 1;
+  while (GS < per_lane) GS <<= 1;
+  const int G = kWave / GS;
+  const int64_t pix_per_block = (int64_t)G * kBwdWaves;
+  const dim3 grid((unsigned)((d.rows + pix_per_block - 1) / pix_per_block));
+  k_backward<TIn, TG, VEC, NV><<<grid, dim3(kBwdThreads), 0, stream>>>(
+      static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
+      static_cast<const TIn*>(feat), map, static_cast<TIn*>(grad_depth),
+      static_cast<TIn*>(grad_feat), (int32_t)d.C, (int32_t)d.D, d.hw, d.rows, GS);
+  return hipGetLastError();
+}
+
+template <typename TIn, typename TG, int VEC>
+hipError_t run_nv(const Dims& d, const void* grad_out, const void* depth, const void* feat,
+                  const int32_t* map, void* grad_depth, void* grad_feat, hipStream_t stream) {
+  const int64_t CV = d.C / VEC;
+  if (CV <= 64) return run<TIn, TG, VEC, 1>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  if (CV <= 128) return run<TIn, TG, VEC, 2>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  if (CV <= 256) return run<TIn, TG, VEC, 4>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  if (CV <= 512) return run<TIn, TG, VEC, 8>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  return run<TIn, TG, VEC, 16>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+}
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+size_t backward_workspace_bytes(const Dims& d) { return sizeof(int32_t) * (size_t)d.P; }
+
+hipError_t launch_backward(const Dims& d, int in_dtype, int out_dtype, const void* grad_out,
+                           const void* depth, const void* feat, const int32_t* rd,
+                           const int32_t* rb, int32_t n_valid, void* grad_depth,
+                           void* grad_feat, void* workspace, hipStream_t stream) {
+  int32_t* map = static_cast<int32_t*>(workspace);
+  k_fill<<<dim3((unsigned)((d.P + 255) / 256)), dim3(256), 0, stream>>>(map, d.P, -1);
+  if (n_valid > 0)
+    k_point_map<<<dim3((unsigned)((n_valid + 255) / 256)), dim3(256), 0, stream>>>(
+        rd, rb, n_valid, map, d.P, d.cells);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+
+  const bool al = aligned16(grad_out) && aligned16(feat) && aligned16(grad_feat);
+  if (in_dtype == BEVPOOL_F32) {
+    if (al && d.C % 4 == 0)
+      return run_nv<float, float, 4>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+    return run_nv<float, float, 1>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  }
+  if (out_dtype == BEVPOOL_F16) {
+    if (al && d.C % 8 == 0)
+      return run_nv<half_t, half_t, 8>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+    return run_nv<half_t, half_t, 1>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  }
+  if (al && d.C % 8 == 0)
+    return run_nv<half_t, float, 8>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+  return run_nv<half_t, float, 1>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+}
+
+}  // namespace bevpool

@@ -1,0 +1,138 @@
+"""C-ABI contract of libbevpool.so, checked without a GPU.
+
+Validation happens before any HIP call, so every documented error path can
+be exercised here with dummy (never dereferenced) pointers.
+"""
+
+import ctypes
+
+import pytest
+
+from paper_2211_17111_amd import bevpool as bp
+
+OK, EINVAL, EOVERFLOW, EDTYPE, EWORKSPACE, ELAUNCH = 0, -1, -2, -3, -4, -5
+DUMMY = 0x1000  # non-NULL, never dereferenced: every call below fails validation first
+
+SHAPE = dict(B=1, N=6, D=118, H=40, W=100, C=80, X=128, Y=128, Z=1)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    return bp.load_library()
+
+
+def _shape(**kw):
+    return bp.make_shape({**SHAPE, **kw})
+
+
+def test_exports_every_declared_symbol(lib):
+    names = bp.declared_symbols()
+    assert set(names) == {
+        "bevpool_version", "bevpool_strerror", "bevpool_last_error",
+        "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
+        "bevpool_backward_workspace_size", "bevpool_backward",
+    }
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_version_and_strerror(lib):
+    assert lib.bevpool_version() == 1
+    for code in (OK, EINVAL, EOVERFLOW, EDTYPE, EWORKSPACE, ELAUNCH):
+        assert lib.bevpool_strerror(code)
+    assert lib.bevpool_strerror(12345) == b"unknown status"
+
+
+def test_workspace_sizes(lib):
+    s = _shape()
+    n = ctypes.c_size_t()
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(s), ctypes.byref(n)) == OK
+    P = 6 * 118 * 40 * 100
+    assert n.value >= 2 * 4 * P  # radix ping-pong buffers
+    assert lib.bevpool_backward_workspace_size(ctypes.byref(s), ctypes.byref(n)) == OK
+    assert n.value == 4 * P
+    assert lib.bevpool_prepare_workspace_size(None, ctypes.byref(n)) == EINVAL
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(s), None) == EINVAL
+
+
+@pytest.mark.parametrize("dim", list("BNDHWCXYZ"))
+def test_non_positive_dims_rejected(lib, dim):
+    for v in (0, -3):
+        s = _shape(**{dim: v})
+        n = ctypes.c_size_t()
+        assert lib.bevpool_prepare_workspace_size(ctypes.byref(s), ctypes.byref(n)) == EINVAL
+        assert b"must be >= 1" in lib.bevpool_last_error()
+
+
+def test_overflow_rejected(lib):
+    n = ctypes.c_size_t()
+    big = _shape(B=700)   # P = 1.98e9 < 2^31
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(big), ctypes.byref(n)) == OK
+    over = _shape(B=800)   # P = 2.27e9 >= 2^31
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(over), ctypes.byref(n)) == EOVERFLOW
+    wide = _shape(C=2048)
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(wide), ctypes.byref(n)) == EOVERFLOW
+    out_over = _shape(B=1, X=8192, Y=8192, Z=1, C=64)
+    assert lib.bevpool_prepare_workspace_size(ctypes.byref(out_over), ctypes.byref(n)) == EOVERFLOW
+
+
+def _fwd(lib, s, in_dt=0, out_dt=0, nv=100, ni=10, ptrs=None, out=DUMMY):
+    p = ptrs or [DUMMY] * 7
+    return lib.bevpool_forward(ctypes.byref(s), in_dt, out_dt, *p, nv, ni, out, None)
+
+
+def test_forward_validation(lib):
+    s = _shape()
+    assert _fwd(lib, s, in_dt=2) == EDTYPE
+    assert _fwd(lib, s, out_dt=7) == EDTYPE
+    assert _fwd(lib, s, in_dt=0, out_dt=1) == EDTYPE   # f32 in, f16 out
+    assert _fwd(lib, s, ni=-1) == EINVAL
+    assert _fwd(lib, s, nv=10**6, ni=128 * 128 + 1) == EINVAL    # more intervals than cells
+    assert _fwd(lib, s, nv=5, ni=6) == EINVAL          # more intervals than points
+    assert _fwd(lib, s, nv=-1, ni=0) == EINVAL
+    assert _fwd(lib, s, nv=6 * 118 * 40 * 100 + 1) == EINVAL
+    assert _fwd(lib, s, out=None) == EINVAL
+    for k in range(7):
+        ptrs = [DUMMY] * 7
+        ptrs[k] = None
+        assert _fwd(lib, s, ptrs=ptrs) == EINVAL
+        assert b"is NULL" in lib.bevpool_last_error()
+    assert lib.bevpool_forward(None, 0, 0, *([DUMMY] * 7), 1, 1, DUMMY, None) == EINVAL
+
+
+def test_prepare_validation(lib):
+    s = _shape()
+    need = ctypes.c_size_t()
+    lib.bevpool_prepare_workspace_size(ctypes.byref(s), ctypes.byref(need))
+    args = [DUMMY] * 7
+    assert lib.bevpool_prepare(ctypes.byref(s), *args, DUMMY, need.value - 1, None) == EWORKSPACE
+    assert lib.bevpool_prepare(ctypes.byref(s), *args, None, need.value, None) == EWORKSPACE
+    for k in range(7):
+        a = [DUMMY] * 7
+        a[k] = None
+        assert lib.bevpool_prepare(ctypes.byref(s), *a, DUMMY, need.value, None) == EINVAL
+
+
+def test_backward_validation(lib):
+    s = _shape()
+    need = ctypes.c_size_t()
+    lib.bevpool_backward_workspace_size(ctypes.byref(s), ctypes.byref(need))
+    def call(nv=5, ws=DUMMY, wsb=None, ptrs=None, in_dt=0, out_dt=0):
+        p = ptrs or [DUMMY] * 7
+        return lib.bevpool_backward(ctypes.byref(s), in_dt, out_dt, p[0], p[1], p[2], p[3], p[4],
+                                    nv, p[5], p[6], ws, need.value if wsb is None else wsb, None)
+    assert call(ws=None) == EWORKSPACE
+    assert call(wsb=need.value - 4) == EWORKSPACE
+    assert call(nv=-1) == EINVAL
+    assert call(nv=6 * 118 * 40 * 100 + 1) == EINVAL
+    assert call(in_dt=3) == EDTYPE
+    for k in range(7):
+        p = [DUMMY] * 7
+        p[k] = None
+        assert call(ptrs=p) == EINVAL
+
+
+def test_binding_raises_with_message(lib):
+    with pytest.raises(bp.BevpoolError) as ei:
+        bp.bevpool_prepare_workspace_size(dict(SHAPE, C=0))
+    assert ei.value.status == EINVAL and "C" in str(ei.value)

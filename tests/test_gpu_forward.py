@@ -1,0 +1,174 @@
+"""GPU forward pooling against the float64 oracle.
+
+Full-output comparison where the oracle runs in seconds; at the large sizes,
+sampled cells (longest intervals, random occupied and empty cells, first and
+last cell) plus properties that hold at any size.  Tolerance per element:
+|gpu - oracle| <= tol * sum|terms| + 1e-6, tol = 1e-5 (fp32 inputs) or 2e-3
+(fp16 inputs, fp32 accumulation).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import _gpu
+import oracle
+from paper_2211_17111_amd import bevpool as bp
+from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(depth, feat, coor, shape, out_dtype=None):
+    plan = _gpu.run_prepare(coor, shape)
+    odt = _gpu.torch_dtype(out_dtype) if out_dtype else None
+    out = bp.forward(_gpu.to_dev(depth), _gpu.to_dev(feat), plan, out_dtype=odt)
+    torch.cuda.synchronize()
+    return out, plan
+
+
+@pytest.mark.parametrize("name", ["tiny", "bevdet"])
+def test_forward_full(name):
+    cfg = CONFIGS[name]
+    _gpu.say(f"forward full parity: {name}")
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg)
+    out, _ = _run(data["depth"], data["feat"], coor, cfg.shape())
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
+    _gpu.assert_within(out.cpu().numpy(), ref, mag, cfg.dtype, name)
+
+
+@pytest.mark.parametrize("C", [1, 3, 16, 17, 64, 80, 260])
+@pytest.mark.parametrize("dtype,out_dtype", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
+def test_forward_random_channels(C, dtype, out_dtype):
+    shape = dict(B=2, N=2, D=9, H=7, W=13, C=C, X=12, Y=10, Z=2)
+    rng = np.random.default_rng(C)
+    coor = random_coor(rng, shape, p_out=0.4)
+    data = draw_small(rng, shape, dtype=dtype)
+    _gpu.say(f"forward random C={C} {dtype}->{out_dtype}")
+    out, _ = _run(data["depth"], data["feat"], coor, shape, out_dtype)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+    _gpu.assert_within(out.float().cpu().numpy(), ref, mag, dtype, f"C={C} {dtype}->{out_dtype}")
+
+
+def test_forward_misaligned_takes_scalar_path():
+    shape = dict(B=1, N=2, D=6, H=5, W=9, C=8, X=6, Y=6, Z=1)
+    rng = np.random.default_rng(1)
+    coor = random_coor(rng, shape)
+    data = draw_small(rng, shape)
+    plan = _gpu.run_prepare(coor, shape)
+    # feat and out offset by one element: not 16-byte aligned
+    fbuf = torch.empty(data["feat"].size + 1, dtype=torch.float32, device=_gpu.DEV)
+    feat = fbuf[1:].view(data["feat"].shape)
+    feat.copy_(torch.from_numpy(data["feat"]))
+    obuf = torch.empty(1 * 6 * 6 * 8 + 1, dtype=torch.float32, device=_gpu.DEV)
+    out = obuf[1:].view(1, 1, 6, 6, 8)
+    bp.forward(_gpu.to_dev(data["depth"]), feat, plan, out=out)
+    torch.cuda.synchronize()
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+    _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", "misaligned")
+
+
+def test_forward_edge_cases():
+    shape = dict(B=1, N=1, D=8, H=50, W=60, C=80, X=8, Y=8, Z=1)   # P = 24000
+    P = 24000
+    rng = np.random.default_rng(2)
+    data = draw_small(rng, shape)
+    cases = {
+        "no point in range": np.full((P, 3), -5, dtype=np.int32),
+        "one interval of 24000 points": np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1)),
+        "first and last cell only": np.where(rng.random((P, 1)) < 0.5,
+                                             np.array([[0, 0, 0]]), np.array([[7, 7, 0]])).astype(np.int32),
+        "single point": np.concatenate([np.full((P - 1, 3), -1, dtype=np.int32),
+                                        np.array([[3, 3, 0]], dtype=np.int32)]),
+    }
+    for label, coor in cases.items():
+        _gpu.say(f"forward edge case: {label}")
+        out, _ = _run(data["depth"], data["feat"], coor, shape)
+        ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+        _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", label)
+        occupied = mag.reshape(-1, 80).any(axis=1)
+        assert np.all(out.cpu().numpy().reshape(-1, 80)[~occupied] == 0.0), label
+
+
+def test_forward_nan_free_and_empty_exact_zero():
+    # Poison the output buffer first: every element must be overwritten.
+    cfg = CONFIGS["bevdet"]
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg)
+    plan = _gpu.run_prepare(coor, cfg.shape())
+    out = torch.full((1, 1, 128, 128, 64), float("nan"), device=_gpu.DEV)
+    bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan, out=out)
+    o = out.cpu().numpy().reshape(-1, 64)
+    assert np.isfinite(o).all()
+    occ = np.zeros(o.shape[0], dtype=bool)
+    occ[plan.ranks_bev.cpu().numpy()] = True
+    assert np.all(o[~occ] == 0.0) and np.signbit(o[~occ]).sum() == 0
+
+
+def _sample_cells(plan, cells, rng, k=120):
+    st = plan.interval_starts.cpu().numpy()
+    ln = plan.interval_lengths.cpu().numpy()
+    rb = plan.ranks_bev.cpu().numpy()
+    occ_cells = rb[st]
+    longest = occ_cells[np.argsort(ln)[-20:]]
+    rand_occ = rng.choice(occ_cells, size=min(k, occ_cells.size), replace=False)
+    empty = np.setdiff1d(np.arange(cells), occ_cells)
+    rand_empty = rng.choice(empty, size=min(20, empty.size), replace=False) if empty.size else empty
+    return np.unique(np.concatenate([longest, rand_occ, rand_empty, [0, cells - 1]]))
+
+
+@pytest.mark.parametrize("name", ["headline", "large", "train"])
+def test_forward_full_size_sampled(name):
+    cfg = CONFIGS[name]
+    _gpu.say(f"forward sampled parity: {name}")
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    out, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), cfg.out_dtype)
+    rng = np.random.default_rng(7)
+    cells = _sample_cells(plan, cfg.cells, rng)
+    ref, mag = oracle.forward_cells_ref(data["depth"], data["feat"], coor, cfg.shape(), cells)
+    got = out.reshape(cfg.cells, cfg.C)[torch.from_numpy(cells).to(_gpu.DEV)].float().cpu().numpy()
+    _gpu.assert_within(got, ref, mag, cfg.dtype, name)
+    # mass conservation over the whole output, in float64 on the host
+    kept = oracle.kept_mask(coor, cfg.shape()).reshape(cfg.B, cfg.N, cfg.D, cfg.H, cfg.W)
+    mass = np.einsum("bndhw,bnhwc->c", data["depth"].astype(np.float64) * kept,
+                     data["feat"].astype(np.float64))
+    absmass = np.einsum("bndhw,bnhwc->c", np.abs(data["depth"].astype(np.float64)) * kept,
+                        np.abs(data["feat"].astype(np.float64)))
+    total = out.double().reshape(cfg.cells, cfg.C).sum(dim=0).cpu().numpy()
+    _gpu.assert_within(total, mass, absmass, cfg.dtype, f"{name} mass")
+
+
+def test_forward_deterministic_and_batch_independent():
+    cfg = CONFIGS["large"]
+    _gpu.say("forward determinism + batch independence: large")
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    out1, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), "f32")
+    out2 = bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan,
+                      out_dtype=torch.float32)
+    assert torch.equal(out1, out2)
+    # sample b of a B=4 run equals a B=1 run on that sample's inputs, bitwise
+    one = dict(cfg.shape(), B=1)
+    per = cfg.P // cfg.B
+    plan1 = _gpu.run_prepare(coor[:per], one)
+    for b in (0, 3):
+        o = bp.forward(_gpu.to_dev(data["depth"][b:b + 1]), _gpu.to_dev(data["feat"][b:b + 1]),
+                       plan1, out_dtype=torch.float32)
+        assert torch.equal(o[0], out1[b])
+
+
+def test_forward_with_oracle_plan():
+    # The plan is plain arrays at the boundary: the oracle's plan drives the GPU.
+    cfg = CONFIGS["bevdet"]
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    ref_plan = oracle.prepare_ref(coor, cfg.shape())
+    plan = bp.Plan(cfg.shape(), *(_gpu.to_dev(ref_plan[k]) for k in
+                                  ("ranks_depth", "ranks_feat", "ranks_bev",
+                                   "interval_starts", "interval_lengths")),
+                   ref_plan["n_valid"], ref_plan["n_intervals"])
+    out = bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
+    _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", "oracle plan")
