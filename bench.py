@@ -124,6 +124,8 @@ def main():
     log(f"{len(sets)} buffer sets, {sets[0].nbytes() / 2**20:.1f} MiB each")
     ws_p_bytes = bp.bevpool_prepare_workspace_size(shape)
     ws_p = torch.empty(ws_p_bytes, dtype=torch.uint8, device=dev)
+    ws_f_bytes = bp.bevpool_forward_workspace_size(shape)
+    ws_f = torch.empty(ws_f_bytes, dtype=torch.uint8, device=dev)
     ws_b_bytes = bp.bevpool_backward_workspace_size(shape)
     ws_b = torch.empty(ws_b_bytes, dtype=torch.uint8, device=dev)
     code = bp.BEVPOOL_F32 if cfg.dtype == "f32" else bp.BEVPOOL_F16
@@ -144,7 +146,7 @@ def main():
 
     def forward(s):
         bp.bevpool_forward(shape, code, ocode, s.depth, s.feat, s.rd, s.rf, s.rb, s.st, s.ln, nv, ni,
-                           s.out, stream)
+                           s.out, ws_f, ws_f_bytes, stream)
 
     def backward(s):
         bp.bevpool_backward(shape, code, ocode, s.grad_out, s.depth, s.feat, s.rd, s.rb, nv, s.gd, s.gf,

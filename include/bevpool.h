@@ -134,16 +134,23 @@ int bevpool_prepare(const bevpool_shape* shape, const int32_t* coor,
  * equal ranks_bev in ascending order); n_valid is the number of entries of
  * the ranks arrays and n_intervals that of the interval arrays.  out is
  * written in full, exactly once per element, without atomics; results are
- * bitwise reproducible.  out must not alias any input.  in_dtype applies to depth and feat, out_dtype to
- * out; both F32 or both F16, or F16 in with F32 out.  n_intervals == 0
- * writes an all-zero out.
+ * bitwise reproducible.  out must not alias any input.  in_dtype applies to
+ * depth and feat, out_dtype to out; both F32 or both F16, or F16 in with F32
+ * out.  n_intervals == 0 writes an all-zero out.
+ *
+ * Work is split into equal ranges of sorted points, one wavefront each;
+ * cells cut by a range boundary are summed from per-range partials held in
+ * the workspace (bevpool_forward_workspace_size bytes, float32 partial rows).
+ * The workspace contents are scratch: one forward at a time per workspace.
  */
+int bevpool_forward_workspace_size(const bevpool_shape* shape, size_t* bytes);
 int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
                     const void* depth, const void* feat,
                     const int32_t* ranks_depth, const int32_t* ranks_feat,
                     const int32_t* ranks_bev, const int32_t* interval_starts,
                     const int32_t* interval_lengths, int32_t n_valid,
-                    int32_t n_intervals, void* out, void* stream);
+                    int32_t n_intervals, void* out, void* workspace,
+                    size_t workspace_bytes, void* stream);
 
 /*
  * Gradients of bevpool_forward (not in the paper; chain rule):

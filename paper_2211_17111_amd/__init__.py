@@ -14,6 +14,7 @@ from .bevpool import (  # noqa: F401
     bevpool_backward,
     bevpool_backward_workspace_size,
     bevpool_forward,
+    bevpool_forward_workspace_size,
     bevpool_last_error,
     bevpool_prepare,
     bevpool_prepare_workspace_size,

@@ -64,8 +64,10 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_prepare.restype = ctypes.c_int
     lib.bevpool_prepare.argtypes = [shp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
     lib.bevpool_forward.restype = ctypes.c_int
+    lib.bevpool_forward_workspace_size.restype = ctypes.c_int
+    lib.bevpool_forward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_forward.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp,
-                                    i32, i32, vp, vp]
+                                    i32, i32, vp, vp, sz, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -146,15 +148,24 @@ def bevpool_prepare(shape, coor, ranks_depth, ranks_feat, ranks_bev, interval_st
            "bevpool_prepare")
 
 
+def bevpool_forward_workspace_size(shape) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib, lib.bevpool_forward_workspace_size(ctypes.byref(make_shape(shape)), ctypes.byref(n)),
+           "bevpool_forward_workspace_size")
+    return n.value
+
+
 def bevpool_forward(shape, in_dtype, out_dtype, depth, feat, ranks_depth, ranks_feat, ranks_bev,
-                    interval_starts, interval_lengths, n_valid, n_intervals, out,
-                    stream=None) -> None:
+                    interval_starts, interval_lengths, n_valid, n_intervals, out, workspace,
+                    workspace_bytes, stream=None) -> None:
     lib = load_library()
     s = make_shape(shape)
     _check(lib, lib.bevpool_forward(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
                                     _ptr(feat), _ptr(ranks_depth), _ptr(ranks_feat), _ptr(ranks_bev),
                                     _ptr(interval_starts), _ptr(interval_lengths), int(n_valid),
-                                    int(n_intervals), _ptr(out), _stream(stream)),
+                                    int(n_intervals), _ptr(out), _ptr(workspace), int(workspace_bytes),
+                                    _stream(stream)),
            "bevpool_forward")
 
 
@@ -231,7 +242,8 @@ def prepare(coor: torch.Tensor, shape, stream=None) -> Plan:
 
 
 def forward(depth: torch.Tensor, feat: torch.Tensor, plan: Plan, out_dtype=None,
-            out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+            out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+            stream=None) -> torch.Tensor:
     sd = plan.shape
     B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
     _require(depth, "depth")
@@ -244,9 +256,12 @@ def forward(depth: torch.Tensor, feat: torch.Tensor, plan: Plan, out_dtype=None,
     if out is None:
         out = torch.empty((B, Z, Y, X, C), dtype=odt, device=depth.device)
     _require(out, "out", odt)
+    if workspace is None:
+        workspace = torch.empty(bevpool_forward_workspace_size(sd), dtype=torch.uint8, device=depth.device)
     bevpool_forward(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, plan.ranks_depth,
                     plan.ranks_feat, plan.ranks_bev, plan.interval_starts, plan.interval_lengths,
-                    plan.n_valid, plan.n_intervals, out, stream)
+                    plan.n_valid, plan.n_intervals, out, workspace,
+                    workspace.numel() * workspace.element_size(), stream)
     return out
 
 

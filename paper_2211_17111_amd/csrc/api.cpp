@@ -144,11 +144,20 @@ int bevpool_prepare(const bevpool_shape* shape, const int32_t* coor, int32_t* ra
                   "bevpool_prepare");
 }
 
+int bevpool_forward_workspace_size(const bevpool_shape* shape, size_t* bytes) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(bytes);
+  *bytes = bevpool::forward_workspace_bytes(d);
+  return ok();
+}
+
 int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype, const void* depth,
                     const void* feat, const int32_t* ranks_depth, const int32_t* ranks_feat,
                     const int32_t* ranks_bev, const int32_t* interval_starts,
                     const int32_t* interval_lengths, int32_t n_valid, int32_t n_intervals,
-                    void* out, void* stream) {
+                    void* out, void* workspace, size_t workspace_bytes, void* stream) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);
   if (st != BEVPOOL_OK) return st;
@@ -170,9 +179,13 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype, con
     REQUIRE_PTR(interval_starts);
     REQUIRE_PTR(interval_lengths);
   }
+  const size_t need = bevpool::forward_workspace_bytes(d);
+  if (workspace == nullptr || workspace_bytes < need)
+    return fail(BEVPOOL_EWORKSPACE, "forward needs %zu workspace bytes, got %zu at %p", need,
+                workspace_bytes, workspace);
   return from_hip(bevpool::launch_forward(d, in_dtype, out_dtype, depth, feat, ranks_depth,
                                           ranks_feat, ranks_bev, interval_starts,
-                                          interval_lengths, n_valid, n_intervals, out,
+                                          interval_lengths, n_valid, n_intervals, out, workspace,
                                           static_cast<hipStream_t>(stream)),
                   "bevpool_forward");
 }

@@ -48,10 +48,12 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
                           hipStream_t stream);
 
 // ---- forward ---------------------------------------------------------------
+size_t forward_workspace_bytes(const Dims& d);
 hipError_t launch_forward(const Dims& d, int in_dtype, int out_dtype, const void* depth,
                           const void* feat, const int32_t* rd, const int32_t* rf,
                           const int32_t* rb, const int32_t* starts, const int32_t* lengths,
-                          int32_t n_valid, int32_t n_intervals, void* out, hipStream_t stream);
+                          int32_t n_valid, int32_t n_intervals, void* out, void* workspace,
+                          hipStream_t stream);
 
 // ---- backward --------------------------------------------------------------
 size_t backward_workspace_bytes(const Dims& d);

@@ -30,6 +30,7 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == {
         "bevpool_version", "bevpool_strerror", "bevpool_last_error",
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
+        "bevpool_forward_workspace_size",
         "bevpool_backward_workspace_size", "bevpool_backward",
     }
     for n in names:
@@ -76,9 +77,13 @@ def test_overflow_rejected(lib):
     assert lib.bevpool_prepare_workspace_size(ctypes.byref(out_over), ctypes.byref(n)) == EOVERFLOW
 
 
-def _fwd(lib, s, in_dt=0, out_dt=0, nv=100, ni=10, ptrs=None, out=DUMMY):
+def _fwd(lib, s, in_dt=0, out_dt=0, nv=100, ni=10, ptrs=None, out=DUMMY, ws=DUMMY, wsb=None):
     p = ptrs or [DUMMY] * 7
-    return lib.bevpool_forward(ctypes.byref(s), in_dt, out_dt, *p, nv, ni, out, None)
+    if wsb is None:
+        n = ctypes.c_size_t()
+        lib.bevpool_forward_workspace_size(ctypes.byref(s), ctypes.byref(n))
+        wsb = n.value
+    return lib.bevpool_forward(ctypes.byref(s), in_dt, out_dt, *p, nv, ni, out, ws, wsb, None)
 
 
 def test_forward_validation(lib):
@@ -97,7 +102,12 @@ def test_forward_validation(lib):
         ptrs[k] = None
         assert _fwd(lib, s, ptrs=ptrs) == EINVAL
         assert b"is NULL" in lib.bevpool_last_error()
-    assert lib.bevpool_forward(None, 0, 0, *([DUMMY] * 7), 1, 1, DUMMY, None) == EINVAL
+    assert lib.bevpool_forward(None, 0, 0, *([DUMMY] * 7), 1, 1, DUMMY, DUMMY, 1 << 30, None) == EINVAL
+    assert _fwd(lib, s, ws=None) == EWORKSPACE
+    n = ctypes.c_size_t()
+    assert lib.bevpool_forward_workspace_size(ctypes.byref(s), ctypes.byref(n)) == OK
+    assert n.value > 0
+    assert _fwd(lib, s, wsb=n.value - 1) == EWORKSPACE
 
 
 def test_prepare_validation(lib):
