@@ -132,19 +132,35 @@ def main():
     ocode = bp.BEVPOOL_F32 if cfg.out_dtype == "f32" else bp.BEVPOOL_F16
     stream = torch.cuda.current_stream()
 
-    def prepare(s):
+    def plan(s):
         bp.bevpool_prepare(shape, s.coor, s.rd, s.rf, s.rb, s.st, s.ln, s.counts, ws_p, ws_p_bytes, stream)
 
     # plans for every set; counts are fixed by the geometry
     for s in sets:
-        prepare(s)
+        plan(s)
     torch.cuda.synchronize()
     nv, ni = (int(v) for v in sets[0].counts.cpu().tolist())
     for s in sets:
         assert s.counts.cpu().tolist() == [nv, ni]
     log(f"n_valid={nv} n_intervals={ni}")
+    sched_bytes, ws_s_bytes = bp.bevpool_schedule_size(shape, nv, ni)
+    ws_s = torch.empty(ws_s_bytes, dtype=torch.uint8, device=dev)
+    for s in sets:
+        s.sched = torch.empty(sched_bytes, dtype=torch.uint8, device=dev)
+
+    def prepare(s):
+        plan(s)
+        bp.bevpool_schedule(shape, s.rd, s.rb, nv, ni, s.sched, sched_bytes, ws_s, ws_s_bytes, stream)
+
+    for s in sets:
+        prepare(s)
+    torch.cuda.synchronize()
 
     def forward(s):
+        bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, nv, ni,
+                                     s.out, stream)
+
+    def forward_ranges(s):
         bp.bevpool_forward(shape, code, ocode, s.depth, s.feat, s.rd, s.rf, s.rb, s.st, s.ln, nv, ni,
                            s.out, ws_f, ws_f_bytes, stream)
 
@@ -185,22 +201,35 @@ def main():
         f"bwd {bwd_ms:.4f}")
 
     # ---- cold forward latency (the metric) --------------------------------
-    def timed_forwards(n, pick):
+    def timed_forwards(n, pick, fn=forward):
+        """Per-launch event pairs and the whole back-to-back region."""
         starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
         ends = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
         for i in range(min(n, 16)):
-            forward(pick(i))
+            fn(pick(i))
         torch.cuda.synchronize()
         for i in range(n):
             s = pick(i)
             starts[i].record(stream)
-            forward(s)
+            fn(s)
             ends[i].record(stream)
         torch.cuda.synchronize()
-        return np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
+        per = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
+        r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        r0.record(stream)
+        for i in range(n):
+            fn(pick(i))
+        r1.record(stream)
+        torch.cuda.synchronize()
+        return per, r0.elapsed_time(r1) / n
 
-    cold = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)])
-    warm = timed_forwards(max(64, args.fwd_launches // 4), lambda i: sets[0])
+    cold, cold_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)])
+    warm, warm_region = timed_forwards(max(64, args.fwd_launches // 4), lambda i: sets[0])
+    cold_rng, cold_rng_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)],
+                                               forward_ranges)
+    log(f"forward back-to-back region: cold {cold_region * 1e3:.2f} us/launch, warm "
+        f"{warm_region * 1e3:.2f}; range-partition forward cold {cold_rng.mean() * 1e3:.2f} us "
+        f"(region {cold_rng_region * 1e3:.2f})")
     fwd_ms = float(cold.mean())
     min_bytes = forward_min_bytes(cfg, nv, ni)
     achieved = min_bytes / (fwd_ms * 1e-3) / 1e9
@@ -258,7 +287,11 @@ def main():
                                 "p50": float(np.median(cold)), "p90": float(np.percentile(cold, 90)),
                                 "launches": int(cold.size), "rotating_sets": len(sets),
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
+            "forward_cold_region_ms_per_launch": cold_region,
             "forward_warm_ms": float(warm.mean()),
+            "forward_warm_region_ms_per_launch": warm_region,
+            "forward_unscheduled_cold_ms": float(cold_rng.mean()),
+            "forward_unscheduled_cold_region_ms_per_launch": cold_rng_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
             "prepare_plus_forward_ms": prep_ms + fwd_in_step_ms, "step_wall_ms": wall_ms,
             "paper_context": "0.82 ms at 640x1600 (abstract), hardware not stated; 15.1x the previous "

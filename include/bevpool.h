@@ -153,6 +153,43 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
                     size_t workspace_bytes, void* stream);
 
 /*
+ * Forward schedule (optional, built once per plan like the plan itself).
+ *
+ * The schedule regroups the kept points of a plan by (cell, pixel): when
+ * several depth bins of one pixel fall into the same cell, their depth scores
+ * are summed first and the pixel's feature row is read once.  It also cuts
+ * the regrouped points into work items that each own whole cells, splitting
+ * a large task into channel slices instead of point ranges, so the scheduled
+ * forward needs no cross-item reduction.
+ *
+ * bevpool_schedule_size gives the schedule buffer size and the build
+ * workspace size for a plan with n_valid kept points and n_intervals
+ * occupied cells.  bevpool_schedule reads the first n_valid entries of
+ * ranks_depth and ranks_bev of a plan from bevpool_prepare and writes the
+ * schedule (device memory owned by the caller; opaque layout).  Enqueued on
+ * `stream`; deterministic.
+ *
+ * bevpool_forward_scheduled computes exactly what bevpool_forward computes
+ * (same layouts, dtypes and zero-filled empty cells, every element written
+ * once, no atomics, bitwise reproducible) from the schedule alone; n_valid
+ * and n_intervals must be the values the schedule was built with.  It needs
+ * no workspace and leaves the schedule unchanged, so concurrent forwards may
+ * share one schedule.  A schedule whose cell count does not match n_intervals
+ * leaves `out` unwritten.
+ */
+int bevpool_schedule_size(const bevpool_shape* shape, int32_t n_valid,
+                          int32_t n_intervals, size_t* schedule_bytes,
+                          size_t* workspace_bytes);
+int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
+                     const int32_t* ranks_bev, int32_t n_valid, int32_t n_intervals,
+                     void* schedule, size_t schedule_bytes, void* workspace,
+                     size_t workspace_bytes, void* stream);
+int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                              const void* depth, const void* feat, const void* schedule,
+                              size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                              void* out, void* stream);
+
+/*
  * Gradients of bevpool_forward (not in the paper; chain rule):
  *   grad_depth[p]  = sum_c grad_out[rank_bev(p), c] * feat[rank_feat(p), c]
  *                    for a kept point p, and +0.0 for a dropped point;

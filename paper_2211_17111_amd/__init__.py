@@ -9,19 +9,25 @@ from .bevpool import (  # noqa: F401
     BEVPOOL_F32,
     BevpoolError,
     Plan,
+    Schedule,
     backward,
     bev_pool,
     bevpool_backward,
     bevpool_backward_workspace_size,
     bevpool_forward,
+    bevpool_forward_scheduled,
     bevpool_forward_workspace_size,
     bevpool_last_error,
     bevpool_prepare,
     bevpool_prepare_workspace_size,
+    bevpool_schedule,
+    bevpool_schedule_size,
     bevpool_strerror,
     bevpool_version,
     declared_symbols,
     forward,
+    forward_scheduled,
     load_library,
     prepare,
+    schedule,
 )

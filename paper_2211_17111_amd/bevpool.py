@@ -68,6 +68,13 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_forward.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, vp, vp,
                                     i32, i32, vp, vp, sz, vp]
+    lib.bevpool_schedule_size.restype = ctypes.c_int
+    lib.bevpool_schedule_size.argtypes = [shp, i32, i32, ctypes.POINTER(sz), ctypes.POINTER(sz)]
+    lib.bevpool_schedule.restype = ctypes.c_int
+    lib.bevpool_schedule.argtypes = [shp, vp, vp, i32, i32, vp, sz, vp, sz, vp]
+    lib.bevpool_forward_scheduled.restype = ctypes.c_int
+    lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
+                                              vp, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -169,6 +176,36 @@ def bevpool_forward(shape, in_dtype, out_dtype, depth, feat, ranks_depth, ranks_
            "bevpool_forward")
 
 
+def bevpool_schedule_size(shape, n_valid, n_intervals) -> tuple[int, int]:
+    lib = load_library()
+    a, b = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    _check(lib, lib.bevpool_schedule_size(ctypes.byref(make_shape(shape)), int(n_valid), int(n_intervals),
+                                          ctypes.byref(a), ctypes.byref(b)),
+           "bevpool_schedule_size")
+    return a.value, b.value
+
+
+def bevpool_schedule(shape, ranks_depth, ranks_bev, n_valid, n_intervals, schedule, schedule_bytes,
+                     workspace, workspace_bytes, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_schedule(ctypes.byref(s), _ptr(ranks_depth), _ptr(ranks_bev), int(n_valid),
+                                     int(n_intervals), _ptr(schedule), int(schedule_bytes),
+                                     _ptr(workspace), int(workspace_bytes), _stream(stream)),
+           "bevpool_schedule")
+
+
+def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
+                              n_valid, n_intervals, out, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_forward_scheduled(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
+                                              _ptr(feat), _ptr(schedule), int(schedule_bytes),
+                                              int(n_valid), int(n_intervals), _ptr(out),
+                                              _stream(stream)),
+           "bevpool_forward_scheduled")
+
+
 def bevpool_backward_workspace_size(shape) -> int:
     lib = load_library()
     n = ctypes.c_size_t(0)
@@ -262,6 +299,51 @@ def forward(depth: torch.Tensor, feat: torch.Tensor, plan: Plan, out_dtype=None,
                     plan.ranks_feat, plan.ranks_bev, plan.interval_starts, plan.interval_lengths,
                     plan.n_valid, plan.n_intervals, out, workspace,
                     workspace.numel() * workspace.element_size(), stream)
+    return out
+
+
+@dataclass
+class Schedule:
+    """Device buffer of a forward schedule built from a plan."""
+    plan: Plan
+    buffer: torch.Tensor
+
+    def header(self) -> list[int]:
+        """Counts the schedule recorded: pairs, tasks, items, n_valid, cells, cells found."""
+        return self.buffer[:64].view(torch.int32)[:8].cpu().tolist()
+
+
+def schedule(plan: Plan, stream=None) -> Schedule:
+    """Build the forward schedule of a plan on the GPU (checks its counts)."""
+    sb, wb = bevpool_schedule_size(plan.shape, plan.n_valid, plan.n_intervals)
+    dev = plan.ranks_depth.device
+    buf = torch.empty(max(sb, 1), dtype=torch.uint8, device=dev)
+    ws = torch.empty(max(wb, 1), dtype=torch.uint8, device=dev)
+    bevpool_schedule(plan.shape, plan.ranks_depth, plan.ranks_bev, plan.n_valid, plan.n_intervals,
+                     buf, sb, ws, wb, stream)
+    sch = Schedule(plan, buf)
+    if plan.n_valid > 0:
+        hdr = sch.header()
+        if hdr[3] != plan.n_valid or hdr[5] != plan.n_intervals:
+            raise BevpoolError(-1, "bevpool_schedule", f"schedule counts {hdr} do not match the plan")
+    return sch
+
+
+def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, out_dtype=None,
+                      out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+    plan = sched.plan
+    sd = plan.shape
+    B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
+    _require(depth, "depth")
+    _require(feat, "feat", depth.dtype)
+    if tuple(depth.shape) != (B, N, D, H, W) or tuple(feat.shape) != (B, N, H, W, C):
+        raise ValueError("depth/feat shapes do not match the plan")
+    odt = out_dtype or depth.dtype
+    if out is None:
+        out = torch.empty((B, Z, Y, X, C), dtype=odt, device=depth.device)
+    _require(out, "out", odt)
+    bevpool_forward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, sched.buffer,
+                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, out, stream)
     return out
 
 

@@ -190,6 +190,84 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype, con
                   "bevpool_forward");
 }
 
+static int check_counts(const bevpool::Dims& d, int32_t n_valid, int32_t n_intervals) {
+  if (n_valid < 0 || n_valid > d.P)
+    return fail(BEVPOOL_EINVAL, "n_valid = %d outside [0, %lld]", n_valid, (long long)d.P);
+  const int64_t cap = d.P < d.cells ? d.P : d.cells;
+  if (n_intervals < 0 || n_intervals > cap || n_intervals > n_valid ||
+      (n_valid > 0 && n_intervals == 0))
+    return fail(BEVPOOL_EINVAL, "n_intervals = %d inconsistent with n_valid = %d (cells %lld)",
+                n_intervals, n_valid, (long long)d.cells);
+  return BEVPOOL_OK;
+}
+
+int bevpool_schedule_size(const bevpool_shape* shape, int32_t n_valid, int32_t n_intervals,
+                          size_t* schedule_bytes, size_t* workspace_bytes) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_counts(d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(schedule_bytes);
+  REQUIRE_PTR(workspace_bytes);
+  const bevpool::ScheduleLayout L = bevpool::schedule_layout(d, n_valid, n_intervals);
+  *schedule_bytes = L.total;
+  *workspace_bytes = L.ws_total;
+  return ok();
+}
+
+int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
+                     const int32_t* ranks_bev, int32_t n_valid, int32_t n_intervals,
+                     void* schedule, size_t schedule_bytes, void* workspace,
+                     size_t workspace_bytes, void* stream) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_counts(d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
+  if (n_valid > 0) {
+    REQUIRE_PTR(ranks_depth);
+    REQUIRE_PTR(ranks_bev);
+  }
+  REQUIRE_PTR(schedule);
+  const bevpool::ScheduleLayout L = bevpool::schedule_layout(d, n_valid, n_intervals);
+  if (schedule_bytes < L.total)
+    return fail(BEVPOOL_EINVAL, "schedule needs %zu bytes, got %zu", L.total, schedule_bytes);
+  if (workspace == nullptr || workspace_bytes < L.ws_total)
+    return fail(BEVPOOL_EWORKSPACE, "schedule build needs %zu workspace bytes, got %zu at %p",
+                L.ws_total, workspace_bytes, workspace);
+  return from_hip(bevpool::launch_schedule(d, ranks_depth, ranks_bev, n_valid, n_intervals,
+                                           schedule, workspace, static_cast<hipStream_t>(stream)),
+                  "bevpool_schedule");
+}
+
+int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                              const void* depth, const void* feat, const void* schedule,
+                              size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                              void* out, void* stream) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_dtypes(in_dtype, out_dtype);
+  if (st != BEVPOOL_OK) return st;
+  st = check_counts(d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(out);
+  if (n_intervals > 0) {
+    REQUIRE_PTR(depth);
+    REQUIRE_PTR(feat);
+    REQUIRE_PTR(schedule);
+    const size_t need = bevpool::schedule_layout(d, n_valid, n_intervals).total;
+    if (schedule_bytes < need)
+      return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
+                  schedule_bytes, need);
+  }
+  return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, depth, feat, schedule,
+                                                    n_valid, n_intervals, out,
+                                                    static_cast<hipStream_t>(stream)),
+                  "bevpool_forward_scheduled");
+}
+
 int bevpool_backward_workspace_size(const bevpool_shape* shape, size_t* bytes) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);

@@ -93,8 +93,12 @@ __global__ __launch_bounds__(kFwdThreads) void k_fwd_ranges(const TIn* __restric
   const int g = lane / cvc;
   const int vi = lane - g * cvc;
 
-  // this wave's points: ranges w*G .. w*G+G-1
-  const int64_t w = (int64_t)blockIdx.x * kFwdWaves + wid;
+  // this wave's points: ranges w*G .. w*G+G-1.  Workgroup b runs on die
+  // b % kXcds; consecutive blocks of ranges are given to the same die so its
+  // L2 holds the feature rows of one region of the grid.
+  const int64_t per_die = gridDim.x / kXcds;
+  const int64_t lb = (int64_t)(blockIdx.x % kXcds) * per_die + blockIdx.x / kXcds;
+  const int64_t w = lb * kFwdWaves + wid;
   const int64_t wb = w * G * RG;
   if (wb >= a.n_valid) return;
   const int wn = (int)min<int64_t>((int64_t)G * RG, a.n_valid - wb);
@@ -257,9 +261,11 @@ hipError_t run(const Dims& d, const void* depth, const void* feat, FwdArgs a, vo
   const int64_t G = kWave / (CV < kWave ? CV : kWave);
   const int64_t n_ranges = (a.n_valid + a.RG - 1) / a.RG;
   const int64_t waves = (n_ranges + G - 1) / G;
+  const int64_t blocks = (waves + kFwdWaves - 1) / kFwdWaves;
+  const int64_t padded = ((blocks + kXcds - 1) / kXcds) * kXcds;  // surplus blocks exit
   k_fwd_ranges<TIn, TOut, VEC>
-      <<<dim3((unsigned)((waves + kFwdWaves - 1) / kFwdWaves), chunks), dim3(kFwdThreads), 0,
-         stream>>>(static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
+      <<<dim3((unsigned)padded, chunks), dim3(kFwdThreads), 0, stream>>>(
+          static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
   const int64_t cwaves = (a.n_intervals + G - 1) / G;
   k_fwd_cells<TOut, VEC>
       <<<dim3((unsigned)((cwaves + kFwdWaves - 1) / kFwdWaves), chunks), dim3(kFwdThreads), 0,

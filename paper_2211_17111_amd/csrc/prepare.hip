@@ -11,6 +11,8 @@
 // contiguous run of 1024 elements so lane order within a round and round
 // order within a wave both follow the element order.
 
+#include <algorithm>
+
 #include "device_utils.h"
 #include "internal.h"
 
@@ -331,7 +333,286 @@ __global__ __launch_bounds__(256) void k_interval_lengths(const int32_t* __restr
   }
 }
 
+// ------------------------------------------------------------------ schedule
+//
+// The forward schedule regroups the kept points of a plan by (cell, pixel):
+// several depth bins of one pixel often land in the same cell, and their
+// depth scores can be summed before the pixel's feature row is read once.
+// The regrouping is two more stable radix sorts of the plan (by feature rank,
+// then by BEV rank), after which runs of equal (BEV rank, feature rank) are
+// "pairs".  Pairs are then cut into tasks that own whole cells: task k owns
+// the cells whose first pair lies in [k*T, (k+1)*T).  A task with more than T
+// pairs is further split by channels into several work items, which need no
+// cross-item reduction because channels are independent.
+
+// Generic ordered compaction over the same 4096-element tiles as the filter:
+// Op provides count(), flag(i), visit(i) (called for every i < count) and
+// emit(i, position) (called for flagged i, positions in index order).
+template <class Op>
+__global__ __launch_bounds__(kPrepThreads) void k_compact_count(Op op, int32_t* __restrict__ tile_counts) {
+  __shared__ int wave_tot[kWavesPerTile];
+  const int64_t n = op.count();
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const int64_t base = (int64_t)blockIdx.x * kPrepTile + (int64_t)wid * kWaveSpan;
+  int cnt = 0;
+#pragma unroll 4
+  for (int r = 0; r < kPrepRounds; ++r) {
+    const int64_t i = base + r * kWave + lane;
+    cnt += __popcll(wave_ballot(i < n && op.flag(i)));
+  }
+  if (lane == 0) wave_tot[wid] = cnt;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int t = 0;
+    for (int w = 0; w < kWavesPerTile; ++w) t += wave_tot[w];
+    tile_counts[blockIdx.x] = t;
+  }
+}
+
+template <class Op>
+__global__ __launch_bounds__(kPrepThreads) void k_compact_scatter(Op op,
+                                                                  const int32_t* __restrict__ tile_offsets) {
+  __shared__ int wave_tot[kWavesPerTile];
+  const int64_t n = op.count();
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const int64_t base = (int64_t)blockIdx.x * kPrepTile + (int64_t)wid * kWaveSpan;
+  uint32_t flags = 0;
+  int cnt = 0;
+#pragma unroll
+  for (int r = 0; r < kPrepRounds; ++r) {
+    const int64_t i = base + r * kWave + lane;
+    const bool f = i < n && op.flag(i);
+    if (i < n) op.visit(i);
+    flags |= (uint32_t)f << r;
+    cnt += __popcll(wave_ballot(f));
+  }
+  if (lane == 0) wave_tot[wid] = cnt;
+  __syncthreads();
+  int off = tile_offsets[blockIdx.x];
+  for (int w = 0; w < wid; ++w) off += wave_tot[w];
+#pragma unroll
+  for (int r = 0; r < kPrepRounds; ++r) {
+    const bool f = (flags >> r) & 1u;
+    const uint64_t m = wave_ballot(f);
+    if (f) op.emit(base + r * kWave + lane, off + rank_below(m));
+    off += __popcll(m);
+  }
+}
+
+__device__ __forceinline__ int32_t pixel_of(int32_t p, int64_t per_view, int64_t hw) {
+  return (int32_t)(((int64_t)p / per_view) * hw + (int64_t)p % hw);
+}
+
+struct PairHeads {  // runs of equal (BEV rank, pixel) with consecutive depth bins
+  const int32_t* rd;
+  const int32_t* rb;
+  const int32_t* vals;  // plan position of each regrouped point
+  const int32_t* hdr;
+  int64_t per_view, hw;
+  int32_t* pair_rd0;
+  int32_t* pair_cell;
+  int32_t* head_pos;   // regrouped position of each pair's first point
+  __device__ int64_t count() const { return hdr[kHdrValid]; }
+  __device__ bool flag(int64_t i) const {
+    if (i == 0) return true;
+    const int32_t a = vals[i], b = vals[i - 1];
+    const int32_t pa = rd[a], pb = rd[b];
+    return rb[a] != rb[b] || pixel_of(pa, per_view, hw) != pixel_of(pb, per_view, hw) ||
+           (int64_t)pa != (int64_t)pb + hw;
+  }
+  __device__ void visit(int64_t) const {}
+  __device__ void emit(int64_t i, int32_t pos) const {
+    const int32_t a = vals[i];
+    pair_rd0[pos] = rd[a];
+    pair_cell[pos] = rb[a];
+    head_pos[pos] = (int32_t)i;
+  }
+};
+
+struct CellHeads {  // first pair of every occupied cell
+  const int32_t* pair_cell;
+  const int32_t* hdr;
+  int32_t* cell_id;
+  int32_t* cell_pair;
+  int32_t cap;  // occupied cells the plan declares (n_intervals)
+  __device__ int64_t count() const { return hdr[kHdrPairs]; }
+  __device__ bool flag(int64_t k) const { return k == 0 || pair_cell[k] != pair_cell[k - 1]; }
+  __device__ void visit(int64_t) const {}
+  __device__ void emit(int64_t k, int32_t pos) const {
+    if (pos >= cap) return;  // plan inconsistent with n_intervals: never write past the arrays
+    cell_pair[pos] = (int32_t)k;
+    cell_id[pos] = pair_cell[k];
+  }
+};
+
+__global__ void k_sched_init(int32_t* __restrict__ hdr, int32_t n_valid, int32_t n_occ) {
+  if (threadIdx.x < 16) hdr[threadIdx.x] = 0;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    hdr[kHdrValid] = n_valid;
+    hdr[kHdrOcc] = n_occ;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sched_rf_keys(const int32_t* __restrict__ rd, int64_t n,
+                                                       int64_t per_view, int64_t hw,
+                                                       int32_t* __restrict__ keys,
+                                                       int32_t* __restrict__ vals) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) {
+    keys[i] = pixel_of(rd[i], per_view, hw);
+    vals[i] = (int32_t)i;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_sched_rb_keys(const int32_t* __restrict__ rb,
+                                                       const int32_t* __restrict__ vals, int64_t n,
+                                                       int32_t* __restrict__ keys) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) keys[i] = rb[vals[i]];
+}
+
+__global__ void k_sched_sentinels(int32_t* __restrict__ hdr, int32_t* __restrict__ head_pos,
+                                  int32_t* __restrict__ cell_pair) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) {
+    const int32_t np = hdr[kHdrPairs];
+    head_pos[np] = hdr[kHdrValid];
+    cell_pair[min(hdr[kHdrOcc], hdr[kHdrOccFound])] = np;
+    hdr[kHdrTasks] = (np + kSchedTaskPairs - 1) / kSchedTaskPairs;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_pair_npts(const int32_t* __restrict__ head_pos,
+                                                   const int32_t* __restrict__ hdr,
+                                                   int32_t* __restrict__ pair_npts) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k < hdr[kHdrPairs]) pair_npts[k] = head_pos[k + 1] - head_pos[k];
+}
+
+// task_cell[k] = first occupied cell whose first pair is >= k*T.  Nothing
+// is written when the plan's cell count disagrees with what was found.
+__global__ __launch_bounds__(256) void k_sched_tasks(const int32_t* __restrict__ cell_pair,
+                                                     const int32_t* __restrict__ hdr, int32_t n_occ,
+                                                     int32_t* __restrict__ task_cell) {
+  if (hdr[kHdrOccFound] != n_occ) return;
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int32_t T = kSchedTaskPairs;
+  const int32_t n_tasks = hdr[kHdrTasks];
+  if (j == 0) task_cell[0] = 0;
+  if (j >= 1 && j < n_occ) {
+    const int32_t hi = min(cell_pair[j] / T, n_tasks);
+    for (int32_t k = max(cell_pair[j - 1] / T + 1, 1); k <= hi; ++k) task_cell[k] = (int32_t)j;
+  } else if (j == n_occ && n_occ > 0) {
+    for (int32_t k = max(cell_pair[n_occ - 1] / T + 1, 1); k <= n_tasks; ++k) task_cell[k] = n_occ;
+  }
+}
+
+__device__ __forceinline__ int32_t task_chunks(const int32_t* cell_pair, const int32_t* task_cell,
+                                               int64_t k, int max_chunks) {
+  const int32_t w = cell_pair[task_cell[k + 1]] - cell_pair[task_cell[k]];
+  if (w <= 0) return 0;
+  const int32_t c = (w + kSchedTaskPairs - 1) / kSchedTaskPairs;
+  return c < max_chunks ? c : max_chunks;
+}
+
+__global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ cell_pair,
+                                                     const int32_t* __restrict__ task_cell,
+                                                     const int32_t* __restrict__ hdr, int64_t cap,
+                                                     int max_chunks, int32_t* __restrict__ count) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= cap) return;
+  const bool ok = hdr[kHdrOccFound] == hdr[kHdrOcc] && k < hdr[kHdrTasks];
+  count[k] = ok ? task_chunks(cell_pair, task_cell, k, max_chunks) : 0;
+}
+
+// Items in task order; work[i] = pairs of the item's task / its chunk count.
+__global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ cell_pair,
+                                                      const int32_t* __restrict__ task_cell,
+                                                      int32_t* __restrict__ hdr, int max_chunks,
+                                                      const int32_t* __restrict__ offset,
+                                                      int32_t* __restrict__ item_info,
+                                                      int32_t* __restrict__ item_chunk,
+                                                      int32_t* __restrict__ work) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (hdr[kHdrOccFound] != hdr[kHdrOcc] || k >= hdr[kHdrTasks]) return;
+  const int32_t K = task_chunks(cell_pair, task_cell, k, max_chunks);
+  if (K == 0) return;
+  const int32_t base = offset[k];
+  const int32_t cb = task_cell[k], ce = task_cell[k + 1];
+  const int32_t pb = cell_pair[cb], pe = cell_pair[ce];
+  for (int32_t c = 0; c < K; ++c) {
+    int32_t* info = item_info + 4 * (int64_t)(base + c);
+    info[0] = cb;
+    info[1] = ce;
+    info[2] = pb;
+    info[3] = pe;
+    item_chunk[base + c] = c | (K << 16);
+    work[base + c] = (pe - pb + K - 1) / K;
+  }
+}
+
+__global__ __launch_bounds__(256) void k_item_work_tail(const int32_t* __restrict__ hdr,
+                                                        int32_t* __restrict__ work, int64_t cap) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < cap && i >= hdr[kHdrItems]) work[i] = 0;
+}
+
+// xcd_begin[x] = first item whose exclusive work prefix reaches x/8 of the
+// total work, so each die gets a contiguous run of items of about equal work.
+// `cum` holds the exclusive prefix of the per-item work.
+__global__ __launch_bounds__(256) void k_xcd_bounds(const int32_t* __restrict__ cum,
+                                                    const int32_t* __restrict__ hdr,
+                                                    int32_t* __restrict__ xcd_begin) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t n = hdr[kHdrItems];
+  const int64_t total = hdr[kHdrWork];
+  if (i == 0) {
+    xcd_begin[0] = 0;
+    xcd_begin[kXcds] = (int32_t)n;
+    if (n == 0)
+      for (int x = 1; x < kXcds; ++x) xcd_begin[x] = 0;
+  }
+  if (i >= n) return;
+  const int64_t lo = i > 0 ? cum[i - 1] : -1;
+  const int64_t hi = cum[i];
+  for (int x = 1; x < kXcds; ++x) {
+    const int64_t b = (total * x + kXcds - 1) / kXcds;
+    if (lo < b && b <= hi) xcd_begin[x] = (int32_t)i;
+    if (i == n - 1 && b > hi) xcd_begin[x] = (int32_t)n;
+  }
+}
+
 inline size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
+
+// returns true when the sorted result ends in (k1, v1)
+bool radix_sort_pairs(int32_t* k0, int32_t* v0, int32_t* k1, int32_t* v1, const int32_t* n_ptr,
+                      int64_t ntiles, int key_bits, int32_t* hist, int32_t* sums,
+                      hipStream_t stream) {
+  const int passes = (key_bits + kMaxDigitBits - 1) / kMaxDigitBits;
+  const int digit_bits = (key_bits + passes - 1) / passes;
+  const dim3 grid((unsigned)ntiles), block(kPrepThreads);
+  for (int pass = 0; pass < passes; ++pass) {
+    const int shift = pass * digit_bits;
+    const int bits = (key_bits - shift) < digit_bits ? (key_bits - shift) : digit_bits;
+    int32_t* ik = (pass % 2 == 0) ? k0 : k1;
+    int32_t* iv = (pass % 2 == 0) ? v0 : v1;
+    int32_t* ok = (pass % 2 == 0) ? k1 : k0;
+    int32_t* ov = (pass % 2 == 0) ? v1 : v0;
+    k_radix_hist<<<grid, block, 0, stream>>>(ik, n_ptr, shift, 1 << bits, hist, ntiles);
+    scan_exclusive(hist, (int64_t(1) << bits) * ntiles, sums, nullptr, stream);
+    k_radix_scatter<<<grid, block, 0, stream>>>(ik, iv, ok, ov, nullptr, n_ptr, shift, bits, hist,
+                                                ntiles, 1, 1);
+  }
+  return passes % 2 == 1;
+}
+
+int bit_length(int64_t v) {
+  int b = 1;
+  while ((int64_t(1) << b) < v) ++b;
+  return b;
+}
 
 }  // namespace
 
@@ -409,6 +690,121 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
   const int64_t cap = d.P < d.cells ? d.P : d.cells;
   k_interval_lengths<<<dim3((unsigned)((cap + 255) / 256)), dim3(256), 0, stream>>>(starts, lengths,
                                                                                    counts);
+  return hipGetLastError();
+}
+
+}  // namespace bevpool
+
+namespace bevpool {
+
+int schedule_max_chunks(const Dims& d) { return (d.C % 16 == 0) ? (int)(d.C / 16) : 1; }
+
+ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals) {
+  ScheduleLayout L{};
+  L.n_valid = n_valid;
+  L.n_occ = n_intervals;
+  L.tasks_cap = (n_valid + kSchedTaskPairs - 1) / kSchedTaskPairs + 1;
+  L.items_cap = 2 * L.tasks_cap;
+  const size_t nv = (size_t)(n_valid > 0 ? n_valid : 1);
+  size_t off = 0;
+  auto take = [&](size_t n_ints) {
+    const size_t o = off;
+    off += align_up(sizeof(int32_t) * n_ints);
+    return o;
+  };
+  L.header = take(16);
+  L.pair_rd0 = take(nv);
+  L.pair_cell = take(nv);
+  L.pair_npts = take(nv);
+  L.cell_id = take((size_t)n_intervals + 1);
+  L.cell_pair = take((size_t)n_intervals + 1);
+  L.task_cell = take((size_t)L.tasks_cap + 1);
+  L.item_info = take(4 * (size_t)L.items_cap);
+  L.item_chunk = take((size_t)L.items_cap);
+  L.xcd_begin = take(kXcds + 1);
+  L.total = off;
+
+  L.ntiles = ((int64_t)nv + kPrepTile - 1) / kPrepTile;
+  const int64_t scan_n = std::max<int64_t>(256 * L.ntiles, L.items_cap);
+  L.nscan = (scan_n + kScanTile - 1) / kScanTile;
+  off = 0;
+  L.ws_keys_a = take(nv);
+  L.ws_vals_a = take(nv);
+  L.ws_head = take(nv + 1);
+  L.ws_keys_b = take(nv);
+  L.ws_vals_b = take(nv);
+  L.ws_tiles = take((size_t)std::max<int64_t>(L.ntiles, L.tasks_cap + L.items_cap) + 2);
+  L.ws_hist = take((size_t)(256 * L.ntiles));
+  L.ws_sums = take((size_t)L.nscan + 1);
+  L.ws_total = off;
+  L.rf_bits = bit_length(d.rows);
+  L.rb_bits = bit_length(d.cells);
+  return L;
+}
+
+hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
+                           int32_t n_intervals, void* schedule, void* workspace,
+                           hipStream_t stream) {
+  const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
+  char* sc = static_cast<char*>(schedule);
+  char* ws = static_cast<char*>(workspace);
+  auto S = [&](size_t o) { return reinterpret_cast<int32_t*>(sc + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<int32_t*>(ws + o); };
+  int32_t* hdr = S(L.header);
+  int32_t* tiles = W(L.ws_tiles);
+  int32_t* sums = W(L.ws_sums);
+
+  k_sched_init<<<1, 64, 0, stream>>>(hdr, n_valid, n_intervals);
+  if (n_valid == 0) return hipGetLastError();
+
+  // regroup by (BEV rank, feature rank, plan position)
+  const unsigned g256 = (unsigned)((n_valid + 255) / 256);
+  k_sched_rf_keys<<<g256, 256, 0, stream>>>(rd, n_valid, d.per_view, d.hw, W(L.ws_keys_a),
+                                            W(L.ws_vals_a));
+  const bool in_b = radix_sort_pairs(W(L.ws_keys_a), W(L.ws_vals_a), W(L.ws_keys_b), W(L.ws_vals_b),
+                                     hdr + kHdrValid, L.ntiles, L.rf_bits, W(L.ws_hist), sums, stream);
+  int32_t* k0 = in_b ? W(L.ws_keys_b) : W(L.ws_keys_a);
+  int32_t* v0 = in_b ? W(L.ws_vals_b) : W(L.ws_vals_a);
+  int32_t* k1 = in_b ? W(L.ws_keys_a) : W(L.ws_keys_b);
+  int32_t* v1 = in_b ? W(L.ws_vals_a) : W(L.ws_vals_b);
+  k_sched_rb_keys<<<g256, 256, 0, stream>>>(rb, v0, n_valid, k0);
+  const bool in_1 = radix_sort_pairs(k0, v0, k1, v1, hdr + kHdrValid, L.ntiles, L.rb_bits,
+                                     W(L.ws_hist), sums, stream);
+  const int32_t* vals = in_1 ? v1 : v0;
+
+  // pairs
+  const dim3 grid((unsigned)L.ntiles), block(kPrepThreads);
+  int32_t* head_pos = W(L.ws_head);
+  PairHeads ph{rd, rb, vals, hdr, d.per_view, d.hw, S(L.pair_rd0), S(L.pair_cell), head_pos};
+  k_compact_count<<<grid, block, 0, stream>>>(ph, tiles);
+  scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrPairs, stream);
+  k_compact_scatter<<<grid, block, 0, stream>>>(ph, tiles);
+
+  // occupied cells
+  CellHeads ch{S(L.pair_cell), hdr, S(L.cell_id), S(L.cell_pair), n_intervals};
+  k_compact_count<<<grid, block, 0, stream>>>(ch, tiles);
+  scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
+  k_compact_scatter<<<grid, block, 0, stream>>>(ch, tiles);
+  k_sched_sentinels<<<1, 64, 0, stream>>>(hdr, head_pos, S(L.cell_pair));
+  k_pair_npts<<<g256, 256, 0, stream>>>(head_pos, hdr, S(L.pair_npts));
+
+  // tasks, work items in task order, and the per-die item ranges
+  k_sched_tasks<<<(unsigned)((n_intervals + 1 + 255) / 256), 256, 0, stream>>>(
+      S(L.cell_pair), hdr, n_intervals, S(L.task_cell));
+  const int maxk = schedule_max_chunks(d);
+  int32_t* count = tiles;                 // [tasks_cap]: items per task, then their offsets
+  int32_t* work = tiles + L.tasks_cap;    // [items_cap]: work per item, then its prefix
+  const unsigned gt = (unsigned)((L.tasks_cap + 255) / 256);
+  k_item_counts<<<gt, 256, 0, stream>>>(S(L.cell_pair), S(L.task_cell), hdr, L.tasks_cap, maxk,
+                                        count);
+  scan_exclusive(count, L.tasks_cap, sums, hdr + kHdrItems, stream);
+  k_item_scatter<<<gt, 256, 0, stream>>>(S(L.cell_pair), S(L.task_cell), hdr, maxk, count,
+                                         S(L.item_info), S(L.item_chunk), work);
+  k_item_work_tail<<<(unsigned)((L.items_cap + 255) / 256), 256, 0, stream>>>(hdr, work,
+                                                                            L.items_cap);
+  scan_exclusive(work, L.items_cap, sums, hdr + kHdrWork, stream);
+  k_xcd_bounds<<<(unsigned)((L.items_cap + 255) / 256), 256, 0, stream>>>(work, hdr,
+                                                                        S(L.xcd_begin));
   return hipGetLastError();
 }
 

@@ -30,7 +30,8 @@ def test_exports_every_declared_symbol(lib):
     assert set(names) == {
         "bevpool_version", "bevpool_strerror", "bevpool_last_error",
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
-        "bevpool_forward_workspace_size",
+        "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
+        "bevpool_forward_scheduled",
         "bevpool_backward_workspace_size", "bevpool_backward",
     }
     for n in names:
@@ -146,3 +147,29 @@ def test_binding_raises_with_message(lib):
     with pytest.raises(bp.BevpoolError) as ei:
         bp.bevpool_prepare_workspace_size(dict(SHAPE, C=0))
     assert ei.value.status == EINVAL and "C" in str(ei.value)
+
+
+def test_schedule_validation(lib):
+    s = _shape()
+    sb, wb = ctypes.c_size_t(), ctypes.c_size_t()
+    assert lib.bevpool_schedule_size(ctypes.byref(s), 1000, 100, ctypes.byref(sb), ctypes.byref(wb)) == OK
+    assert sb.value > 4 * 1000 and wb.value > 4 * 4 * 1000
+    assert lib.bevpool_schedule_size(ctypes.byref(s), -1, 0, ctypes.byref(sb), ctypes.byref(wb)) == EINVAL
+    assert lib.bevpool_schedule_size(ctypes.byref(s), 10, 11, ctypes.byref(sb), ctypes.byref(wb)) == EINVAL
+    assert lib.bevpool_schedule_size(ctypes.byref(s), 10, 0, ctypes.byref(sb), ctypes.byref(wb)) == EINVAL
+    lib.bevpool_schedule_size(ctypes.byref(s), 1000, 100, ctypes.byref(sb), ctypes.byref(wb))
+    call = lambda **k: lib.bevpool_schedule(ctypes.byref(s), k.get("rd", DUMMY), k.get("rb", DUMMY), 1000, 100,
+                                            k.get("sc", DUMMY), k.get("sb", sb.value), k.get("ws", DUMMY),
+                                            k.get("wb", wb.value), None)
+    assert call(rd=None) == EINVAL
+    assert call(sc=None) == EINVAL
+    assert call(sb=sb.value - 1) == EINVAL
+    assert call(ws=None) == EWORKSPACE
+    assert call(wb=wb.value - 1) == EWORKSPACE
+    f = lambda **k: lib.bevpool_forward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0), DUMMY, DUMMY,
+                                                  k.get("sc", DUMMY), k.get("sb", sb.value), 1000, 100,
+                                                  k.get("out", DUMMY), None)
+    assert f(i=0, o=1) == EDTYPE
+    assert f(sc=None) == EINVAL
+    assert f(sb=16) == EINVAL
+    assert f(out=None) == EINVAL

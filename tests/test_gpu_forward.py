@@ -18,40 +18,54 @@ from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coo
 
 pytestmark = pytest.mark.gpu
 
+PATHS = ["ranges", "scheduled"]
 
-def _run(depth, feat, coor, shape, out_dtype=None):
+
+@pytest.fixture(params=PATHS)
+def path(request):
+    return request.param
+
+
+def _fwd(path, depth_t, feat_t, plan, out_dtype=None, out=None, sched=None):
+    if path == "scheduled":
+        sched = sched or bp.schedule(plan)
+        return bp.forward_scheduled(depth_t, feat_t, sched, out_dtype=out_dtype, out=out)
+    return bp.forward(depth_t, feat_t, plan, out_dtype=out_dtype, out=out)
+
+
+def _run(depth, feat, coor, shape, out_dtype=None, path="ranges"):
     plan = _gpu.run_prepare(coor, shape)
     odt = _gpu.torch_dtype(out_dtype) if out_dtype else None
-    out = bp.forward(_gpu.to_dev(depth), _gpu.to_dev(feat), plan, out_dtype=odt)
+    out = _fwd(path, _gpu.to_dev(depth), _gpu.to_dev(feat), plan, out_dtype=odt)
     torch.cuda.synchronize()
     return out, plan
 
 
 @pytest.mark.parametrize("name", ["tiny", "bevdet"])
-def test_forward_full(name):
+def test_forward_full(name, path):
     cfg = CONFIGS[name]
-    _gpu.say(f"forward full parity: {name}")
+    _gpu.say(f"forward full parity: {name} {path}")
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
-    out, _ = _run(data["depth"], data["feat"], coor, cfg.shape())
+    out, _ = _run(data["depth"], data["feat"], coor, cfg.shape(), path=path)
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
     _gpu.assert_within(out.cpu().numpy(), ref, mag, cfg.dtype, name)
 
 
 @pytest.mark.parametrize("C", [1, 3, 16, 17, 64, 80, 260])
 @pytest.mark.parametrize("dtype,out_dtype", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
-def test_forward_random_channels(C, dtype, out_dtype):
+def test_forward_random_channels(C, dtype, out_dtype, path):
     shape = dict(B=2, N=2, D=9, H=7, W=13, C=C, X=12, Y=10, Z=2)
     rng = np.random.default_rng(C)
     coor = random_coor(rng, shape, p_out=0.4)
     data = draw_small(rng, shape, dtype=dtype)
-    _gpu.say(f"forward random C={C} {dtype}->{out_dtype}")
-    out, _ = _run(data["depth"], data["feat"], coor, shape, out_dtype)
+    _gpu.say(f"forward random C={C} {dtype}->{out_dtype} {path}")
+    out, _ = _run(data["depth"], data["feat"], coor, shape, out_dtype, path=path)
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
     _gpu.assert_within(out.float().cpu().numpy(), ref, mag, dtype, f"C={C} {dtype}->{out_dtype}")
 
 
-def test_forward_misaligned_takes_scalar_path():
+def test_forward_misaligned_takes_scalar_path(path):
     shape = dict(B=1, N=2, D=6, H=5, W=9, C=8, X=6, Y=6, Z=1)
     rng = np.random.default_rng(1)
     coor = random_coor(rng, shape)
@@ -63,13 +77,13 @@ def test_forward_misaligned_takes_scalar_path():
     feat.copy_(torch.from_numpy(data["feat"]))
     obuf = torch.empty(1 * 6 * 6 * 8 + 1, dtype=torch.float32, device=_gpu.DEV)
     out = obuf[1:].view(1, 1, 6, 6, 8)
-    bp.forward(_gpu.to_dev(data["depth"]), feat, plan, out=out)
+    _fwd(path, _gpu.to_dev(data["depth"]), feat, plan, out=out)
     torch.cuda.synchronize()
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
     _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", "misaligned")
 
 
-def test_forward_edge_cases():
+def test_forward_edge_cases(path):
     shape = dict(B=1, N=1, D=8, H=50, W=60, C=80, X=8, Y=8, Z=1)   # P = 24000
     P = 24000
     rng = np.random.default_rng(2)
@@ -83,22 +97,22 @@ def test_forward_edge_cases():
                                         np.array([[3, 3, 0]], dtype=np.int32)]),
     }
     for label, coor in cases.items():
-        _gpu.say(f"forward edge case: {label}")
-        out, _ = _run(data["depth"], data["feat"], coor, shape)
+        _gpu.say(f"forward edge case: {label} {path}")
+        out, _ = _run(data["depth"], data["feat"], coor, shape, path=path)
         ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
         _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", label)
         occupied = mag.reshape(-1, 80).any(axis=1)
         assert np.all(out.cpu().numpy().reshape(-1, 80)[~occupied] == 0.0), label
 
 
-def test_forward_nan_free_and_empty_exact_zero():
+def test_forward_nan_free_and_empty_exact_zero(path):
     # Poison the output buffer first: every element must be overwritten.
     cfg = CONFIGS["bevdet"]
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
     plan = _gpu.run_prepare(coor, cfg.shape())
     out = torch.full((1, 1, 128, 128, 64), float("nan"), device=_gpu.DEV)
-    bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan, out=out)
+    _fwd(path, _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan, out=out)
     o = out.cpu().numpy().reshape(-1, 64)
     assert np.isfinite(o).all()
     occ = np.zeros(o.shape[0], dtype=bool)
@@ -119,12 +133,12 @@ def _sample_cells(plan, cells, rng, k=120):
 
 
 @pytest.mark.parametrize("name", ["headline", "large", "train"])
-def test_forward_full_size_sampled(name):
+def test_forward_full_size_sampled(name, path):
     cfg = CONFIGS[name]
-    _gpu.say(f"forward sampled parity: {name}")
+    _gpu.say(f"forward sampled parity: {name} {path}")
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg, with_grad=False)
-    out, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), cfg.out_dtype)
+    out, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), cfg.out_dtype, path=path)
     rng = np.random.default_rng(7)
     cells = _sample_cells(plan, cfg.cells, rng)
     ref, mag = oracle.forward_cells_ref(data["depth"], data["feat"], coor, cfg.shape(), cells)
@@ -140,14 +154,14 @@ def test_forward_full_size_sampled(name):
     _gpu.assert_within(total, mass, absmass, cfg.dtype, f"{name} mass")
 
 
-def test_forward_deterministic_and_batch_consistent():
+def test_forward_deterministic_and_batch_consistent(path):
     cfg = CONFIGS["large"]
-    _gpu.say("forward determinism + batch consistency: large")
+    _gpu.say(f"forward determinism + batch consistency: large {path}")
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg, with_grad=False)
-    out1, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), "f32")
-    out2 = bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan,
-                      out_dtype=torch.float32)
+    out1, plan = _run(data["depth"], data["feat"], coor, cfg.shape(), "f32", path=path)
+    out2 = _fwd(path, _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan,
+                out_dtype=torch.float32)
     assert torch.equal(out1, out2)   # bitwise reproducible run to run
     # Sample 0 of the B=4 run and a B=1 run on sample 0's inputs both match the
     # oracle.  They need not be bitwise equal: the fp32 summation order of a
@@ -155,8 +169,8 @@ def test_forward_deterministic_and_batch_consistent():
     one = dict(cfg.shape(), B=1)
     per = cfg.P // cfg.B
     plan1 = _gpu.run_prepare(coor[:per], one)
-    o = bp.forward(_gpu.to_dev(data["depth"][:1]), _gpu.to_dev(data["feat"][:1]), plan1,
-                   out_dtype=torch.float32)
+    o = _fwd(path, _gpu.to_dev(data["depth"][:1]), _gpu.to_dev(data["feat"][:1]), plan1,
+             out_dtype=torch.float32)
     ref, mag = oracle.forward_ref(data["depth"][:1], data["feat"][:1], coor[:per], one)
     _gpu.assert_within(o.cpu().numpy(), ref, mag, "f16", "B=1 run")
     _gpu.assert_within(out1[:1].cpu().numpy(), ref, mag, "f16", "sample 0 of B=4 run")
@@ -175,3 +189,44 @@ def test_forward_with_oracle_plan():
     out = bp.forward(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), plan)
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
     _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", "oracle plan")
+
+
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
+def test_schedule_counts(name):
+    """The schedule's pair, task and item counts against a numpy derivation
+    from the oracle's plan.  A pair is a maximal run of kept points with the
+    same BEV rank, the same pixel and consecutive depth bins."""
+    cfg = CONFIGS[name]
+    coor = frustum_coor(cfg)
+    plan = _gpu.run_prepare(coor, cfg.shape())
+    sched = bp.schedule(plan)
+    hdr = sched.header()
+    ref = oracle.prepare_ref(coor, cfg.shape())
+    rb = ref["ranks_bev"].astype(np.int64)
+    rf = ref["ranks_feat"].astype(np.int64)
+    rd = ref["ranks_depth"].astype(np.int64)
+    o = np.lexsort((rd, rf, rb))
+    rb, rf, rd = rb[o], rf[o], rd[o]
+    hw = cfg.H * cfg.W
+    head = np.ones(rb.size, dtype=bool)
+    head[1:] = (rb[1:] != rb[:-1]) | (rf[1:] != rf[:-1]) | (rd[1:] != rd[:-1] + hw)
+    n_pairs = int(head.sum())
+    n_tasks = -(-n_pairs // 2048)
+    assert hdr[0] == n_pairs and hdr[1] == n_tasks
+    assert hdr[3] == ref["n_valid"] and hdr[4] == ref["n_intervals"] and hdr[5] == ref["n_intervals"]
+    assert n_tasks <= hdr[2] <= 2 * n_tasks + 1
+
+
+def test_scheduled_matches_ranges():
+    cfg = CONFIGS["headline"]
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    plan = _gpu.run_prepare(coor, cfg.shape())
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    a = bp.forward(d, f, plan)
+    sched = bp.schedule(plan)
+    b = bp.forward_scheduled(d, f, sched)
+    c = bp.forward_scheduled(d, f, sched)
+    assert torch.equal(b, c)
+    # both within float32 rounding of each other relative to the output scale
+    assert float((a - b).abs().max()) <= 1e-4 * float(a.abs().max())
