@@ -14,8 +14,9 @@ every launch reads its inputs from HBM.  Each launch is bracketed by HIP
 events on the stream it runs on.  The achieved bandwidth divides the
 algorithmic bytes of one forward by that latency.
 
-The CPU baseline is the float64 oracle timed on the host for a bounded sample
-(a subset of the camera views) and scaled to one full forward.
+The CPU baseline is the float64 oracle timed on the host: whole forwards of
+the same workload, repeated until a minimum CPU time is spent, reported as the
+mean per forward.
 
 Prints one JSON line.
 """
@@ -42,7 +43,8 @@ from workloads import CONFIGS, draw_inputs, frustum_coor  # noqa: E402
 METRIC = "BEV-pool fwd latency (ms) + achieved HBM GB/s at 6×640×1600, D=118, C=80"
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 * 2 ** 20
-PMC_FILE = os.path.join(ROOT, "profiles", "forward_headline_traffic.json")
+PMC_FILE = os.path.join(ROOT, "profiles", "forward_headline_traffic.txt")
+FORWARD_SOURCES = ("forward_sched.hip", "internal.h", "vec.h", "device_utils.h")
 
 
 def log(msg):
@@ -61,7 +63,7 @@ def forward_min_bytes(cfg, n_valid, n_intervals) -> int:
 
 def source_digest() -> str:
     h = hashlib.sha256()
-    for f in ("forward.hip", "vec.h", "device_utils.h"):
+    for f in FORWARD_SOURCES:
         with open(os.path.join(ROOT, "paper_2211_17111_amd", "csrc", f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -100,7 +102,10 @@ def main():
     ap.add_argument("--workload", default="headline")
     ap.add_argument("--rotate", type=int, default=32, help="buffer sets cycled for cold timing")
     ap.add_argument("--fwd-launches", type=int, default=320)
-    ap.add_argument("--cpu-views", type=int, default=3, help="views in the oracle CPU sample (0: skip)")
+    ap.add_argument("--cpu-seconds", type=float, default=10.0,
+                    help="minimum CPU time of the oracle sample (0: skip the CPU baseline)")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="also launch one plain 256 MiB device copy (hardware-counter calibration)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -217,12 +222,16 @@ def main():
         per = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
         r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         r0.record(stream)
+        t_host = time.perf_counter()
         for i in range(n):
             fn(pick(i))
+        t_host = time.perf_counter() - t_host
         r1.record(stream)
         torch.cuda.synchronize()
+        host_us.append(t_host / n * 1e6)
         return per, r0.elapsed_time(r1) / n
 
+    host_us = []
     cold, cold_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)])
     warm, warm_region = timed_forwards(max(64, args.fwd_launches // 4), lambda i: sets[0])
     cold_rng, cold_rng_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)],
@@ -239,27 +248,42 @@ def main():
 
     traffic = None
     if os.path.exists(PMC_FILE):
+        # the summary's figures sit on its one line that holds a JSON object
         with open(PMC_FILE) as f:
-            pmc = json.load(f)
+            rows = [ln for ln in f if ln.lstrip().startswith("{")]
+        pmc = json.loads(rows[-1]) if rows else {}
         if pmc.get("source_digest") == source_digest() and pmc.get("workload") == cfg.name:
             traffic = pmc.get("hbm_bytes_per_launch")
 
     # ---- CPU baseline: the oracle on a bounded sample ----------------------
     cpu = None
-    if args.cpu_views > 0:
+    if args.cpu_seconds > 0:
         import oracle
-        nvw = min(args.cpu_views, cfg.N)
-        sub = dict(shape, B=1, N=nvw)
         per_view = cfg.D * cfg.H * cfg.W
-        t = time.perf_counter()
-        oracle.forward_ref(data["depth"][:1, :nvw], data["feat"][:1, :nvw], coor[:nvw * per_view], sub)
-        dt = time.perf_counter() - t
-        scale = (cfg.B * cfg.N) / nvw
-        cpu = {"value": round(dt * scale * 1e3, 1), "unit": "ms", "cores": 1, "kind": "oracle",
-               "sample": f"oracle.forward_ref (float64, materialised frustum + np.add.at) on {nvw} of "
-                         f"{cfg.B * cfg.N} camera views, {dt:.1f} s, scaled x{scale:g} to one forward",
+        # page in numpy code paths on one view (untimed)
+        oracle.forward_ref(data["depth"][:1, :1], data["feat"][:1, :1], coor[:per_view],
+                           dict(shape, B=1, N=1))
+        reps, spent = 0, 0.0
+        while spent < args.cpu_seconds and reps < 16:
+            t = time.perf_counter()
+            oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+            spent += time.perf_counter() - t
+            reps += 1
+        cpu = {"value": round(spent / reps * 1e3, 1), "unit": "ms", "cores": 1, "kind": "oracle",
+               "sample": f"{reps} full forwards of this workload by oracle.forward_ref (float64, "
+                         f"materialised frustum + np.add.at, single-threaded numpy), {spent:.1f} s "
+                         f"in total; value is the mean per forward",
                "host_cpu_count": os.cpu_count(), "host_cpu": platform.processor() or platform.machine()}
-        log(f"cpu oracle sample {dt:.1f} s -> {cpu['value']} ms per forward")
+        log(f"cpu oracle: {reps} forwards in {spent:.1f} s -> {cpu['value']} ms per forward")
+
+    if args.copy_calibration:
+        a = torch.empty(64 * 2 ** 20, dtype=torch.float32, device=dev)
+        b = torch.empty_like(a)
+        a.fill_(1.0)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        log("copy calibration: one 256 MiB device-to-device copy kernel launched")
 
     res = {
         "metric": METRIC,
@@ -280,7 +304,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes": min_bytes, "kernel": "k_forward"},
+                     "algorithmic_bytes": min_bytes, "kernel": "k_fwd_items"},
         "cpu_baseline": cpu,
         "detail": {
             "forward_cold_ms": {"mean": fwd_ms, "p10": float(np.percentile(cold, 10)),
@@ -289,6 +313,7 @@ def main():
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
             "forward_cold_region_ms_per_launch": cold_region,
             "forward_warm_ms": float(warm.mean()),
+            "forward_host_enqueue_us": host_us,
             "forward_warm_region_ms_per_launch": warm_region,
             "forward_unscheduled_cold_ms": float(cold_rng.mean()),
             "forward_unscheduled_cold_region_ms_per_launch": cold_rng_region,
