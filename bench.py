@@ -12,7 +12,9 @@ cold: the forward is launched over R rotating buffer sets (depth, feature,
 plan, output) whose total size is several times the 256 MB Infinity Cache, so
 every launch reads its inputs from HBM.  Each launch is bracketed by HIP
 events on the stream it runs on.  The achieved bandwidth divides the
-algorithmic bytes of one forward by that latency.
+algorithmic bytes of one forward by that latency.  --forward picks the entry
+point timed as the metric (interval-table or tiled-schedule forward); the
+other one is timed the same way and reported beside it.
 
 The CPU baseline is the float64 oracle timed on the host: whole forwards of
 the same workload, repeated until a minimum CPU time is spent, reported as the
@@ -44,7 +46,9 @@ METRIC = "BEV-pool fwd latency (ms) + achieved HBM GB/s at 6×640×1600, D=118, 
 HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 * 2 ** 20
 PMC_FILE = os.path.join(ROOT, "profiles", "forward_headline_traffic.txt")
-FORWARD_SOURCES = ("forward_sched.hip", "internal.h", "vec.h", "device_utils.h")
+# kernels of each forward path (the interval path is two launches, timed together)
+FORWARD_KERNELS = {"interval": "k_fwd_ranges+k_fwd_cells", "tiled": "k_fwd_tiles"}
+FORWARD_SOURCES = ("forward.hip", "forward_tiles.hip", "internal.h", "vec.h", "device_utils.h")
 
 
 def log(msg):
@@ -104,6 +108,9 @@ def main():
     ap.add_argument("--fwd-launches", type=int, default=320)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle sample (0: skip the CPU baseline)")
+    ap.add_argument("--forward", choices=["interval", "tiled"], default="interval",
+                    help="forward entry point timed as the metric: bevpool_forward (interval table) "
+                         "or bevpool_forward_scheduled (tiled schedule); the other is reported too")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also launch one plain 256 MiB device copy (hardware-counter calibration)")
     args = ap.parse_args()
@@ -161,13 +168,17 @@ def main():
         prepare(s)
     torch.cuda.synchronize()
 
-    def forward(s):
+    def forward_tiled(s):
         bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, nv, ni,
                                      s.out, stream)
 
-    def forward_ranges(s):
+    def forward_interval(s):
         bp.bevpool_forward(shape, code, ocode, s.depth, s.feat, s.rd, s.rf, s.rb, s.st, s.ln, nv, ni,
                            s.out, ws_f, ws_f_bytes, stream)
+
+    paths = {"interval": forward_interval, "tiled": forward_tiled}
+    forward = paths[args.forward]
+    other_name = "tiled" if args.forward == "interval" else "interval"
 
     def backward(s):
         bp.bevpool_backward(shape, code, ocode, s.grad_out, s.depth, s.feat, s.rd, s.rb, nv, s.gd, s.gf,
@@ -234,11 +245,11 @@ def main():
     host_us = []
     cold, cold_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)])
     warm, warm_region = timed_forwards(max(64, args.fwd_launches // 4), lambda i: sets[0])
-    cold_rng, cold_rng_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)],
-                                               forward_ranges)
-    log(f"forward back-to-back region: cold {cold_region * 1e3:.2f} us/launch, warm "
-        f"{warm_region * 1e3:.2f}; range-partition forward cold {cold_rng.mean() * 1e3:.2f} us "
-        f"(region {cold_rng_region * 1e3:.2f})")
+    cold_oth, cold_oth_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)],
+                                               paths[other_name])
+    log(f"{args.forward} forward back-to-back region: cold {cold_region * 1e3:.2f} us/launch, warm "
+        f"{warm_region * 1e3:.2f}; {other_name} forward cold {cold_oth.mean() * 1e3:.2f} us "
+        f"(region {cold_oth_region * 1e3:.2f})")
     fwd_ms = float(cold.mean())
     min_bytes = forward_min_bytes(cfg, nv, ni)
     achieved = min_bytes / (fwd_ms * 1e-3) / 1e9
@@ -252,7 +263,8 @@ def main():
         with open(PMC_FILE) as f:
             rows = [ln for ln in f if ln.lstrip().startswith("{")]
         pmc = json.loads(rows[-1]) if rows else {}
-        if pmc.get("source_digest") == source_digest() and pmc.get("workload") == cfg.name:
+        if (pmc.get("source_digest") == source_digest() and pmc.get("workload") == cfg.name
+                and pmc.get("kernel") == FORWARD_KERNELS[args.forward]):
             traffic = pmc.get("hbm_bytes_per_launch")
 
     # ---- CPU baseline: the oracle on a bounded sample ----------------------
@@ -304,7 +316,7 @@ def main():
                    "parallelism": "single GPU"},
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
-                     "algorithmic_bytes": min_bytes, "kernel": "k_fwd_items"},
+                     "algorithmic_bytes": min_bytes, "kernel": FORWARD_KERNELS[args.forward]},
         "cpu_baseline": cpu,
         "detail": {
             "forward_cold_ms": {"mean": fwd_ms, "p10": float(np.percentile(cold, 10)),
@@ -315,8 +327,9 @@ def main():
             "forward_warm_ms": float(warm.mean()),
             "forward_host_enqueue_us": host_us,
             "forward_warm_region_ms_per_launch": warm_region,
-            "forward_unscheduled_cold_ms": float(cold_rng.mean()),
-            "forward_unscheduled_cold_region_ms_per_launch": cold_rng_region,
+            "forward_path": args.forward,
+            f"forward_{other_name}_cold_ms": float(cold_oth.mean()),
+            f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
             "prepare_plus_forward_ms": prep_ms + fwd_in_step_ms, "step_wall_ms": wall_ms,
             "paper_context": "0.82 ms at 640x1600 (abstract), hardware not stated; 15.1x the previous "

@@ -230,6 +230,9 @@ int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
     REQUIRE_PTR(ranks_bev);
   }
   REQUIRE_PTR(schedule);
+  if (d.D > 65535)
+    return fail(BEVPOOL_EINVAL, "the schedule stores depth bins in 16 bits: D = %lld > 65535",
+                (long long)d.D);
   const bevpool::ScheduleLayout L = bevpool::schedule_layout(d, n_valid, n_intervals);
   if (schedule_bytes < L.total)
     return fail(BEVPOOL_EINVAL, "schedule needs %zu bytes, got %zu", L.total, schedule_bytes);

@@ -53,4 +53,14 @@ __device__ __forceinline__ int block_exclusive_scan(int v, int* lds, int* total)
   return off + inc - v;
 }
 
+// Workgroup barrier that orders LDS accesses only.  __syncthreads() also
+// waits for the calling wave's outstanding global loads and stores, which
+// stalls a barrier behind unrelated stores; callers that exchange data only
+// through LDS (or wait for their own global copies explicitly) use this.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
 }  // namespace bevpool

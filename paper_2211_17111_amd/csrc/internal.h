@@ -9,6 +9,8 @@
 
 namespace bevpool {
 
+constexpr int kWaveLanes = 64;
+
 // Sizes derived from a validated shape, all in int64 to avoid overflow while
 // checking limits.
 struct Dims {
@@ -48,40 +50,80 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
                           hipStream_t stream);
 
 // ---- schedule ----------------------------------------------------------------
-// Device layout of a forward schedule (all int32), built from a plan:
-//   header[16]            runtime counts, see kHdr*
-//   pair_rd0[n_valid]     depth rank of the first point of each pair
-//   pair_cell[n_valid]    BEV rank of each pair
-//   pair_npts[n_valid]    points of each pair: depth ranks rd0 + k*H*W
-//   cell_id[n_occ]        BEV rank of each occupied cell, ascending
-//   cell_pair[n_occ + 1]  first pair of each occupied cell (+ end sentinel)
-//   task_cell[tasks + 1]  first occupied cell owned by each task
-//   item_info[items][4]   first cell, end cell, first pair, end pair of the
-//                         task each work item belongs to, in task order
-//   item_chunk[items]     channel chunk of the item | (chunks of its task << 16)
-//   xcd_begin[kXcds + 1]  first item of each XCD: contiguous item ranges of
-//                         about equal work, so an XCD's L2 holds the feature
-//                         rows of one region of the BEV grid
-// A pair is a maximal run of kept points with the same BEV rank, the same
-// pixel and consecutive depth bins.
-constexpr int kSchedTaskPairs = 2048;  // nominal pairs per task
-constexpr int kHdrPairs = 0, kHdrTasks = 1, kHdrItems = 2, kHdrValid = 3, kHdrOcc = 4,
-              kHdrOccFound = 5, kHdrWork = 6;
+// A forward schedule regroups the kept points of a plan for the tiled forward
+// kernel.  Definitions:
+//   pair   maximal run of kept points with the same cell, the same pixel and
+//          consecutive depth bins (their depth scores multiply one feature row)
+//   cell   occupied BEV cell; cells are ordered by (b, z, Morton(y, x)) so that
+//          consecutive cells are close in the grid (falls back to the BEV rank
+//          when that key would not fit 31 bits)
+//   tile   consecutive cells, cut where the first pair of a cell crosses a
+//          multiple of kTilePairs / 2, where the cell index crosses a
+//          multiple of tile_max_cells(), and around any cell with more than
+//          kTilePairs / 2 pairs; so a tile of several cells has at most
+//          kTilePairs pairs and at most tile_max_cells() cells
+//   rows   the distinct feature rows of a tile, ascending: the rows the
+//          forward stages in LDS
+//   item   channel slice k of K of a tile; K grows with the tile's staged
+//          bytes (counted at 4 bytes per element, so one schedule serves
+//          both element types)
+// Device layout (int32 / uint32, 256-byte aligned arrays):
+//   header[16]               counts, see kHdr*
+//   pair_rl[n_valid]         index of the pair's feature row in its tile's rows
+//   pair_dn[n_valid]         first depth bin | (points << 16)
+//   cell_out[n_occ + 1]      BEV rank of each cell in tile order
+//   cell_pair[n_occ + 1]     first pair of each cell (+ end sentinel)
+//   tile_cell[n_occ + 1]     first cell of each tile (+ end sentinel)
+//   tile_row0[n_occ + 1]     first row entry of each tile (+ end sentinel)
+//   rows[n_valid]            feature rank of each row entry
+//   row_dbase[n_valid]       depth rank of each row entry's pixel at depth bin 0
+//   empty[cells - n_occ + 1] BEV rank of each empty cell, ascending
+//   item_tile[items_cap]     tile of each item, in tile order
+//   item_slice[items_cap]    k | (K << 16)
+//   xcd_begin[kXcds + 1]     first item of each XCD: contiguous item ranges of
+//                            about equal work, so one die's L2 holds the
+//                            feature rows of one region of the grid
+constexpr int kTilePairs = 4096;              // pairs a workgroup holds in LDS at once
+constexpr int kTileThreads = 1024;            // forward workgroup
+constexpr int kTileWindowBytes = 48 * 1024;   // LDS per buffer of staged feature rows (two)
+constexpr int kTileMaxCells = 512;            // cap of tile_max_cells()
+constexpr int kTileItemBytes = 192 * 1024;    // staged feature bytes per item (target)
+constexpr int kHdrPairs = 0, kHdrTiles = 1, kHdrItems = 2, kHdrValid = 3, kHdrOcc = 4,
+              kHdrOccFound = 5, kHdrEmpty = 6, kHdrRowEntries = 7, kHdrWork = 8;
 // gfx950 (MI355X) has 8 accelerator complex dies; workgroup i of a launch is
 // dispatched to die i % 8, each die with its own L2.
 constexpr int kXcds = 8;
 
+// Lane groups of the forward kernel.  A slice of `cs` channels is processed
+// in sub-slices of at most 64 vectors of `vec` elements; a lane group has one
+// lane per vector of a sub-slice and as many groups as fit in a wave share it.
+// Each group holds the accumulators of at most tile_max_units(vec) (cell,
+// chunk) units.
+inline int tile_group_lanes(int64_t cs, int vec) {
+  const int64_t g = (cs + vec - 1) / vec;
+  return (int)(g > kWaveLanes ? kWaveLanes : g);
+}
+inline int tile_groups(int64_t cs, int vec) {
+  return (kTileThreads / kWaveLanes) * (kWaveLanes / tile_group_lanes(cs, vec));
+}
+constexpr int tile_max_units(int vec) { return vec == 1 ? 8 : 16 / vec; }
+// Most cells a tile may hold: the (cell, chunk) units of any item, at most
+// one per cell plus one per chunk of a balanced split, must fit the groups'
+// accumulators for every vector width the forward may use (1, 4, 8).
+int tile_max_cells(const Dims& d);
+
 struct ScheduleLayout {
-  size_t header, pair_rd0, pair_cell, pair_npts, cell_id, cell_pair, task_cell, item_info,
-      item_chunk, xcd_begin, total;
-  int64_t n_valid, n_occ, tasks_cap, items_cap;
+  size_t header, pair_rl, pair_dn, cell_out, cell_pair, tile_cell, tile_row0, rows, row_dbase, empty,
+      item_tile, item_slice, xcd_begin, total;
+  int64_t n_valid, n_occ, n_empty, items_cap;
   // build workspace
-  size_t ws_keys_a, ws_vals_a, ws_keys_b, ws_vals_b, ws_head, ws_tiles, ws_hist, ws_sums, ws_total;
+  size_t ws_ka, ws_va, ws_kb, ws_vb, ws_head, ws_pair_rb, ws_pair_row, ws_flags, ws_tiles,
+      ws_hist, ws_sums, ws_total;
   int64_t ntiles, nscan;
-  int rf_bits, rb_bits;
+  int row_bits, key_bits, tile_bits;
+  int morton_level;  // cells keyed by (b*Z + z) << 2L | Morton(y, x); -1: by BEV rank
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
-int schedule_max_chunks(const Dims& d);
 hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
                            int32_t n_intervals, void* schedule, void* workspace,
                            hipStream_t stream);

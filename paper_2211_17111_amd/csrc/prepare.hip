@@ -335,19 +335,20 @@ __global__ __launch_bounds__(256) void k_interval_lengths(const int32_t* __restr
 
 // ------------------------------------------------------------------ schedule
 //
-// The forward schedule regroups the kept points of a plan by (cell, pixel):
-// several depth bins of one pixel often land in the same cell, and their
-// depth scores can be summed before the pixel's feature row is read once.
-// The regrouping is two more stable radix sorts of the plan (by feature rank,
-// then by BEV rank), after which runs of equal (BEV rank, feature rank) are
-// "pairs".  Pairs are then cut into tasks that own whole cells: task k owns
-// the cells whose first pair lies in [k*T, (k+1)*T).  A task with more than T
-// pairs is further split by channels into several work items, which need no
-// cross-item reduction because channels are independent.
+// The forward schedule regroups the kept points of a plan into pairs, cells,
+// tiles and items (see internal.h).  Steps, all on the device:
+//   1. stable radix sorts of the plan by feature rank, then by cell key
+//      (Morton order of the cell), giving (cell, pixel, depth rank) order;
+//   2. pair heads and cell heads by ordered compaction;
+//   3. tile heads over the cells;
+//   4. the distinct rows of each tile: pairs sorted by (tile, row), heads of
+//      equal runs, and each pair's index into its tile's row list;
+//   5. the empty cells, by compaction of an occupancy map;
+//   6. items per tile, their work, and per-die item ranges.
 
 // Generic ordered compaction over the same 4096-element tiles as the filter:
-// Op provides count(), flag(i), visit(i) (called for every i < count) and
-// emit(i, position) (called for flagged i, positions in index order).
+// Op provides count(), flag(i), and emit(i, position) (called for flagged i,
+// positions in index order).
 template <class Op>
 __global__ __launch_bounds__(kPrepThreads) void k_compact_count(Op op, int32_t* __restrict__ tile_counts) {
   __shared__ int wave_tot[kWavesPerTile];
@@ -384,7 +385,6 @@ __global__ __launch_bounds__(kPrepThreads) void k_compact_scatter(Op op,
   for (int r = 0; r < kPrepRounds; ++r) {
     const int64_t i = base + r * kWave + lane;
     const bool f = i < n && op.flag(i);
-    if (i < n) op.visit(i);
     flags |= (uint32_t)f << r;
     cnt += __popcll(wave_ballot(f));
   }
@@ -405,45 +405,27 @@ __device__ __forceinline__ int32_t pixel_of(int32_t p, int64_t per_view, int64_t
   return (int32_t)(((int64_t)p / per_view) * hw + (int64_t)p % hw);
 }
 
-struct PairHeads {  // runs of equal (BEV rank, pixel) with consecutive depth bins
-  const int32_t* rd;
-  const int32_t* rb;
-  const int32_t* vals;  // plan position of each regrouped point
-  const int32_t* hdr;
-  int64_t per_view, hw;
-  int32_t* pair_rd0;
-  int32_t* pair_cell;
-  int32_t* head_pos;   // regrouped position of each pair's first point
-  __device__ int64_t count() const { return hdr[kHdrValid]; }
-  __device__ bool flag(int64_t i) const {
-    if (i == 0) return true;
-    const int32_t a = vals[i], b = vals[i - 1];
-    const int32_t pa = rd[a], pb = rd[b];
-    return rb[a] != rb[b] || pixel_of(pa, per_view, hw) != pixel_of(pb, per_view, hw) ||
-           (int64_t)pa != (int64_t)pb + hw;
-  }
-  __device__ void visit(int64_t) const {}
-  __device__ void emit(int64_t i, int32_t pos) const {
-    const int32_t a = vals[i];
-    pair_rd0[pos] = rd[a];
-    pair_cell[pos] = rb[a];
-    head_pos[pos] = (int32_t)i;
-  }
-};
+// Spreads the low 16 bits of v to the even bit positions.
+__device__ __forceinline__ uint32_t spread_bits(uint32_t v) {
+  v &= 0xffffu;
+  v = (v | (v << 8)) & 0x00ff00ffu;
+  v = (v | (v << 4)) & 0x0f0f0f0fu;
+  v = (v | (v << 2)) & 0x33333333u;
+  v = (v | (v << 1)) & 0x55555555u;
+  return v;
+}
 
-struct CellHeads {  // first pair of every occupied cell
-  const int32_t* pair_cell;
-  const int32_t* hdr;
-  int32_t* cell_id;
-  int32_t* cell_pair;
-  int32_t cap;  // occupied cells the plan declares (n_intervals)
-  __device__ int64_t count() const { return hdr[kHdrPairs]; }
-  __device__ bool flag(int64_t k) const { return k == 0 || pair_cell[k] != pair_cell[k - 1]; }
-  __device__ void visit(int64_t) const {}
-  __device__ void emit(int64_t k, int32_t pos) const {
-    if (pos >= cap) return;  // plan inconsistent with n_intervals: never write past the arrays
-    cell_pair[pos] = (int32_t)k;
-    cell_id[pos] = pair_cell[k];
+struct CellKey {  // BEV rank -> sort key of its cell
+  int64_t XY;
+  int32_t X;
+  int32_t level;  // -1: the BEV rank itself
+  __device__ int32_t operator()(int32_t rb) const {
+    if (level < 0) return rb;
+    const int32_t bz = (int32_t)(rb / XY);
+    const int32_t r = (int32_t)(rb - (int64_t)bz * XY);
+    const int32_t y = r / X, x = r - y * X;
+    return (int32_t)(((uint32_t)bz << (2 * level)) | spread_bits((uint32_t)x) |
+                     (spread_bits((uint32_t)y) << 1));
   }
 };
 
@@ -456,10 +438,10 @@ __global__ void k_sched_init(int32_t* __restrict__ hdr, int32_t n_valid, int32_t
   }
 }
 
-__global__ __launch_bounds__(256) void k_sched_rf_keys(const int32_t* __restrict__ rd, int64_t n,
-                                                       int64_t per_view, int64_t hw,
-                                                       int32_t* __restrict__ keys,
-                                                       int32_t* __restrict__ vals) {
+__global__ __launch_bounds__(256) void k_row_keys(const int32_t* __restrict__ rd, int64_t n,
+                                                  int64_t per_view, int64_t hw,
+                                                  int32_t* __restrict__ keys,
+                                                  int32_t* __restrict__ vals) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) {
     keys[i] = pixel_of(rd[i], per_view, hw);
@@ -467,89 +449,261 @@ __global__ __launch_bounds__(256) void k_sched_rf_keys(const int32_t* __restrict
   }
 }
 
-__global__ __launch_bounds__(256) void k_sched_rb_keys(const int32_t* __restrict__ rb,
-                                                       const int32_t* __restrict__ vals, int64_t n,
-                                                       int32_t* __restrict__ keys) {
+__global__ __launch_bounds__(256) void k_cell_keys(const int32_t* __restrict__ rb,
+                                                   const int32_t* __restrict__ vals, int64_t n,
+                                                   CellKey key, int32_t* __restrict__ keys) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) keys[i] = rb[vals[i]];
+  if (i < n) keys[i] = key(rb[vals[i]]);
 }
 
-__global__ void k_sched_sentinels(int32_t* __restrict__ hdr, int32_t* __restrict__ head_pos,
-                                  int32_t* __restrict__ cell_pair) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) {
-    const int32_t np = hdr[kHdrPairs];
-    head_pos[np] = hdr[kHdrValid];
-    cell_pair[min(hdr[kHdrOcc], hdr[kHdrOccFound])] = np;
-    hdr[kHdrTasks] = (np + kSchedTaskPairs - 1) / kSchedTaskPairs;
+struct PairHeads {  // runs of equal (cell, pixel) over consecutive depth bins
+  const int32_t* rd;
+  const int32_t* rb;
+  const int32_t* vals;  // plan position of each regrouped point
+  const int32_t* hdr;
+  int64_t per_view, hw;
+  int32_t* pair_rb;
+  int32_t* pair_row;
+  uint32_t* pair_dn;
+  int32_t* head_pos;  // regrouped position of each pair's first point
+  __device__ int64_t count() const { return hdr[kHdrValid]; }
+  __device__ bool flag(int64_t i) const {
+    if (i == 0) return true;
+    const int32_t a = vals[i], b = vals[i - 1];
+    const int32_t pa = rd[a], pb = rd[b];
+    return rb[a] != rb[b] || pixel_of(pa, per_view, hw) != pixel_of(pb, per_view, hw) ||
+           (int64_t)pa != (int64_t)pb + hw;
+  }
+  __device__ void emit(int64_t i, int32_t pos) const {
+    const int32_t a = vals[i];
+    const int32_t p = rd[a];
+    pair_rb[pos] = rb[a];
+    pair_row[pos] = pixel_of(p, per_view, hw);
+    pair_dn[pos] = (uint32_t)(((int64_t)p % per_view) / hw);
+    head_pos[pos] = (int32_t)i;
+  }
+};
+
+__global__ __launch_bounds__(256) void k_pair_points(const int32_t* __restrict__ head_pos,
+                                                     const int32_t* __restrict__ hdr,
+                                                     uint32_t* __restrict__ pair_dn) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  const int64_t np = hdr[kHdrPairs];
+  if (p < np) {
+    const int64_t next = (p + 1 < np) ? head_pos[p + 1] : hdr[kHdrValid];
+    pair_dn[p] |= (uint32_t)(next - head_pos[p]) << 16;
   }
 }
 
-__global__ __launch_bounds__(256) void k_pair_npts(const int32_t* __restrict__ head_pos,
-                                                   const int32_t* __restrict__ hdr,
-                                                   int32_t* __restrict__ pair_npts) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k < hdr[kHdrPairs]) pair_npts[k] = head_pos[k + 1] - head_pos[k];
+struct CellHeads {  // first pair of every occupied cell
+  const int32_t* pair_rb;
+  const int32_t* hdr;
+  int32_t* cell_out;
+  int32_t* cell_pair;
+  int32_t cap;  // occupied cells the plan declares (n_intervals)
+  __device__ int64_t count() const { return hdr[kHdrPairs]; }
+  __device__ bool flag(int64_t k) const { return k == 0 || pair_rb[k] != pair_rb[k - 1]; }
+  __device__ void emit(int64_t k, int32_t pos) const {
+    if (pos >= cap) return;  // plan inconsistent with n_intervals: never write past the arrays
+    cell_pair[pos] = (int32_t)k;
+    cell_out[pos] = pair_rb[k];
+  }
+};
+
+__global__ void k_cells_end(int32_t* __restrict__ hdr, int32_t* __restrict__ cell_pair) {
+  if (threadIdx.x == 0 && blockIdx.x == 0)
+    cell_pair[min(hdr[kHdrOcc], hdr[kHdrOccFound])] = hdr[kHdrPairs];
 }
 
-// task_cell[k] = first occupied cell whose first pair is >= k*T.  Nothing
-// is written when the plan's cell count disagrees with what was found.
-__global__ __launch_bounds__(256) void k_sched_tasks(const int32_t* __restrict__ cell_pair,
-                                                     const int32_t* __restrict__ hdr, int32_t n_occ,
-                                                     int32_t* __restrict__ task_cell) {
-  if (hdr[kHdrOccFound] != n_occ) return;
-  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int32_t T = kSchedTaskPairs;
-  const int32_t n_tasks = hdr[kHdrTasks];
-  if (j == 0) task_cell[0] = 0;
-  if (j >= 1 && j < n_occ) {
-    const int32_t hi = min(cell_pair[j] / T, n_tasks);
-    for (int32_t k = max(cell_pair[j - 1] / T + 1, 1); k <= hi; ++k) task_cell[k] = (int32_t)j;
-  } else if (j == n_occ && n_occ > 0) {
-    for (int32_t k = max(cell_pair[n_occ - 1] / T + 1, 1); k <= n_tasks; ++k) task_cell[k] = n_occ;
+struct TileHeads {  // first cell of every tile
+  const int32_t* cell_pair;
+  const int32_t* hdr;
+  int32_t* tile_cell;
+  int32_t max_cells;
+  __device__ int64_t count() const {
+    return hdr[kHdrOccFound] == hdr[kHdrOcc] ? hdr[kHdrOcc] : 0;
+  }
+  __device__ bool big(int64_t c) const { return cell_pair[c + 1] - cell_pair[c] > kTilePairs / 2; }
+  __device__ bool flag(int64_t c) const {
+    if (c == 0 || c % max_cells == 0) return true;
+    return big(c) || big(c - 1) || cell_pair[c] / (kTilePairs / 2) != cell_pair[c - 1] / (kTilePairs / 2);
+  }
+  __device__ void emit(int64_t c, int32_t pos) const { tile_cell[pos] = (int32_t)c; }
+};
+
+__global__ void k_tiles_end(const int32_t* __restrict__ hdr, int32_t* __restrict__ tile_cell) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) tile_cell[hdr[kHdrTiles]] = hdr[kHdrOcc];
+}
+
+// Largest index i in [0, n) with a[i] <= v (a ascending, a[0] <= v).
+__device__ __forceinline__ int32_t upper_index(const int32_t* __restrict__ a, int32_t n, int32_t v) {
+  int32_t lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (a[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// Tile of every pair (into pair_tile) and the (row, pair) keys of the row sort.
+__global__ __launch_bounds__(256) void k_pair_tiles(const int32_t* __restrict__ hdr,
+                                                    const int32_t* __restrict__ cell_pair,
+                                                    const int32_t* __restrict__ tile_cell,
+                                                    const int32_t* __restrict__ pair_row,
+                                                    int32_t* __restrict__ pair_tile,
+                                                    int32_t* __restrict__ keys,
+                                                    int32_t* __restrict__ vals) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p >= hdr[kHdrPairs] || hdr[kHdrOccFound] != hdr[kHdrOcc]) return;
+  const int32_t c = upper_index(cell_pair, hdr[kHdrOcc], (int32_t)p);
+  pair_tile[p] = upper_index(tile_cell, hdr[kHdrTiles], c);
+  keys[p] = pair_row[p];
+  vals[p] = (int32_t)p;
+}
+
+__global__ __launch_bounds__(256) void k_tile_keys(const int32_t* __restrict__ hdr,
+                                                   const int32_t* __restrict__ vals,
+                                                   const int32_t* __restrict__ pair_tile,
+                                                   int32_t* __restrict__ keys) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < hdr[kHdrPairs]) keys[q] = pair_tile[vals[q]];
+}
+
+__device__ __forceinline__ bool row_head(const int32_t* vals, const int32_t* pair_tile,
+                                         const int32_t* pair_row, int64_t q) {
+  if (q == 0) return true;
+  const int32_t a = vals[q], b = vals[q - 1];
+  return pair_tile[a] != pair_tile[b] || pair_row[a] != pair_row[b];
+}
+
+// flags[q] = 1 at the first pair of each (tile, row) run, 0 elsewhere (and
+// beyond the pairs, up to cap).
+__global__ __launch_bounds__(256) void k_row_flags(const int32_t* __restrict__ hdr,
+                                                   const int32_t* __restrict__ vals,
+                                                   const int32_t* __restrict__ pair_tile,
+                                                   const int32_t* __restrict__ pair_row,
+                                                   int64_t cap, int32_t* __restrict__ flags) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= cap) return;
+  flags[q] = (q < hdr[kHdrPairs] && row_head(vals, pair_tile, pair_row, q)) ? 1 : 0;
+}
+
+// With flags exclusively scanned: row entry of each sorted pair (kept in
+// flags), the row list (feature rank and the pixel's depth rank at bin 0),
+// and each tile's first entry.
+__global__ __launch_bounds__(256) void k_row_scatter(const int32_t* __restrict__ hdr,
+                                                     const int32_t* __restrict__ vals,
+                                                     const int32_t* __restrict__ pair_tile,
+                                                     const int32_t* __restrict__ pair_row,
+                                                     int32_t* __restrict__ flags,
+                                                     int32_t* __restrict__ rows,
+                                                     int32_t* __restrict__ row_dbase,
+                                                     int32_t* __restrict__ tile_row0,
+                                                     int64_t per_view, int64_t hw) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= hdr[kHdrPairs]) return;
+  const int32_t a = vals[q];
+  const bool head = row_head(vals, pair_tile, pair_row, q);
+  const int32_t e = flags[q] + (head ? 1 : 0) - 1;
+  flags[q] = e;
+  if (head) {
+    const int64_t row = pair_row[a];
+    rows[e] = (int32_t)row;
+    row_dbase[e] = (int32_t)((row / hw) * per_view + row % hw);
+  }
+  if (q == 0 || pair_tile[a] != pair_tile[vals[q - 1]]) tile_row0[pair_tile[a]] = e;
+}
+
+__global__ void k_rows_end(const int32_t* __restrict__ hdr, int32_t* __restrict__ tile_row0) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) tile_row0[hdr[kHdrTiles]] = hdr[kHdrRowEntries];
+}
+
+__global__ __launch_bounds__(256) void k_pair_rl(const int32_t* __restrict__ hdr,
+                                                 const int32_t* __restrict__ vals,
+                                                 const int32_t* __restrict__ pair_tile,
+                                                 const int32_t* __restrict__ entry,
+                                                 const int32_t* __restrict__ tile_row0,
+                                                 uint32_t* __restrict__ pair_rl) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= hdr[kHdrPairs]) return;
+  const int32_t a = vals[q];
+  pair_rl[a] = (uint32_t)(entry[q] - tile_row0[pair_tile[a]]);
+}
+
+__global__ __launch_bounds__(256) void k_fill_i32(int32_t* __restrict__ a, int64_t n, int32_t v) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) a[i] = v;
+}
+
+__global__ __launch_bounds__(256) void k_mark_cells(const int32_t* __restrict__ hdr,
+                                                    const int32_t* __restrict__ cell_out,
+                                                    int64_t cells, int32_t* __restrict__ occ) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c < min(hdr[kHdrOcc], hdr[kHdrOccFound])) {
+    const int32_t cell = cell_out[c];
+    if (cell >= 0 && cell < cells) occ[cell] = 1;
   }
 }
 
-__device__ __forceinline__ int32_t task_chunks(const int32_t* cell_pair, const int32_t* task_cell,
-                                               int64_t k, int max_chunks) {
-  const int32_t w = cell_pair[task_cell[k + 1]] - cell_pair[task_cell[k]];
-  if (w <= 0) return 0;
-  const int32_t c = (w + kSchedTaskPairs - 1) / kSchedTaskPairs;
-  return c < max_chunks ? c : max_chunks;
+struct EmptyCells {  // BEV ranks no kept point maps to, ascending
+  const int32_t* occ;
+  int64_t cells;
+  int32_t* empty;
+  int64_t cap;
+  __device__ int64_t count() const { return cells; }
+  __device__ bool flag(int64_t i) const { return occ[i] == 0; }
+  __device__ void emit(int64_t i, int32_t pos) const {
+    if (pos < cap) empty[pos] = (int32_t)i;
+  }
+};
+
+struct SliceCounts {  // channel slice counts a tile may take, ascending
+  int32_t k[16];
+  int32_t n;
+};
+
+// Slices of tile t: the fewest allowed K that bring its staged rows (counted
+// at 4 bytes per element) within the per-item target.
+__device__ __forceinline__ int32_t tile_slices(const int32_t* tile_row0, int64_t t, int64_t C,
+                                               const SliceCounts& sk) {
+  const int64_t rows = tile_row0[t + 1] - tile_row0[t];
+  for (int i = 0; i < sk.n; ++i)
+    if (rows * (C / sk.k[i]) * 4 <= kTileItemBytes) return sk.k[i];
+  return sk.k[sk.n - 1];
 }
 
-__global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ cell_pair,
-                                                     const int32_t* __restrict__ task_cell,
-                                                     const int32_t* __restrict__ hdr, int64_t cap,
-                                                     int max_chunks, int32_t* __restrict__ count) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (k >= cap) return;
-  const bool ok = hdr[kHdrOccFound] == hdr[kHdrOcc] && k < hdr[kHdrTasks];
-  count[k] = ok ? task_chunks(cell_pair, task_cell, k, max_chunks) : 0;
+__global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
+                                                     const int32_t* __restrict__ tile_row0,
+                                                     int64_t C, SliceCounts sk, int64_t cap,
+                                                     int32_t* __restrict__ count) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= cap) return;
+  const bool ok = hdr[kHdrOccFound] == hdr[kHdrOcc] && t < hdr[kHdrTiles];
+  count[t] = ok ? tile_slices(tile_row0, t, C, sk) : 0;
 }
 
-// Items in task order; work[i] = pairs of the item's task / its chunk count.
-__global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ cell_pair,
-                                                      const int32_t* __restrict__ task_cell,
-                                                      int32_t* __restrict__ hdr, int max_chunks,
+// Items in tile order; work[i] ~ staged row elements + half the pair-row
+// products of the item, in units of 64 elements.
+__global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ hdr,
+                                                      const int32_t* __restrict__ tile_cell,
+                                                      const int32_t* __restrict__ cell_pair,
+                                                      const int32_t* __restrict__ tile_row0,
+                                                      int64_t C, SliceCounts sk,
                                                       const int32_t* __restrict__ offset,
-                                                      int32_t* __restrict__ item_info,
-                                                      int32_t* __restrict__ item_chunk,
+                                                      int32_t* __restrict__ item_tile,
+                                                      int32_t* __restrict__ item_slice,
                                                       int32_t* __restrict__ work) {
-  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (hdr[kHdrOccFound] != hdr[kHdrOcc] || k >= hdr[kHdrTasks]) return;
-  const int32_t K = task_chunks(cell_pair, task_cell, k, max_chunks);
-  if (K == 0) return;
-  const int32_t base = offset[k];
-  const int32_t cb = task_cell[k], ce = task_cell[k + 1];
-  const int32_t pb = cell_pair[cb], pe = cell_pair[ce];
-  for (int32_t c = 0; c < K; ++c) {
-    int32_t* info = item_info + 4 * (int64_t)(base + c);
-    info[0] = cb;
-    info[1] = ce;
-    info[2] = pb;
-    info[3] = pe;
-    item_chunk[base + c] = c | (K << 16);
-    work[base + c] = (pe - pb + K - 1) / K;
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (hdr[kHdrOccFound] != hdr[kHdrOcc] || t >= hdr[kHdrTiles]) return;
+  const int32_t K = tile_slices(tile_row0, t, C, sk);
+  const int64_t rows = tile_row0[t + 1] - tile_row0[t];
+  const int64_t pairs = cell_pair[tile_cell[t + 1]] - cell_pair[tile_cell[t]];
+  const int64_t w = ((rows + pairs / 2) * (C / K) + 63) / 64;
+  const int32_t base = offset[t];
+  for (int32_t k = 0; k < K; ++k) {
+    item_tile[base + k] = (int32_t)t;
+    item_slice[base + k] = k | (K << 16);
+    work[base + k] = (int32_t)(w < 0x3fffffff ? w : 0x3fffffff);
   }
 }
 
@@ -559,8 +713,8 @@ __global__ __launch_bounds__(256) void k_item_work_tail(const int32_t* __restric
   if (i < cap && i >= hdr[kHdrItems]) work[i] = 0;
 }
 
-// xcd_begin[x] = first item whose exclusive work prefix reaches x/8 of the
-// total work, so each die gets a contiguous run of items of about equal work.
+// xcd_begin[x] = first item whose preceding work reaches x/8 of the total,
+// so each die gets a contiguous run of items of about equal work.
 // `cum` holds the exclusive prefix of the per-item work.
 __global__ __launch_bounds__(256) void k_xcd_bounds(const int32_t* __restrict__ cum,
                                                     const int32_t* __restrict__ hdr,
@@ -697,15 +851,48 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 
 namespace bevpool {
 
-int schedule_max_chunks(const Dims& d) { return (d.C % 16 == 0) ? (int)(d.C / 16) : 1; }
+int tile_max_cells(const Dims& d) {
+  int64_t best = kTileMaxCells;
+  for (int vec : {1, 4, 8}) {
+    if (d.C % vec != 0) continue;
+    const int64_t cs = d.C < 64 * vec ? d.C : 64 * vec;
+    const int64_t m = (int64_t)(tile_max_units(vec) - 1) * tile_groups(cs, vec);
+    if (m < best) best = m;
+  }
+  return (int)(best > 0 ? best : 1);
+}
+
+namespace {
+
+SliceCounts slice_counts(const Dims& d) {
+  SliceCounts sk{};
+  sk.n = 0;
+  for (int64_t k = 1; k <= d.C && sk.n < 16; ++k)
+    if (d.C % k == 0 && (k == 1 || (d.C / k) % 8 == 0)) sk.k[sk.n++] = (int32_t)k;
+  return sk;
+}
+
+// Morton level L (2^L >= X, Y) when (b*Z + z) << 2L | Morton(y, x) fits 31
+// bits, else -1.
+int morton_level(const Dims& d) {
+  int L = 0;
+  while ((int64_t(1) << L) < d.X || (int64_t(1) << L) < d.Y) ++L;
+  if (L > 15) return -1;
+  if (bit_length(d.B * d.Z) + 2 * L > 31) return -1;
+  return L;
+}
+
+}  // namespace
 
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals) {
   ScheduleLayout L{};
   L.n_valid = n_valid;
   L.n_occ = n_intervals;
-  L.tasks_cap = (n_valid + kSchedTaskPairs - 1) / kSchedTaskPairs + 1;
-  L.items_cap = 2 * L.tasks_cap;
+  L.n_empty = d.cells > n_intervals ? d.cells - n_intervals : 0;
+  const SliceCounts sk = slice_counts(d);
+  L.items_cap = (n_intervals + 1) * sk.k[sk.n - 1];
   const size_t nv = (size_t)(n_valid > 0 ? n_valid : 1);
+  const size_t nocc = (size_t)n_intervals + 1;
   size_t off = 0;
   auto take = [&](size_t n_ints) {
     const size_t o = off;
@@ -713,32 +900,42 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
     return o;
   };
   L.header = take(16);
-  L.pair_rd0 = take(nv);
-  L.pair_cell = take(nv);
-  L.pair_npts = take(nv);
-  L.cell_id = take((size_t)n_intervals + 1);
-  L.cell_pair = take((size_t)n_intervals + 1);
-  L.task_cell = take((size_t)L.tasks_cap + 1);
-  L.item_info = take(4 * (size_t)L.items_cap);
-  L.item_chunk = take((size_t)L.items_cap);
+  L.pair_rl = take(nv);
+  L.pair_dn = take(nv);
+  L.cell_out = take(nocc);
+  L.cell_pair = take(nocc);
+  L.tile_cell = take(nocc);
+  L.tile_row0 = take(nocc);
+  L.rows = take(nv);
+  L.row_dbase = take(nv);
+  L.empty = take((size_t)L.n_empty + 1);
+  L.item_tile = take((size_t)L.items_cap);
+  L.item_slice = take((size_t)L.items_cap);
   L.xcd_begin = take(kXcds + 1);
   L.total = off;
 
-  L.ntiles = ((int64_t)nv + kPrepTile - 1) / kPrepTile;
-  const int64_t scan_n = std::max<int64_t>(256 * L.ntiles, L.items_cap);
+  const int64_t span = std::max<int64_t>((int64_t)nv, d.cells);
+  L.ntiles = (span + kPrepTile - 1) / kPrepTile;
+  const int64_t scan_n = std::max<int64_t>(std::max<int64_t>(256 * L.ntiles, L.items_cap), span);
   L.nscan = (scan_n + kScanTile - 1) / kScanTile;
   off = 0;
-  L.ws_keys_a = take(nv);
-  L.ws_vals_a = take(nv);
-  L.ws_head = take(nv + 1);
-  L.ws_keys_b = take(nv);
-  L.ws_vals_b = take(nv);
-  L.ws_tiles = take((size_t)std::max<int64_t>(L.ntiles, L.tasks_cap + L.items_cap) + 2);
+  L.ws_ka = take(nv);
+  L.ws_va = take(nv);
+  L.ws_kb = take(nv);
+  L.ws_vb = take(nv);
+  L.ws_head = take(nv);
+  L.ws_pair_rb = take(nv);
+  L.ws_pair_row = take(nv);
+  L.ws_flags = take((size_t)span + 1);
+  L.ws_tiles = take((size_t)std::max<int64_t>(L.ntiles, nocc + L.items_cap) + 2);
   L.ws_hist = take((size_t)(256 * L.ntiles));
   L.ws_sums = take((size_t)L.nscan + 1);
   L.ws_total = off;
-  L.rf_bits = bit_length(d.rows);
-  L.rb_bits = bit_length(d.cells);
+  L.row_bits = bit_length(d.rows);
+  L.morton_level = morton_level(d);
+  L.key_bits = L.morton_level < 0 ? bit_length(d.cells)
+                                  : bit_length(d.B * d.Z) + 2 * L.morton_level;
+  L.tile_bits = bit_length(n_intervals + 1);
   return L;
 }
 
@@ -753,53 +950,97 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
   int32_t* hdr = S(L.header);
   int32_t* tiles = W(L.ws_tiles);
   int32_t* sums = W(L.ws_sums);
+  int32_t* hist = W(L.ws_hist);
+  const dim3 grid((unsigned)L.ntiles), block(kPrepThreads);
+  const unsigned g_nv = (unsigned)((n_valid + 255) / 256);
 
   k_sched_init<<<1, 64, 0, stream>>>(hdr, n_valid, n_intervals);
+
+  // empty cells (also when nothing is kept)
+  int32_t* occ = W(L.ws_flags);
+  k_fill_i32<<<(unsigned)((d.cells + 255) / 256), 256, 0, stream>>>(occ, d.cells, 0);
+  if (n_valid > 0) {
+    // 1. regroup by (cell key, pixel, plan position)
+    k_row_keys<<<g_nv, 256, 0, stream>>>(rd, n_valid, d.per_view, d.hw, W(L.ws_ka), W(L.ws_va));
+    const bool in_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
+                                       hdr + kHdrValid, L.ntiles, L.row_bits, hist, sums, stream);
+    int32_t* k0 = in_b ? W(L.ws_kb) : W(L.ws_ka);
+    int32_t* v0 = in_b ? W(L.ws_vb) : W(L.ws_va);
+    int32_t* k1 = in_b ? W(L.ws_ka) : W(L.ws_kb);
+    int32_t* v1 = in_b ? W(L.ws_va) : W(L.ws_vb);
+    const CellKey ck{d.X * d.Y, (int32_t)d.X, L.morton_level};
+    k_cell_keys<<<g_nv, 256, 0, stream>>>(rb, v0, n_valid, ck, k0);
+    const bool in_1 = radix_sort_pairs(k0, v0, k1, v1, hdr + kHdrValid, L.ntiles, L.key_bits, hist,
+                                       sums, stream);
+    const int32_t* vals = in_1 ? v1 : v0;
+
+    // 2. pairs and cells
+    int32_t* head_pos = W(L.ws_head);
+    uint32_t* pair_dn = reinterpret_cast<uint32_t*>(S(L.pair_dn));
+    PairHeads ph{rd, rb, vals, hdr, d.per_view, d.hw, W(L.ws_pair_rb), W(L.ws_pair_row), pair_dn,
+                 head_pos};
+    k_compact_count<<<grid, block, 0, stream>>>(ph, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrPairs, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(ph, tiles);
+    k_pair_points<<<g_nv, 256, 0, stream>>>(head_pos, hdr, pair_dn);
+    CellHeads ch{W(L.ws_pair_rb), hdr, S(L.cell_out), S(L.cell_pair), n_intervals};
+    k_compact_count<<<grid, block, 0, stream>>>(ch, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(ch, tiles);
+    k_cells_end<<<1, 64, 0, stream>>>(hdr, S(L.cell_pair));
+
+    // 3. tiles
+    TileHeads th{S(L.cell_pair), hdr, S(L.tile_cell), tile_max_cells(d)};
+    k_compact_count<<<grid, block, 0, stream>>>(th, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrTiles, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(th, tiles);
+    k_tiles_end<<<1, 64, 0, stream>>>(hdr, S(L.tile_cell));
+
+    // 4. distinct rows per tile
+    int32_t* pair_tile = W(L.ws_pair_rb);  // cell ranks are no longer needed
+    k_pair_tiles<<<g_nv, 256, 0, stream>>>(hdr, S(L.cell_pair), S(L.tile_cell), W(L.ws_pair_row),
+                                           pair_tile, W(L.ws_ka), W(L.ws_va));
+    const bool r_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
+                                      hdr + kHdrPairs, L.ntiles, L.row_bits, hist, sums, stream);
+    int32_t* rk0 = r_b ? W(L.ws_kb) : W(L.ws_ka);
+    int32_t* rv0 = r_b ? W(L.ws_vb) : W(L.ws_va);
+    int32_t* rk1 = r_b ? W(L.ws_ka) : W(L.ws_kb);
+    int32_t* rv1 = r_b ? W(L.ws_va) : W(L.ws_vb);
+    k_tile_keys<<<g_nv, 256, 0, stream>>>(hdr, rv0, pair_tile, rk0);
+    const bool t_1 = radix_sort_pairs(rk0, rv0, rk1, rv1, hdr + kHdrPairs, L.ntiles, L.tile_bits,
+                                      hist, sums, stream);
+    const int32_t* pvals = t_1 ? rv1 : rv0;
+    int32_t* entry = W(L.ws_head);  // pair heads are no longer needed
+    k_row_flags<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, W(L.ws_pair_row), n_valid, entry);
+    scan_exclusive(entry, n_valid, sums, hdr + kHdrRowEntries, stream);
+    k_row_scatter<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, W(L.ws_pair_row), entry,
+                                            S(L.rows), S(L.row_dbase), S(L.tile_row0),
+                                            d.per_view, d.hw);
+    k_rows_end<<<1, 64, 0, stream>>>(hdr, S(L.tile_row0));
+    k_pair_rl<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, entry, S(L.tile_row0),
+                                        reinterpret_cast<uint32_t*>(S(L.pair_rl)));
+    k_mark_cells<<<(unsigned)((n_intervals + 255) / 256 + 1), 256, 0, stream>>>(hdr, S(L.cell_out),
+                                                                              d.cells, occ);
+  }
+
+  // 5. empty cells
+  const dim3 cgrid((unsigned)((d.cells + kPrepTile - 1) / kPrepTile));
+  EmptyCells ec{occ, d.cells, S(L.empty), L.n_empty};
+  k_compact_count<<<cgrid, block, 0, stream>>>(ec, tiles);
+  scan_exclusive(tiles, (int64_t)cgrid.x, sums, hdr + kHdrEmpty, stream);
+  k_compact_scatter<<<cgrid, block, 0, stream>>>(ec, tiles);
   if (n_valid == 0) return hipGetLastError();
 
-  // regroup by (BEV rank, feature rank, plan position)
-  const unsigned g256 = (unsigned)((n_valid + 255) / 256);
-  k_sched_rf_keys<<<g256, 256, 0, stream>>>(rd, n_valid, d.per_view, d.hw, W(L.ws_keys_a),
-                                            W(L.ws_vals_a));
-  const bool in_b = radix_sort_pairs(W(L.ws_keys_a), W(L.ws_vals_a), W(L.ws_keys_b), W(L.ws_vals_b),
-                                     hdr + kHdrValid, L.ntiles, L.rf_bits, W(L.ws_hist), sums, stream);
-  int32_t* k0 = in_b ? W(L.ws_keys_b) : W(L.ws_keys_a);
-  int32_t* v0 = in_b ? W(L.ws_vals_b) : W(L.ws_vals_a);
-  int32_t* k1 = in_b ? W(L.ws_keys_a) : W(L.ws_keys_b);
-  int32_t* v1 = in_b ? W(L.ws_vals_a) : W(L.ws_vals_b);
-  k_sched_rb_keys<<<g256, 256, 0, stream>>>(rb, v0, n_valid, k0);
-  const bool in_1 = radix_sort_pairs(k0, v0, k1, v1, hdr + kHdrValid, L.ntiles, L.rb_bits,
-                                     W(L.ws_hist), sums, stream);
-  const int32_t* vals = in_1 ? v1 : v0;
-
-  // pairs
-  const dim3 grid((unsigned)L.ntiles), block(kPrepThreads);
-  int32_t* head_pos = W(L.ws_head);
-  PairHeads ph{rd, rb, vals, hdr, d.per_view, d.hw, S(L.pair_rd0), S(L.pair_cell), head_pos};
-  k_compact_count<<<grid, block, 0, stream>>>(ph, tiles);
-  scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrPairs, stream);
-  k_compact_scatter<<<grid, block, 0, stream>>>(ph, tiles);
-
-  // occupied cells
-  CellHeads ch{S(L.pair_cell), hdr, S(L.cell_id), S(L.cell_pair), n_intervals};
-  k_compact_count<<<grid, block, 0, stream>>>(ch, tiles);
-  scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
-  k_compact_scatter<<<grid, block, 0, stream>>>(ch, tiles);
-  k_sched_sentinels<<<1, 64, 0, stream>>>(hdr, head_pos, S(L.cell_pair));
-  k_pair_npts<<<g256, 256, 0, stream>>>(head_pos, hdr, S(L.pair_npts));
-
-  // tasks, work items in task order, and the per-die item ranges
-  k_sched_tasks<<<(unsigned)((n_intervals + 1 + 255) / 256), 256, 0, stream>>>(
-      S(L.cell_pair), hdr, n_intervals, S(L.task_cell));
-  const int maxk = schedule_max_chunks(d);
-  int32_t* count = tiles;                 // [tasks_cap]: items per task, then their offsets
-  int32_t* work = tiles + L.tasks_cap;    // [items_cap]: work per item, then its prefix
-  const unsigned gt = (unsigned)((L.tasks_cap + 255) / 256);
-  k_item_counts<<<gt, 256, 0, stream>>>(S(L.cell_pair), S(L.task_cell), hdr, L.tasks_cap, maxk,
-                                        count);
-  scan_exclusive(count, L.tasks_cap, sums, hdr + kHdrItems, stream);
-  k_item_scatter<<<gt, 256, 0, stream>>>(S(L.cell_pair), S(L.task_cell), hdr, maxk, count,
-                                         S(L.item_info), S(L.item_chunk), work);
+  // 6. items and per-die ranges
+  const SliceCounts sk = slice_counts(d);
+  const int64_t tcap = n_intervals + 1;
+  int32_t* count = tiles;          // [tcap]: items per tile, then their offsets
+  int32_t* work = tiles + tcap;    // [items_cap]: work per item, then its prefix
+  const unsigned gt = (unsigned)((tcap + 255) / 256);
+  k_item_counts<<<gt, 256, 0, stream>>>(hdr, S(L.tile_row0), d.C, sk, tcap, count);
+  scan_exclusive(count, tcap, sums, hdr + kHdrItems, stream);
+  k_item_scatter<<<gt, 256, 0, stream>>>(hdr, S(L.tile_cell), S(L.cell_pair), S(L.tile_row0), d.C,
+                                         sk, count, S(L.item_tile), S(L.item_slice), work);
   k_item_work_tail<<<(unsigned)((L.items_cap + 255) / 256), 256, 0, stream>>>(hdr, work,
                                                                             L.items_cap);
   scan_exclusive(work, L.items_cap, sums, hdr + kHdrWork, stream);

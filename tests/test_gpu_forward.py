@@ -12,6 +12,7 @@ import pytest
 import torch
 
 import _gpu
+import _sched
 import oracle
 from paper_2211_17111_amd import bevpool as bp
 from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
@@ -105,6 +106,36 @@ def test_forward_edge_cases(path):
         assert np.all(out.cpu().numpy().reshape(-1, 80)[~occupied] == 0.0), label
 
 
+@pytest.mark.parametrize("case", ["one cell in batches", "many small cells", "wide fp16 channels",
+                                  "wide fp32 channels"])
+def test_forward_tile_paths(case, path):
+    """Shapes that drive the scheduled kernel through its less common paths:
+    a single cell with more pairs than one LDS batch, tiles cut by the cell
+    cap, and channel counts needing several 64-lane sub-slices."""
+    rng = np.random.default_rng(5)
+    dtype = "f32"
+    if case == "one cell in batches":
+        shape = dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1)
+        P = 48000
+        coor = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
+        coor[rng.random(P) < 0.1] = -1       # some points out of range
+    elif case == "many small cells":
+        shape = dict(B=1, N=2, D=3, H=30, W=40, C=80, X=64, Y=64, Z=1)
+        coor = random_coor(rng, shape, p_out=0.2)
+    elif case == "wide fp16 channels":
+        shape = dict(B=1, N=2, D=5, H=6, W=7, C=520, X=6, Y=5, Z=1)
+        coor = random_coor(rng, shape, p_out=0.2)
+        dtype = "f16"
+    else:
+        shape = dict(B=1, N=2, D=5, H=6, W=7, C=1024, X=6, Y=5, Z=1)
+        coor = random_coor(rng, shape, p_out=0.2)
+    data = draw_small(rng, shape, dtype=dtype)
+    _gpu.say(f"forward tile path: {case} {path}")
+    out, _ = _run(data["depth"], data["feat"], coor, shape, path=path)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+    _gpu.assert_within(out.float().cpu().numpy(), ref, mag, dtype, case)
+
+
 def test_forward_nan_free_and_empty_exact_zero(path):
     # Poison the output buffer first: every element must be overwritten.
     cfg = CONFIGS["bevdet"]
@@ -191,30 +222,47 @@ def test_forward_with_oracle_plan():
     _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", "oracle plan")
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
-def test_schedule_counts(name):
-    """The schedule's pair, task and item counts against a numpy derivation
-    from the oracle's plan.  A pair is a maximal run of kept points with the
-    same BEV rank, the same pixel and consecutive depth bins."""
-    cfg = CONFIGS[name]
-    coor = frustum_coor(cfg)
-    plan = _gpu.run_prepare(coor, cfg.shape())
+def _check_schedule(coor, shape, label):
+    plan = _gpu.run_prepare(coor, shape)
     sched = bp.schedule(plan)
-    hdr = sched.header()
-    ref = oracle.prepare_ref(coor, cfg.shape())
-    rb = ref["ranks_bev"].astype(np.int64)
-    rf = ref["ranks_feat"].astype(np.int64)
-    rd = ref["ranks_depth"].astype(np.int64)
-    o = np.lexsort((rd, rf, rb))
-    rb, rf, rd = rb[o], rf[o], rd[o]
-    hw = cfg.H * cfg.W
-    head = np.ones(rb.size, dtype=bool)
-    head[1:] = (rb[1:] != rb[:-1]) | (rf[1:] != rf[:-1]) | (rd[1:] != rd[:-1] + hw)
-    n_pairs = int(head.sum())
-    n_tasks = -(-n_pairs // 2048)
-    assert hdr[0] == n_pairs and hdr[1] == n_tasks
-    assert hdr[3] == ref["n_valid"] and hdr[4] == ref["n_intervals"] and hdr[5] == ref["n_intervals"]
-    assert n_tasks <= hdr[2] <= 2 * n_tasks + 1
+    ref_plan = oracle.prepare_ref(coor, shape)
+    got = _sched.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
+    want = _sched.derive(ref_plan, shape)
+    assert got["n"] == want["n"], (label, got["n"], want["n"])
+    for k in want:
+        if k != "n":
+            np.testing.assert_array_equal(got[k], want[k], err_msg=f"{label}: {k}")
+    return want
+
+
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
+def test_schedule_matches_numpy(name):
+    """Every array of the GPU-built schedule against a numpy derivation from
+    the oracle's plan (integer data: bit-exact)."""
+    cfg = CONFIGS[name]
+    _gpu.say(f"schedule vs numpy: {name}")
+    want = _check_schedule(frustum_coor(cfg), cfg.shape(), name)
+    if name == "headline":
+        # the tiles' rows are shared by several pairs: fewer staged rows than pairs
+        assert want["n"]["row_entries"] < 0.5 * want["n"]["pairs"]
+
+
+def test_schedule_edge_shapes():
+    rng = np.random.default_rng(11)
+    shapes = [
+        dict(B=2, N=2, D=9, H=7, W=13, C=17, X=12, Y=10, Z=2),   # C not a multiple of 8
+        dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1),   # few cells, many pairs
+        dict(B=1, N=2, D=3, H=30, W=40, C=80, X=64, Y=64, Z=1),  # many cells of few pairs
+        dict(B=3, N=1, D=4, H=5, W=6, C=16, X=300, Y=7, Z=3),    # X, Y far apart
+    ]
+    for i, shape in enumerate(shapes):
+        _gpu.say(f"schedule edge shape {i}: {shape}")
+        _check_schedule(random_coor(rng, shape, p_out=0.3), shape, f"shape {i}")
+    shape = shapes[1]
+    P = shape["B"] * shape["N"] * shape["D"] * shape["H"] * shape["W"]
+    one = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
+    want = _check_schedule(one, shape, "one cell")
+    assert want["n"]["pairs"] > 4096   # one cell processed in several batches
 
 
 def test_scheduled_matches_ranges():
