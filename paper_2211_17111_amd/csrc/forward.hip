@@ -217,9 +217,21 @@ __global__ __launch_bounds__(kFwdThreads) void k_fwd_cells(TOut* __restrict__ ou
   const int64_t r0 = s / a.RG, r1 = (s + len - 1) / a.RG;
   if (r0 != r1) {
     const int64_t col = (int64_t)(cbase + vi) * VEC;
-    float sum[VEC], t[VEC];
+    // partials added in range order; eight loads in flight per step
+    float sum[VEC];
     Vec<float, VEC>::load(a.part_b + r0 * C + col, sum);
-    for (int64_t r = r0 + 1; r <= r1; ++r) {
+    int64_t r = r0 + 1;
+    for (; r + 8 <= r1 + 1; r += 8) {
+      float t[8][VEC];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) Vec<float, VEC>::load(a.part_a + (r + k) * C + col, t[k]);
+#pragma unroll
+      for (int k = 0; k < 8; ++k)
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) sum[e] += t[k][e];
+    }
+    for (; r <= r1; ++r) {
+      float t[VEC];
       Vec<float, VEC>::load(a.part_a + r * C + col, t);
 #pragma unroll
       for (int e = 0; e < VEC; ++e) sum[e] += t[e];
