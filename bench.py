@@ -111,6 +111,9 @@ def main():
     ap.add_argument("--forward", choices=["interval", "tiled"], default="interval",
                     help="forward entry point timed as the metric: bevpool_forward (interval table) "
                          "or bevpool_forward_scheduled (tiled schedule); the other is reported too")
+    ap.add_argument("--backward", choices=["plan", "scheduled"], default="scheduled",
+                    help="backward entry point used in the steps: bevpool_backward (plan arrays) or "
+                         "bevpool_backward_scheduled")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also launch one plain 256 MiB device copy (hardware-counter calibration)")
     args = ap.parse_args()
@@ -180,9 +183,15 @@ def main():
     forward = paths[args.forward]
     other_name = "tiled" if args.forward == "interval" else "interval"
 
-    def backward(s):
+    def backward_plan(s):
         bp.bevpool_backward(shape, code, ocode, s.grad_out, s.depth, s.feat, s.rd, s.rb, nv, s.gd, s.gf,
                             ws_b, ws_b_bytes, stream)
+
+    def backward_scheduled(s):
+        bp.bevpool_backward_scheduled(shape, code, ocode, s.grad_out, s.depth, s.feat, s.sched,
+                                      sched_bytes, nv, ni, s.gd, s.gf, stream)
+
+    backward = backward_scheduled if args.backward == "scheduled" else backward_plan
 
     # ---- whole-path steps ------------------------------------------------
     def step(i, ev=None):
@@ -328,6 +337,7 @@ def main():
             "forward_host_enqueue_us": host_us,
             "forward_warm_region_ms_per_launch": warm_region,
             "forward_path": args.forward,
+            "backward_path": args.backward,
             f"forward_{other_name}_cold_ms": float(cold_oth.mean()),
             f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,

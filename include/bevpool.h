@@ -210,6 +210,21 @@ int bevpool_backward(const bevpool_shape* shape, int in_dtype, int out_dtype,
                      int32_t n_valid, void* grad_depth, void* grad_feat,
                      void* workspace, size_t workspace_bytes, void* stream);
 
+/* The same gradients from a schedule (bevpool_schedule of the same plan and
+ * shape), which lists every pixel's pairs of kept points: each pixel's
+ * feature row is read once and each pair (a cell and a run of consecutive
+ * depth bins of the pixel) reads its grad_out row once.  grad_depth is
+ * cleared first and the kept points are then written (every element once in
+ * its final value, dropped points +0.0), grad_feat is written once per
+ * element.  No workspace; no atomics (deterministic).  Arguments as for
+ * bevpool_backward and bevpool_forward_scheduled; an all-zero result when
+ * n_valid or n_intervals is 0 (schedule may then be NULL). */
+int bevpool_backward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                               const void* grad_out, const void* depth, const void* feat,
+                               const void* schedule, size_t schedule_bytes, int32_t n_valid,
+                               int32_t n_intervals, void* grad_depth, void* grad_feat,
+                               void* stream);
+
 #ifdef __cplusplus
 } /* extern "C" */
 #endif

@@ -11,8 +11,10 @@ from .bevpool import (  # noqa: F401
     Plan,
     Schedule,
     backward,
+    backward_scheduled,
     bev_pool,
     bevpool_backward,
+    bevpool_backward_scheduled,
     bevpool_backward_workspace_size,
     bevpool_forward,
     bevpool_forward_scheduled,

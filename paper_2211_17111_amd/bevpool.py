@@ -80,6 +80,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_backward.restype = ctypes.c_int
     lib.bevpool_backward.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, vp, i32,
                                      vp, vp, vp, sz, vp]
+    lib.bevpool_backward_scheduled.restype = ctypes.c_int
+    lib.bevpool_backward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, sz,
+                                               i32, i32, vp, vp, vp]
     if path is None:
         _lib = lib
     return lib
@@ -225,6 +228,19 @@ def bevpool_backward(shape, in_dtype, out_dtype, grad_out, depth, feat, ranks_de
            "bevpool_backward")
 
 
+def bevpool_backward_scheduled(shape, in_dtype, out_dtype, grad_out, depth, feat, schedule,
+                               schedule_bytes, n_valid, n_intervals, grad_depth, grad_feat,
+                               stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_backward_scheduled(ctypes.byref(s), int(in_dtype), int(out_dtype),
+                                               _ptr(grad_out), _ptr(depth), _ptr(feat),
+                                               _ptr(schedule), int(schedule_bytes), int(n_valid),
+                                               int(n_intervals), _ptr(grad_depth), _ptr(grad_feat),
+                                               _stream(stream)),
+           "bevpool_backward_scheduled")
+
+
 # ------------------------------------------------------------ allocating helpers
 
 @dataclass
@@ -362,6 +378,21 @@ def backward(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor, pl
     bevpool_backward(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[grad_out.dtype], grad_out, depth, feat,
                      plan.ranks_depth, plan.ranks_bev, plan.n_valid, gd, gf, workspace,
                      workspace.numel() * workspace.element_size(), stream)
+    return gd, gf
+
+
+def backward_scheduled(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor,
+                       sched: Schedule, stream=None):
+    plan = sched.plan
+    sd = plan.shape
+    _require(grad_out, "grad_out")
+    _require(depth, "depth")
+    _require(feat, "feat", depth.dtype)
+    gd = torch.empty_like(depth)
+    gf = torch.empty_like(feat)
+    bevpool_backward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[grad_out.dtype], grad_out,
+                               depth, feat, sched.buffer, sched.buffer.numel(), plan.n_valid,
+                               plan.n_intervals, gd, gf, stream)
     return gd, gf
 
 

@@ -312,4 +312,34 @@ int bevpool_backward(const bevpool_shape* shape, int in_dtype, int out_dtype,
                   "bevpool_backward");
 }
 
+int bevpool_backward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                               const void* grad_out, const void* depth, const void* feat,
+                               const void* schedule, size_t schedule_bytes, int32_t n_valid,
+                               int32_t n_intervals, void* grad_depth, void* grad_feat,
+                               void* stream) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_dtypes(in_dtype, out_dtype);
+  if (st != BEVPOOL_OK) return st;
+  st = check_counts(d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(grad_out);
+  REQUIRE_PTR(depth);
+  REQUIRE_PTR(feat);
+  REQUIRE_PTR(grad_depth);
+  REQUIRE_PTR(grad_feat);
+  if (n_valid > 0 && n_intervals > 0) {
+    REQUIRE_PTR(schedule);
+    const size_t need = bevpool::schedule_layout(d, n_valid, n_intervals).total;
+    if (schedule_bytes < need)
+      return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
+                  schedule_bytes, need);
+  }
+  return from_hip(bevpool::launch_backward_scheduled(d, in_dtype, out_dtype, grad_out, depth, feat,
+                                                     schedule, n_valid, n_intervals, grad_depth,
+                                                     grad_feat, static_cast<hipStream_t>(stream)),
+                  "bevpool_backward_scheduled");
+}
+
 }  // extern "C"

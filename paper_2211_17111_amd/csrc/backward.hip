@@ -2,8 +2,10 @@
 //   grad_depth[p]  = <grad_out[cell(p), :], feat[pixel(p), :]>   (0 if p dropped)
 //   grad_feat[f,:] = sum over kept p of pixel f of depth[p] * grad_out[cell(p), :]
 //
-// Both are produced by one pixel-major pass so every output element is
-// written exactly once, without atomics:
+// Two implementations, both writing every output element exactly once and
+// without atomics (deterministic).
+//
+// From the plan alone (bevpool_backward):
 //   1. k_fill + k_point_map scatter the plan back into frustum-index order,
 //      map[p] = BEV rank of p, or -1 when p was dropped;
 //   2. k_backward gives each feature-map pixel to a group of GS lanes (GS a
@@ -12,6 +14,17 @@
 //      upstream-gradient row of each kept point's cell, reduces the dot
 //      product across the group for grad_depth and accumulates
 //      depth * grad_out for grad_feat.
+//
+// From a schedule (bevpool_backward_scheduled), which lists every pixel's
+// pairs (a cell and a run of consecutive depth bins):
+//   1. k_zero_vec clears grad_depth (coalesced), so dropped points are 0;
+//   2. k_bwd_pixels gives each pixel to a group of GS lanes holding its
+//      feature row; lane l of the group takes pair l of the current chunk
+//      and sums that pair's depth scores; the group then walks the chunk,
+//      reading one grad_out row per pair (a pair's points share their cell),
+//      reducing the dot product with the feature row across the group, which
+//      is grad_depth of every point of the pair, and adding the pair's depth
+//      sum times the row to grad_feat.
 
 #include "device_utils.h"
 #include "internal.h"
@@ -163,6 +176,153 @@ hipError_t run_nv(const Dims& d, const void* grad_out, const void* depth, const 
   return run<TIn, TG, VEC, 16>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
 }
 
+
+template <typename T, int VEC>
+__global__ __launch_bounds__(256) void k_zero_vec(T* __restrict__ a, int64_t nvec) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nvec) store_zero<T, VEC>(a + i * VEC);
+}
+
+struct PixArgs {
+  const int32_t* pix_pair0;
+  const int32_t* bp_cell;
+  const uint32_t* bp_dn;
+  int32_t C, D, hw;
+  int32_t n_pairs;
+  int64_t per_view, rows, cells;
+};
+
+constexpr int kPixUnroll = 4;  // grad_out rows in flight per group
+
+template <typename TIn, typename TG, int VEC, int NV>
+__global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
+    const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
+    TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a, int GS) {
+  const int lane = lane_id();
+  const int G = kWave / GS;
+  const int g = lane / GS;
+  const int vi = lane - g * GS;
+  const int64_t f = ((int64_t)blockIdx.x * kBwdWaves + threadIdx.x / kWave) * G + g;
+  if (f >= a.rows) return;  // whole groups leave together
+  const int C = a.C;
+  const int CV = C / VEC;
+
+  float fv[NV][VEC], acc[NV][VEC];
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int v = vi + k * GS;
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[k][e] = fv[k][e] = 0.f;
+    if (v < CV) Vec<TIn, VEC>::load(feat + f * C + (int64_t)v * VEC, fv[k]);
+  }
+  const int32_t p_begin = max(a.pix_pair0[f], 0);
+  const int32_t p_end = min(a.pix_pair0[f + 1], a.n_pairs);
+  const int64_t dbase = (f / a.hw) * a.per_view + f % a.hw;  // depth rank at bin 0
+
+  for (int32_t pb = p_begin; pb < p_end; pb += GS) {
+    // lane vi: pair pb + vi -- its cell, depth run and summed depth score
+    int32_t my_cell = -1;
+    uint32_t my_dn = 0;
+    float my_w = 0.f;
+    if (pb + vi < p_end) {
+      const int32_t c = a.bp_cell[pb + vi];
+      const uint32_t dn = a.bp_dn[pb + vi];
+      const int32_t d0 = (int32_t)(dn & 0xffffu), n = (int32_t)(dn >> 16);
+      if (c >= 0 && c < a.cells && d0 + n <= a.D) {
+        my_cell = c;
+        my_dn = dn;
+        for (int32_t q = 0; q < n; ++q) my_w += to_float(depth[dbase + (int64_t)(d0 + q) * a.hw]);
+      }
+    }
+    const int cnt = min(GS, p_end - pb);
+    for (int j0 = 0; j0 < cnt; j0 += kPixUnroll) {
+      int32_t cell[kPixUnroll];
+      uint32_t dn[kPixUnroll];
+      float w[kPixUnroll];
+      float gv[kPixUnroll][NV][VEC];
+#pragma unroll
+      for (int u = 0; u < kPixUnroll; ++u) {
+        const int src = g * GS + ((j0 + u) & (GS - 1));
+        cell[u] = __shfl(my_cell, src);
+        dn[u] = (uint32_t)__shfl((int32_t)my_dn, src);
+        w[u] = __shfl(my_w, src);
+        if (j0 + u >= cnt) cell[u] = -1;
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+          const int v = vi + k * GS;
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) gv[u][k][e] = 0.f;
+          if (cell[u] >= 0 && v < CV)
+            Vec<TG, VEC>::load(grad_out + (int64_t)cell[u] * C + (int64_t)v * VEC, gv[u][k]);
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kPixUnroll; ++u) {
+        float part = 0.f;
+#pragma unroll
+        for (int k = 0; k < NV; ++k)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) {
+            part = fmaf(gv[u][k][e], fv[k][e], part);
+            acc[k][e] = fmaf(w[u], gv[u][k][e], acc[k][e]);
+          }
+        for (int o = GS >> 1; o > 0; o >>= 1) part += __shfl_xor(part, o);
+        if (cell[u] >= 0) {
+          const int32_t d0 = (int32_t)(dn[u] & 0xffffu), n = (int32_t)(dn[u] >> 16);
+          for (int32_t q = vi; q < n; q += GS)
+            grad_depth[dbase + (int64_t)(d0 + q) * a.hw] = (TIn)part;
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int k = 0; k < NV; ++k) {
+    const int v = vi + k * GS;
+    if (v < CV) Vec<TIn, VEC>::store(grad_feat + f * C + (int64_t)v * VEC, acc[k]);
+  }
+}
+
+template <typename TIn, typename TG, int VEC, int NV>
+hipError_t run_pixels(const Dims& d, const void* grad_out, const void* depth, const void* feat,
+                      const PixArgs& a, void* grad_depth, void* grad_feat, hipStream_t stream) {
+  const int CV = (int)d.C / VEC;
+  const int per_lane = (CV + NV - 1) / NV;
+  int GS = 1;
+  while (GS < per_lane) GS <<= 1;
+  const int G = kWave / GS;
+  const int64_t pix_per_block = (int64_t)G * kBwdWaves;
+  const dim3 grid((unsigned)((d.rows + pix_per_block - 1) / pix_per_block));
+  k_bwd_pixels<TIn, TG, VEC, NV><<<grid, dim3(kBwdThreads), 0, stream>>>(
+      static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
+      static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat),
+      a, GS);
+  return hipGetLastError();
+}
+
+template <typename TIn, typename TG, int VEC>
+hipError_t run_pixels_nv(const Dims& d, const void* grad_out, const void* depth, const void* feat,
+                         const PixArgs& a, void* grad_depth, void* grad_feat, hipStream_t stream) {
+  const int64_t CV = d.C / VEC;
+  if (CV <= 64) return run_pixels<TIn, TG, VEC, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  if (CV <= 128) return run_pixels<TIn, TG, VEC, 2>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  if (CV <= 256) return run_pixels<TIn, TG, VEC, 4>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  if (CV <= 512) return run_pixels<TIn, TG, VEC, 8>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  return run_pixels<TIn, TG, VEC, 16>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+}
+
+template <typename T>
+hipError_t zero_fill(T* a, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15u) == 0 && n % (16 / sizeof(T)) == 0) {
+    constexpr int V = 16 / sizeof(T);
+    const int64_t nvec = n / V;
+    k_zero_vec<T, V><<<dim3((unsigned)((nvec + 255) / 256)), dim3(256), 0, stream>>>(a, nvec);
+  } else {
+    k_zero_vec<T, 1><<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream>>>(a, n);
+  }
+  return hipGetLastError();
+}
+
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
@@ -195,6 +355,47 @@ hipError_t launch_backward(const Dims& d, int in_dtype, int out_dtype, const voi
   if (al && d.C % 8 == 0)
     return run_nv<half_t, float, 8>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
   return run_nv<half_t, float, 1>(d, grad_out, depth, feat, map, grad_depth, grad_feat, stream);
+}
+
+
+hipError_t launch_backward_scheduled(const Dims& d, int in_dtype, int out_dtype,
+                                     const void* grad_out, const void* depth, const void* feat,
+                                     const void* schedule, int32_t n_valid, int32_t n_intervals,
+                                     void* grad_depth, void* grad_feat, hipStream_t stream) {
+  const bool f32 = in_dtype == BEVPOOL_F32;
+  hipError_t e = f32 ? zero_fill(static_cast<float*>(grad_depth), d.P, stream)
+                     : zero_fill(static_cast<half_t*>(grad_depth), d.P, stream);
+  if (e != hipSuccess) return e;
+  if (n_valid == 0 || n_intervals == 0)  // no kept point: grad_feat is zero too
+    return f32 ? zero_fill(static_cast<float*>(grad_feat), d.rows * d.C, stream)
+               : zero_fill(static_cast<half_t*>(grad_feat), d.rows * d.C, stream);
+  const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
+  const char* sc = static_cast<const char*>(schedule);
+  PixArgs a;
+  a.pix_pair0 = reinterpret_cast<const int32_t*>(sc + L.pix_pair0);
+  a.bp_cell = reinterpret_cast<const int32_t*>(sc + L.bp_cell);
+  a.bp_dn = reinterpret_cast<const uint32_t*>(sc + L.bp_dn);
+  a.C = (int32_t)d.C;
+  a.D = (int32_t)d.D;
+  a.hw = (int32_t)d.hw;
+  a.n_pairs = n_valid;  // pairs never outnumber kept points
+  a.per_view = d.per_view;
+  a.rows = d.rows;
+  a.cells = d.cells;
+  const bool al = aligned16(grad_out) && aligned16(feat) && aligned16(grad_feat);
+  if (f32) {
+    if (al && d.C % 4 == 0)
+      return run_pixels_nv<float, float, 4>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+    return run_pixels_nv<float, float, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  }
+  if (out_dtype == BEVPOOL_F16) {
+    if (al && d.C % 8 == 0)
+      return run_pixels_nv<half_t, half_t, 8>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+    return run_pixels_nv<half_t, half_t, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  }
+  if (al && d.C % 8 == 0)
+    return run_pixels_nv<half_t, float, 8>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+  return run_pixels_nv<half_t, float, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
 }
 
 }  // namespace bevpool

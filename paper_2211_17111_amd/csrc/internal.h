@@ -78,6 +78,9 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //   rows[n_valid]            feature rank of each row entry
 //   row_dbase[n_valid]       depth rank of each row entry's pixel at depth bin 0
 //   empty[cells - n_occ + 1] BEV rank of each empty cell, ascending
+//   bp_cell[n_valid]         pixel-major pairs (the same pairs sorted by feature
+//   bp_dn[n_valid]             rank, then cell key): BEV rank, and d0 | points << 16
+//   pix_pair0[rows + 1]      first pixel-major pair of each feature row
 //   item_tile[items_cap]     tile of each item, in tile order
 //   item_slice[items_cap]    k | (K << 16)
 //   xcd_begin[kXcds + 1]     first item of each XCD: contiguous item ranges of
@@ -114,7 +117,7 @@ int tile_max_cells(const Dims& d);
 
 struct ScheduleLayout {
   size_t header, pair_rl, pair_dn, cell_out, cell_pair, tile_cell, tile_row0, rows, row_dbase, empty,
-      item_tile, item_slice, xcd_begin, total;
+      bp_cell, bp_dn, pix_pair0, item_tile, item_slice, xcd_begin, total;
   int64_t n_valid, n_occ, n_empty, items_cap;
   // build workspace
   size_t ws_ka, ws_va, ws_kb, ws_vb, ws_head, ws_pair_rb, ws_pair_row, ws_flags, ws_tiles,
@@ -146,5 +149,9 @@ hipError_t launch_backward(const Dims& d, int in_dtype, int out_dtype, const voi
                            const void* depth, const void* feat, const int32_t* rd,
                            const int32_t* rb, int32_t n_valid, void* grad_depth,
                            void* grad_feat, void* workspace, hipStream_t stream);
+hipError_t launch_backward_scheduled(const Dims& d, int in_dtype, int out_dtype,
+                                     const void* grad_out, const void* depth, const void* feat,
+                                     const void* schedule, int32_t n_valid, int32_t n_intervals,
+                                     void* grad_depth, void* grad_feat, hipStream_t stream);
 
 }  // namespace bevpool

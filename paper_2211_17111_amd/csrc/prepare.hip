@@ -344,7 +344,9 @@ __global__ __launch_bounds__(256) void k_interval_lengths(const int32_t* __restr
 //   4. the distinct rows of each tile: pairs sorted by (tile, row), heads of
 //      equal runs, and each pair's index into its tile's row list;
 //   5. the empty cells, by compaction of an occupancy map;
-//   6. items per tile, their work, and per-die item ranges.
+//   6. items per tile, their work, and per-die item ranges;
+//   7. the pairs again in pixel-major order (for the backward pass), with
+//      the first pair of every feature row.
 
 // Generic ordered compaction over the same 4096-element tiles as the filter:
 // Op provides count(), flag(i), and emit(i, position) (called for flagged i,
@@ -543,6 +545,48 @@ __device__ __forceinline__ int32_t upper_index(const int32_t* __restrict__ a, in
     if (a[mid] <= v) lo = mid; else hi = mid - 1;
   }
   return lo;
+}
+
+
+// Pixel-major pairs: gather the cell and depth run of pair vals[q].
+__global__ __launch_bounds__(256) void k_pix_pairs(const int32_t* __restrict__ hdr,
+                                                   const int32_t* __restrict__ vals,
+                                                   const int32_t* __restrict__ pair_rb,
+                                                   const uint32_t* __restrict__ pair_dn,
+                                                   int32_t* __restrict__ bp_cell,
+                                                   uint32_t* __restrict__ bp_dn) {
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= hdr[kHdrPairs]) return;
+  const int32_t a = vals[q];
+  bp_cell[q] = pair_rb[a];
+  bp_dn[q] = pair_dn[a];
+}
+
+// pix_pair0[f] = first pixel-major pair whose feature row is >= f, for f in
+// [0, rows]; `keys` holds the feature row of every pixel-major pair.
+__global__ __launch_bounds__(256) void k_pix_offsets(const int32_t* __restrict__ hdr,
+                                                     const int32_t* __restrict__ keys, int64_t rows,
+                                                     int32_t* __restrict__ pix_pair0) {
+  const int64_t f = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (f > rows) return;
+  int32_t lo = 0, hi = hdr[kHdrPairs];
+  while (lo < hi) {
+    const int32_t mid = (lo + hi) >> 1;
+    if (keys[mid] < f) lo = mid + 1; else hi = mid;
+  }
+  pix_pair0[f] = lo;
+}
+
+
+__global__ __launch_bounds__(256) void k_pair_row_keys(const int32_t* __restrict__ hdr,
+                                                       const int32_t* __restrict__ pair_row,
+                                                       int32_t* __restrict__ keys,
+                                                       int32_t* __restrict__ vals) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < hdr[kHdrPairs]) {
+    keys[p] = pair_row[p];
+    vals[p] = (int32_t)p;
+  }
 }
 
 // Tile of every pair (into pair_tile) and the (row, pair) keys of the row sort.
@@ -909,6 +953,9 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.rows = take(nv);
   L.row_dbase = take(nv);
   L.empty = take((size_t)L.n_empty + 1);
+  L.bp_cell = take(nv);
+  L.bp_dn = take(nv);
+  L.pix_pair0 = take((size_t)d.rows + 1);
   L.item_tile = take((size_t)L.items_cap);
   L.item_slice = take((size_t)L.items_cap);
   L.xcd_begin = take(kXcds + 1);
@@ -988,6 +1035,17 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
     scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
     k_compact_scatter<<<grid, block, 0, stream>>>(ch, tiles);
     k_cells_end<<<1, 64, 0, stream>>>(hdr, S(L.cell_pair));
+
+    // 7 (done here, while each pair's BEV rank is at hand). Stable sort by
+    // feature rank keeps the cell-key order within a pixel.
+    k_pair_row_keys<<<g_nv, 256, 0, stream>>>(hdr, W(L.ws_pair_row), W(L.ws_ka), W(L.ws_va));
+    const bool x_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
+                                      hdr + kHdrPairs, L.ntiles, L.row_bits, hist, sums, stream);
+    k_pix_pairs<<<g_nv, 256, 0, stream>>>(hdr, x_b ? W(L.ws_vb) : W(L.ws_va), W(L.ws_pair_rb),
+                                          pair_dn, S(L.bp_cell),
+                                          reinterpret_cast<uint32_t*>(S(L.bp_dn)));
+    k_pix_offsets<<<(unsigned)((d.rows + 1 + 255) / 256), 256, 0, stream>>>(
+        hdr, x_b ? W(L.ws_kb) : W(L.ws_ka), d.rows, S(L.pix_pair0));
 
     // 3. tiles
     TileHeads th{S(L.cell_pair), hdr, S(L.tile_cell), tile_max_cells(d)};

@@ -83,9 +83,11 @@ def layout(shape, n_valid: int, n_occ: int) -> dict:
     nocc = n_occ + 1
     n_empty = max(cells - n_occ, 0)
     items_cap = (n_occ + 1) * slice_counts(shape["C"])[-1]
+    rows = shape["B"] * shape["N"] * shape["H"] * shape["W"]
     sizes = [("header", 16), ("pair_rl", nv), ("pair_dn", nv), ("cell_out", nocc),
              ("cell_pair", nocc), ("tile_cell", nocc), ("tile_row0", nocc), ("rows", nv),
-             ("row_dbase", nv), ("empty", n_empty + 1), ("item_tile", items_cap), ("item_slice", items_cap),
+             ("row_dbase", nv), ("empty", n_empty + 1), ("bp_cell", nv), ("bp_dn", nv),
+             ("pix_pair0", rows + 1), ("item_tile", items_cap), ("item_slice", items_cap),
              ("xcd_begin", XCDS + 1)]
     off, out = 0, {}
     for name, n in sizes:
@@ -116,6 +118,9 @@ def decode(buf: np.ndarray, shape, n_valid: int, n_occ: int) -> dict:
         rows=arr["rows"][:n["row_entries"]].astype(np.int64),
         row_dbase=arr["row_dbase"][:n["row_entries"]].astype(np.int64),
         empty=arr["empty"][:n["empty"]].astype(np.int64),
+        bp_cell=arr["bp_cell"][:np_].astype(np.int64),
+        bp_dn=arr["bp_dn"][:np_].view(np.uint32).astype(np.int64),
+        pix_pair0=arr["pix_pair0"].astype(np.int64),
         item_tile=arr["item_tile"][:n["items"]].astype(np.int64),
         item_slice=arr["item_slice"][:n["items"]].astype(np.int64),
         xcd_begin=arr["xcd_begin"].astype(np.int64),
@@ -164,6 +169,11 @@ def derive(plan: dict, shape) -> dict:
     entry = np.searchsorted(tr[:, 0] * (1 << 32) + tr[:, 1], pair_tile * (1 << 32) + p_row)
     pair_rl = entry - tile_row0[pair_tile]
     pair_dn = p_d0 | (npts << 16)
+    # pixel-major pairs: stable by feature row (cell-key order kept within a pixel)
+    po = np.argsort(p_row, kind="stable")
+    bp_cell, bp_dn = p_rb[po], pair_dn[po]
+    n_rows = shape["B"] * shape["N"] * H * W
+    pix_pair0 = np.searchsorted(p_row[po], np.arange(n_rows + 1), side="left")
     occ = np.zeros(cells, dtype=bool)
     occ[cell_out] = True
     empty = np.flatnonzero(~occ)
@@ -195,5 +205,6 @@ def derive(plan: dict, shape) -> dict:
                work=total),
         pair_rl=pair_rl, pair_dn=pair_dn, cell_out=cell_out, cell_pair=cell_pair,
         tile_cell=tile_cell, tile_row0=tile_row0, rows=rows, row_dbase=row_dbase, empty=empty,
+        bp_cell=bp_cell, bp_dn=bp_dn, pix_pair0=pix_pair0,
         item_tile=np.array(item_tile, dtype=np.int64), item_slice=np.array(item_slice, dtype=np.int64),
         xcd_begin=np.array(xcd, dtype=np.int64))

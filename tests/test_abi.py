@@ -32,7 +32,7 @@ def test_exports_every_declared_symbol(lib):
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
         "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
         "bevpool_forward_scheduled",
-        "bevpool_backward_workspace_size", "bevpool_backward",
+        "bevpool_backward_workspace_size", "bevpool_backward", "bevpool_backward_scheduled",
     }
     for n in names:
         assert hasattr(lib, n), n
@@ -173,3 +173,12 @@ def test_schedule_validation(lib):
     assert f(sc=None) == EINVAL
     assert f(sb=16) == EINVAL
     assert f(out=None) == EINVAL
+    b = lambda **k: lib.bevpool_backward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0),
+                                                   k.get("g", DUMMY), DUMMY, DUMMY, k.get("sc", DUMMY),
+                                                   k.get("sb", sb.value), 1000, 100, DUMMY,
+                                                   k.get("gf", DUMMY), None)
+    assert b(i=0, o=1) == EDTYPE
+    assert b(g=None) == EINVAL
+    assert b(sc=None) == EINVAL
+    assert b(sb=16) == EINVAL
+    assert b(gf=None) == EINVAL

@@ -11,22 +11,35 @@ from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coo
 
 pytestmark = pytest.mark.gpu
 
+PATHS = ["plan", "scheduled"]
 
-def _run(data, coor, shape):
+
+@pytest.fixture(params=PATHS)
+def path(request):
+    return request.param
+
+
+def _bwd(path, g, d, f, plan):
+    if path == "scheduled":
+        return bp.backward_scheduled(g, d, f, bp.schedule(plan))
+    return bp.backward(g, d, f, plan)
+
+
+def _run(data, coor, shape, path="plan"):
     plan = _gpu.run_prepare(coor, shape)
-    gd, gf = bp.backward(_gpu.to_dev(data["grad_out"]), _gpu.to_dev(data["depth"]),
-                         _gpu.to_dev(data["feat"]), plan)
+    gd, gf = _bwd(path, _gpu.to_dev(data["grad_out"]), _gpu.to_dev(data["depth"]),
+                  _gpu.to_dev(data["feat"]), plan)
     torch.cuda.synchronize()
     return gd, gf, plan
 
 
 @pytest.mark.parametrize("name", ["tiny", "bevdet"])
-def test_backward_full(name):
+def test_backward_full(name, path):
     cfg = CONFIGS[name]
-    _gpu.say(f"backward full parity: {name}")
+    _gpu.say(f"backward full parity: {name} {path}")
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
-    gd, gf, _ = _run(data, coor, cfg.shape())
+    gd, gf, _ = _run(data, coor, cfg.shape(), path)
     rgd, rgf, mgd, mgf = oracle.backward_ref(data["grad_out"], data["depth"], data["feat"], coor,
                                              cfg.shape())
     _gpu.assert_within(gd.cpu().numpy(), rgd, mgd, cfg.dtype, f"{name} grad_depth")
@@ -37,19 +50,19 @@ def test_backward_full(name):
 
 @pytest.mark.parametrize("C", [1, 3, 16, 17, 80, 260])
 @pytest.mark.parametrize("dtype,out_dtype", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
-def test_backward_random_channels(C, dtype, out_dtype):
+def test_backward_random_channels(C, dtype, out_dtype, path):
     shape = dict(B=2, N=2, D=9, H=7, W=13, C=C, X=12, Y=10, Z=2)
     rng = np.random.default_rng(50 + C)
     coor = random_coor(rng, shape, p_out=0.4)
     data = draw_small(rng, shape, dtype=dtype, out_dtype=out_dtype)
-    _gpu.say(f"backward random C={C} {dtype}/{out_dtype}")
-    gd, gf, _ = _run(data, coor, shape)
+    _gpu.say(f"backward random C={C} {dtype}/{out_dtype} {path}")
+    gd, gf, _ = _run(data, coor, shape, path)
     rgd, rgf, mgd, mgf = oracle.backward_ref(data["grad_out"], data["depth"], data["feat"], coor, shape)
     _gpu.assert_within(gd.float().cpu().numpy(), rgd, mgd, dtype, f"C={C} grad_depth")
     _gpu.assert_within(gf.float().cpu().numpy(), rgf, mgf, dtype, f"C={C} grad_feat")
 
 
-def test_backward_edge_cases():
+def test_backward_edge_cases(path):
     shape = dict(B=1, N=2, D=70, H=6, W=10, C=16, X=4, Y=4, Z=1)   # D > 64 depth chunks
     P = 2 * 70 * 60
     rng = np.random.default_rng(3)
@@ -60,8 +73,8 @@ def test_backward_edge_cases():
         "random": random_coor(rng, shape),
     }
     for label, coor in cases.items():
-        _gpu.say(f"backward edge case: {label}")
-        gd, gf, _ = _run(data, coor, shape)
+        _gpu.say(f"backward edge case: {label} {path}")
+        gd, gf, _ = _run(data, coor, shape, path)
         rgd, rgf, mgd, mgf = oracle.backward_ref(data["grad_out"], data["depth"], data["feat"],
                                                  coor, shape)
         _gpu.assert_within(gd.cpu().numpy(), rgd, mgd, "f32", f"{label} grad_depth")
@@ -69,12 +82,12 @@ def test_backward_edge_cases():
 
 
 @pytest.mark.parametrize("name", ["headline", "large", "train"])
-def test_backward_full_size_sampled(name):
+def test_backward_full_size_sampled(name, path):
     cfg = CONFIGS[name]
-    _gpu.say(f"backward sampled parity: {name}")
+    _gpu.say(f"backward sampled parity: {name} {path}")
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
-    gd, gf, plan = _run(data, coor, cfg.shape())
+    gd, gf, plan = _run(data, coor, cfg.shape(), path)
     rng = np.random.default_rng(11)
     # points: random, plus every point of the longest interval
     st = plan.interval_starts.cpu().numpy()
@@ -110,14 +123,34 @@ def test_backward_full_size_sampled(name):
     assert abs(lhs - rhs_f) <= tol * scale, (lhs, rhs_f, scale)
 
 
-def test_backward_deterministic():
+def test_backward_deterministic(path):
     cfg = CONFIGS["train"]
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
-    gd1, gf1, plan = _run(data, coor, cfg.shape())
-    gd2, gf2 = bp.backward(_gpu.to_dev(data["grad_out"]), _gpu.to_dev(data["depth"]),
-                           _gpu.to_dev(data["feat"]), plan)
+    gd1, gf1, plan = _run(data, coor, cfg.shape(), path)
+    gd2, gf2 = _bwd(path, _gpu.to_dev(data["grad_out"]), _gpu.to_dev(data["depth"]),
+                    _gpu.to_dev(data["feat"]), plan)
     assert torch.equal(gd1, gd2) and torch.equal(gf1, gf2)
+
+
+def test_backward_paths_agree_on_poisoned_outputs():
+    """Both backward entry points overwrite every element (NaN-poisoned
+    outputs come back finite) and agree to fp32 rounding."""
+    cfg = CONFIGS["bevdet"]
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg)
+    plan = _gpu.run_prepare(coor, cfg.shape())
+    g, d, f = (_gpu.to_dev(data[k]) for k in ("grad_out", "depth", "feat"))
+    sched = bp.schedule(plan)
+    gd = torch.full_like(d, float("nan"))
+    gf = torch.full_like(f, float("nan"))
+    bp.bevpool_backward_scheduled(cfg.shape(), bp.BEVPOOL_F32, bp.BEVPOOL_F32, g, d, f, sched.buffer,
+                                  sched.buffer.numel(), plan.n_valid, plan.n_intervals, gd, gf)
+    torch.cuda.synchronize()
+    assert torch.isfinite(gd).all() and torch.isfinite(gf).all()
+    gd2, gf2 = bp.backward(g, d, f, plan)
+    assert float((gd - gd2).abs().max()) <= 1e-5 * float(gd2.abs().max()) + 1e-6
+    assert float((gf - gf2).abs().max()) <= 1e-5 * float(gf2.abs().max()) + 1e-6
 
 
 def test_autograd_wrapper_tiny():
