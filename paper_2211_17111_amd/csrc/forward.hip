@@ -37,7 +37,7 @@ namespace {
 constexpr int kFwdThreads = 256;
 constexpr int kFwdWaves = kFwdThreads / kWave;
 constexpr int kUnroll = 8;
-constexpr int kMetaPerWave = 512;  // points staged in LDS per wavefront
+constexpr int kMetaPerWave = 256;  // points staged in LDS per wavefront
 
 struct FwdArgs {
   const int32_t* rd;
