@@ -13,7 +13,7 @@ plan, output) whose total size is several times the 256 MB Infinity Cache, so
 every launch reads its inputs from HBM.  Each launch is bracketed by HIP
 events on the stream it runs on.  The achieved bandwidth divides the
 algorithmic bytes of one forward by that latency.  --forward picks the entry
-point timed as the metric (interval-table or tiled-schedule forward); the
+point timed as the metric (interval-table or strip-schedule forward); the
 other one is timed the same way and reported beside it.
 
 The CPU baseline is the float64 oracle timed on the host: whole forwards of
@@ -47,8 +47,8 @@ HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 * 2 ** 20
 PMC_FILE = os.path.join(ROOT, "profiles", "forward_headline_traffic.txt")
 # kernels of each forward path (the interval path is two launches, timed together)
-FORWARD_KERNELS = {"interval": "k_fwd_ranges+k_fwd_cells", "tiled": "k_fwd_tiles"}
-FORWARD_SOURCES = ("forward.hip", "forward_tiles.hip", "internal.h", "vec.h", "device_utils.h")
+FORWARD_KERNELS = {"interval": "k_fwd_ranges+k_fwd_cells", "strips": "k_fwd_strips+k_fwd_combine"}
+FORWARD_SOURCES = ("forward.hip", "forward_strips.hip", "internal.h", "vec.h", "device_utils.h")
 
 
 def log(msg):
@@ -108,9 +108,9 @@ def main():
     ap.add_argument("--fwd-launches", type=int, default=320)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle sample (0: skip the CPU baseline)")
-    ap.add_argument("--forward", choices=["interval", "tiled"], default="interval",
+    ap.add_argument("--forward", choices=["interval", "strips"], default="interval",
                     help="forward entry point timed as the metric: bevpool_forward (interval table) "
-                         "or bevpool_forward_scheduled (tiled schedule); the other is reported too")
+                         "or bevpool_forward_scheduled (strip schedule); the other is reported too")
     ap.add_argument("--backward", choices=["plan", "scheduled"], default="scheduled",
                     help="backward entry point used in the steps: bevpool_backward (plan arrays) or "
                          "bevpool_backward_scheduled")
@@ -170,18 +170,22 @@ def main():
     for s in sets:
         prepare(s)
     torch.cuda.synchronize()
+    n_slots = int(sets[0].sched[:64].view(torch.int32)[7])
+    ws_fs_bytes = bp.bevpool_forward_scheduled_workspace_size(shape, n_slots)
+    ws_fs = torch.empty(max(ws_fs_bytes, 16), dtype=torch.uint8, device=dev)
+    log(f"schedule: {n_slots} slots ({ws_fs_bytes / 2**20:.1f} MiB workspace)")
 
-    def forward_tiled(s):
+    def forward_strips(s):
         bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, nv, ni,
-                                     s.out, stream)
+                                     s.out, ws_fs, ws_fs_bytes, stream)
 
     def forward_interval(s):
         bp.bevpool_forward(shape, code, ocode, s.depth, s.feat, s.rd, s.rf, s.rb, s.st, s.ln, nv, ni,
                            s.out, ws_f, ws_f_bytes, stream)
 
-    paths = {"interval": forward_interval, "tiled": forward_tiled}
+    paths = {"interval": forward_interval, "strips": forward_strips}
     forward = paths[args.forward]
-    other_name = "tiled" if args.forward == "interval" else "interval"
+    other_name = "strips" if args.forward == "interval" else "interval"
 
     def backward_plan(s):
         bp.bevpool_backward(shape, code, ocode, s.grad_out, s.depth, s.feat, s.rd, s.rb, nv, s.gd, s.gf,

@@ -153,30 +153,54 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
                     size_t workspace_bytes, void* stream);
 
 /*
- * Forward schedule (optional, built once per plan like the plan itself).
+ * Schedule (optional): a regrouping of the plan of section 2.1, built once
+ * offline like the plan itself.
  *
- * The schedule regroups the kept points of a plan by (cell, pixel): when
- * several depth bins of one pixel fall into the same cell, their depth scores
- * are summed first and the pixel's feature row is read once.  It also cuts
- * the regrouped points into work items that each own whole cells, splitting
- * a large task into channel slices instead of point ranges, so the scheduled
- * forward needs no cross-item reduction.
+ * The schedule regroups the kept points of a plan by image strips: blocks of
+ * bh x bw feature pixels of one camera image, normally whole pixel columns
+ * (the frustum points of a pixel column lie in one vertical plane, so a
+ * strip's points fall into few BEV cells).  Within a strip, kept points of one
+ * pixel in one cell over consecutive depth bins form a pair: their depth
+ * scores are summed first and the pixel's feature row is read once.  A
+ * strip's pairs are cut into items of at most a few thousand pairs, and an
+ * item's pairs into segments (one per cell).  A cell covered by one segment
+ * is written directly; a cell covered by several has one partial-sum slot per
+ * segment in the forward's workspace, added in a fixed order.
  *
  * bevpool_schedule_size gives the schedule buffer size and the build
  * workspace size for a plan with n_valid kept points and n_intervals
  * occupied cells.  bevpool_schedule reads the first n_valid entries of
  * ranks_depth and ranks_bev of a plan from bevpool_prepare and writes the
- * schedule (device memory owned by the caller; opaque layout).  Enqueued on
- * `stream`; deterministic.
+ * schedule (device memory owned by the caller).  Enqueued on `stream`;
+ * deterministic.  The schedule starts with BEVPOOL_SCHEDULE_HEADER int32
+ * counts, indexed by bevpool_schedule_count; the rest is opaque.  A caller
+ * reads the header back once (after the build has completed) to size the
+ * forward's workspace.
  *
  * bevpool_forward_scheduled computes exactly what bevpool_forward computes
- * (same layouts, dtypes and zero-filled empty cells, every element written
- * once, no atomics, bitwise reproducible) from the schedule alone; n_valid
- * and n_intervals must be the values the schedule was built with.  It needs
- * no workspace and leaves the schedule unchanged, so concurrent forwards may
- * share one schedule.  A schedule whose cell count does not match n_intervals
- * leaves `out` unwritten.
+ * (same layouts, dtypes and zero-filled empty cells, every element of `out`
+ * written once, no atomics, bitwise reproducible) from the schedule alone;
+ * n_valid and n_intervals must be the values the schedule was built with.
+ * Its workspace holds the slots: bevpool_forward_scheduled_workspace_size
+ * bytes for the header's BEVPOOL_SCHEDULE_SLOTS count (float32 rows of C;
+ * may be 0 bytes and NULL when that count is 0).  The workspace contents are
+ * scratch: one forward at a time per workspace; the schedule is only read, so
+ * concurrent forwards may share it.  The size cannot be checked without
+ * reading the schedule: cells whose slots lie beyond a too small workspace
+ * are written as NaN (nothing is written outside the workspace).  A schedule
+ * whose cell count does not match n_intervals leaves `out` unwritten.
  */
+#define BEVPOOL_SCHEDULE_HEADER 16
+enum bevpool_schedule_count {
+  BEVPOOL_SCHEDULE_PAIRS = 0,
+  BEVPOOL_SCHEDULE_ITEMS = 1,
+  BEVPOOL_SCHEDULE_SEGMENTS = 2,
+  BEVPOOL_SCHEDULE_KEPT = 3,        /* n_valid the schedule was built with */
+  BEVPOOL_SCHEDULE_CELLS = 4,       /* n_intervals the schedule was built with */
+  BEVPOOL_SCHEDULE_CELLS_FOUND = 5, /* occupied cells found in the plan */
+  BEVPOOL_SCHEDULE_EMPTY = 6,
+  BEVPOOL_SCHEDULE_SLOTS = 7
+};
 int bevpool_schedule_size(const bevpool_shape* shape, int32_t n_valid,
                           int32_t n_intervals, size_t* schedule_bytes,
                           size_t* workspace_bytes);
@@ -184,10 +208,13 @@ int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
                      const int32_t* ranks_bev, int32_t n_valid, int32_t n_intervals,
                      void* schedule, size_t schedule_bytes, void* workspace,
                      size_t workspace_bytes, void* stream);
+int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t n_slots,
+                                              size_t* bytes);
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
                               size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
-                              void* out, void* stream);
+                              void* out, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /*
  * Gradients of bevpool_forward (not in the paper; chain rule):

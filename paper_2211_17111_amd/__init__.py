@@ -18,6 +18,7 @@ from .bevpool import (  # noqa: F401
     bevpool_backward_workspace_size,
     bevpool_forward,
     bevpool_forward_scheduled,
+    bevpool_forward_scheduled_workspace_size,
     bevpool_forward_workspace_size,
     bevpool_last_error,
     bevpool_prepare,
@@ -29,6 +30,7 @@ from .bevpool import (  # noqa: F401
     declared_symbols,
     forward,
     forward_scheduled,
+    forward_scheduled_workspace,
     load_library,
     prepare,
     schedule,

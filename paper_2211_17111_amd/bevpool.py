@@ -73,8 +73,10 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_schedule.restype = ctypes.c_int
     lib.bevpool_schedule.argtypes = [shp, vp, vp, i32, i32, vp, sz, vp, sz, vp]
     lib.bevpool_forward_scheduled.restype = ctypes.c_int
+    lib.bevpool_forward_scheduled_workspace_size.restype = ctypes.c_int
+    lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
-                                              vp, vp]
+                                              vp, vp, sz, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -198,14 +200,24 @@ def bevpool_schedule(shape, ranks_depth, ranks_bev, n_valid, n_intervals, schedu
            "bevpool_schedule")
 
 
+def bevpool_forward_scheduled_workspace_size(shape, n_slots) -> int:
+    lib = load_library()
+    n = ctypes.c_size_t(0)
+    _check(lib, lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(make_shape(shape)),
+                                                             int(n_slots), ctypes.byref(n)),
+           "bevpool_forward_scheduled_workspace_size")
+    return n.value
+
+
 def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
-                              n_valid, n_intervals, out, stream=None) -> None:
+                              n_valid, n_intervals, out, workspace, workspace_bytes,
+                              stream=None) -> None:
     lib = load_library()
     s = make_shape(shape)
     _check(lib, lib.bevpool_forward_scheduled(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
                                               _ptr(feat), _ptr(schedule), int(schedule_bytes),
                                               int(n_valid), int(n_intervals), _ptr(out),
-                                              _stream(stream)),
+                                              _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
 
 
@@ -320,13 +332,19 @@ def forward(depth: torch.Tensor, feat: torch.Tensor, plan: Plan, out_dtype=None,
 
 @dataclass
 class Schedule:
-    """Device buffer of a forward schedule built from a plan."""
+    """Device buffer of a schedule built from a plan, with its header counts."""
     plan: Plan
     buffer: torch.Tensor
+    counts: list[int]
 
     def header(self) -> list[int]:
-        """Counts the schedule recorded: pairs, tasks, items, n_valid, cells, cells found."""
-        return self.buffer[:64].view(torch.int32)[:8].cpu().tolist()
+        """The 16 header counts (pairs, items, segments, kept points, cells, cells found,
+        empty cells, slots, ...), read back from the device."""
+        return self.buffer[:64].view(torch.int32).cpu().tolist()
+
+    @property
+    def n_slots(self) -> int:
+        return self.counts[7]
 
 
 def schedule(plan: Plan, stream=None) -> Schedule:
@@ -337,16 +355,24 @@ def schedule(plan: Plan, stream=None) -> Schedule:
     ws = torch.empty(max(wb, 1), dtype=torch.uint8, device=dev)
     bevpool_schedule(plan.shape, plan.ranks_depth, plan.ranks_bev, plan.n_valid, plan.n_intervals,
                      buf, sb, ws, wb, stream)
-    sch = Schedule(plan, buf)
+    sch = Schedule(plan, buf, [0] * 16)
     if plan.n_valid > 0:
-        hdr = sch.header()
+        hdr = sch.header()  # synchronises with the build
         if hdr[3] != plan.n_valid or hdr[5] != plan.n_intervals:
             raise BevpoolError(-1, "bevpool_schedule", f"schedule counts {hdr} do not match the plan")
+        sch.counts = hdr
     return sch
 
 
+def forward_scheduled_workspace(sched: Schedule) -> torch.Tensor:
+    """Workspace for forward_scheduled: one float32 row of C per slot of the schedule."""
+    n = bevpool_forward_scheduled_workspace_size(sched.plan.shape, sched.n_slots)
+    return torch.empty(max(n, 16), dtype=torch.uint8, device=sched.buffer.device)
+
+
 def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, out_dtype=None,
-                      out: torch.Tensor | None = None, stream=None) -> torch.Tensor:
+                      out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                      stream=None) -> torch.Tensor:
     plan = sched.plan
     sd = plan.shape
     B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
@@ -358,8 +384,11 @@ def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, 
     if out is None:
         out = torch.empty((B, Z, Y, X, C), dtype=odt, device=depth.device)
     _require(out, "out", odt)
+    if workspace is None:
+        workspace = forward_scheduled_workspace(sched)
     bevpool_forward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, sched.buffer,
-                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, out, stream)
+                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, out, workspace,
+                              workspace.numel() * workspace.element_size(), stream)
     return out
 
 

@@ -244,10 +244,21 @@ int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
                   "bevpool_schedule");
 }
 
+int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t n_slots,
+                                              size_t* bytes) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(bytes);
+  if (n_slots < 0) return fail(BEVPOOL_EINVAL, "n_slots = %d is negative", n_slots);
+  *bytes = bevpool::forward_scheduled_workspace_bytes(d, n_slots);
+  return ok();
+}
+
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
                               size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
-                              void* out, void* stream) {
+                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);
   if (st != BEVPOOL_OK) return st;
@@ -264,9 +275,12 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
     if (schedule_bytes < need)
       return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
                   schedule_bytes, need);
+    if (workspace == nullptr && workspace_bytes > 0)
+      return fail(BEVPOOL_EWORKSPACE, "workspace of %zu bytes at NULL", workspace_bytes);
   }
   return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, depth, feat, schedule,
-                                                    n_valid, n_intervals, out,
+                                                    n_valid, n_intervals, out, workspace,
+                                                    workspace_bytes,
                                                     static_cast<hipStream_t>(stream)),
                   "bevpool_forward_scheduled");
 }

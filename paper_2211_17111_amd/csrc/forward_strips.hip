@@ -1,0 +1,643 @@
+// Scheduled BEVPoolv2 pooling: the same sum as bevpool_forward (section 2.1),
+// driven by a strip schedule built once from the plan (prepare.hip; the
+// layout is described in internal.h).
+//
+// A strip is a block of image pixels, normally whole pixel columns of one
+// camera.  The frustum points of a pixel column lie in one vertical plane, so
+// a strip's kept points fall into few BEV cells, and the strip's feature rows
+// are few enough to sit in LDS.  The work is therefore organised around the
+// image instead of the grid: every feature row is read from memory once per
+// item, every pair (one cell, one pixel, a run of consecutive depth bins)
+// reads its row from LDS, and only the cells a strip shares with its
+// neighbours need a second pass.
+//
+//   k_fwd_strips   one workgroup per (item, channel chunk of up to 64 vectors):
+//     1. copies the strip's feature rows (this chunk) into LDS with 16-byte
+//        loads; meanwhile loads the item's pair records and gathers their
+//        depth scores; each pair's weight (the sum of its points' scores),
+//        local pixel and segment go to LDS;
+//     2. cuts the item's pairs into equal ranges, one per lane group (one lane
+//        per vector of the chunk); each group sums weight x feature row over
+//        its range, reading both from LDS, and finishes a segment when the
+//        next pair belongs to another;
+//     3. a segment cut by range boundaries is added up in range order from
+//        partial sums left in LDS.  Each segment's sum is stored once: into
+//        `out` when the segment alone covers its cell, else into its slot.
+//   k_fwd_combine  one lane group per cell covered by several segments (adds
+//                  its slots in segment order and stores the cell) or per
+//                  empty cell (stores zeros).
+//
+// Every element of `out` is written exactly once and no atomics are used;
+// the summation order depends only on the schedule, so results are bitwise
+// reproducible.
+
+#include "device_utils.h"
+#include "internal.h"
+#include "vec.h"
+
+#include <algorithm>
+
+namespace bevpool {
+
+namespace {
+
+constexpr int kNT = 1024;  // threads of a strip workgroup (one per CU)
+constexpr int kWaves = kNT / kWave;
+constexpr int kPP = kItemPairs / kNT;  // pair records per thread
+constexpr int kDepthBurst = 4;         // depth scores per pair loaded before any is summed
+constexpr int kRowRegs = kStripBytes / 16 / kNT;  // 16-byte row vectors per thread in flight
+constexpr int kBufBytes = kStripBytes + kItemPairs * 12;  // rows | pair records | destinations
+constexpr int kHdrCache = 128;  // item headers of a workgroup kept in LDS
+constexpr int kUnroll = 4;             // pairs per step of the accumulation walk
+constexpr int kCombThreads = 256;
+static_assert(kItemPairs % kNT == 0, "pair records split evenly over the threads");
+static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
+
+struct StripArgs {
+  const int32_t* hdr;
+  const int32_t* pair_rd0;
+  const uint32_t* pair_ln;
+  const int32_t* item_strip;
+  const int32_t* item_pair0;
+  const int32_t* item_seg0;
+  const int32_t* seg_dest;
+  const int32_t* comb_cell;
+  const int32_t* comb_slot0;
+  const int32_t* empty;
+  float* slots;
+  int64_t slot_cap;  // slots the workspace holds
+  int32_t n_valid, n_occ, items_cap;
+  int32_t C, H, W, bh, bw, nhb, nwb, strips;
+  int32_t hw32;    // H * W
+  int64_t P, cells, n_empty;
+};
+
+struct PairRec {
+  float w;      // summed depth score
+  uint32_t ps;  // row offset (local pixel * vectors per row) | segment << 19 | kRecHead
+};
+constexpr uint32_t kRecHead = 1u << 31;  // first pair of a segment
+constexpr int kRecSegShift = 19;
+constexpr uint32_t kRecOff = (1u << kRecSegShift) - 1;
+static_assert(kItemPairs <= (1 << (31 - kRecSegShift)), "segment index fits its field");
+static_assert((int64_t)kStripBytes / 4 * kWave <= kRecOff + 1, "row offset fits its field");
+
+// Raw element vector moved between memory and LDS without conversion.
+template <typename T, int VEC>
+struct Raw {
+  typedef T type;
+};
+template <>
+struct Raw<float, 4> {
+  typedef float4_t type;
+};
+template <>
+struct Raw<half_t, 8> {
+  typedef half8_t type;
+};
+
+template <typename T, int VEC>
+__device__ __forceinline__ void raw_to_float(const typename Raw<T, VEC>::type& r, float* v);
+template <>
+__device__ __forceinline__ void raw_to_float<float, 1>(const float& r, float* v) { v[0] = r; }
+template <>
+__device__ __forceinline__ void raw_to_float<half_t, 1>(const half_t& r, float* v) {
+  v[0] = (float)r;
+}
+template <>
+__device__ __forceinline__ void raw_to_float<float, 4>(const float4_t& r, float* v) {
+  v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w;
+}
+template <>
+__device__ __forceinline__ void raw_to_float<half_t, 8>(const half8_t& r, float* v) {
+#pragma unroll
+  for (int e = 0; e < 8; ++e) v[e] = (float)r[e];
+}
+
+// Exclusive scan over the workgroup with LDS-only barriers; `lds` holds kWaves ints.
+__device__ __forceinline__ int group_exclusive_scan(int v, int* lds) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const int inc = wave_inclusive_scan(v);
+  if (lane == kWave - 1) lds[wid] = inc;
+  lds_barrier();
+  int off = 0;
+#pragma unroll
+  for (int w = 0; w < kWaves; ++w) off += (w < wid) ? lds[w] : 0;
+  return off + inc - v;
+}
+
+// An item's header, the same for the whole workgroup.
+struct ItemHdr {
+  int32_t strip, p0, np, g0, nseg;
+};
+
+template <typename TIn, typename TOut, int VEC>
+__global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ depth,
+                                                    const TIn* __restrict__ feat,
+                                                    TOut* __restrict__ out, StripArgs a) {
+  typedef typename Raw<TIn, VEC>::type RawT;
+  // two buffers of [rows, then partial sums | pair records | segment destinations]
+  __shared__ __attribute__((aligned(16))) char smem[2 * kBufBytes];
+  __shared__ int s_scan[kWaves];
+  __shared__ int32_t s_hdr[3][kHdrCache + 1];  // strip, first pair, first segment
+  static_assert((int64_t)kWaves * kWave * 8 * sizeof(float) <= kStripBytes, "partial sums fit the row area");
+  auto buf_rows = [&](int b) { return reinterpret_cast<RawT*>(smem + b * kBufBytes); };
+  auto buf_pr = [&](int b) { return reinterpret_cast<PairRec*>(smem + b * kBufBytes + kStripBytes); };
+  auto buf_dest = [&](int b) {
+    return reinterpret_cast<int32_t*>(smem + b * kBufBytes + kStripBytes + kItemPairs * sizeof(PairRec));
+  };
+
+  const int32_t* hdr = a.hdr;
+  if (hdr[kHdrOccFound] != a.n_occ || hdr[kHdrOcc] != a.n_occ) return;  // uniform
+  const int32_t n_items = min(hdr[kHdrItems], a.items_cap);
+  const int32_t n_pairs = min(hdr[kHdrPairs], a.n_valid);
+  const int32_t n_segs = min(hdr[kHdrSegs], a.n_valid);
+  // This workgroup's items: a contiguous share of its die's contiguous range,
+  // so a die's L2 serves neighbouring strips' shared depth lines.
+  const int xcd = blockIdx.x % kXcds;
+  const int slot = blockIdx.x / kXcds;
+  const int nslots = gridDim.x / kXcds;
+  const int per_die = (n_items + kXcds - 1) / kXcds;
+  const int d_lo = min(xcd * per_die, n_items);
+  const int d_cnt = min(n_items, d_lo + per_die) - d_lo;
+  const int i_begin = d_lo + (int)(((int64_t)slot * d_cnt) / nslots);
+  const int i_end = d_lo + (int)(((int64_t)(slot + 1) * d_cnt) / nslots);
+  if (i_begin >= i_end) return;
+
+  const int C = a.C;
+  const int CV = C / VEC;
+  const int cbase = blockIdx.y * kWave;
+  const int cvc = min(kWave, CV - cbase);
+  const int tid = threadIdx.x;
+  const int lane = lane_id();
+  const int wave = tid / kWave;
+  const int64_t hw = a.hw32;
+  const TIn* const fchunk = feat + (int64_t)cbase * VEC;
+
+  // item i's header (i clamped to this workgroup's items)
+  // Item headers, copied to LDS once (the launch gives no workgroup more
+  // than kHdrCache items; scalar loads share their wait counter with LDS
+  // reads, so loading headers inside the pipeline would stall every walk).
+  const int n_my = min(i_end - i_begin, kHdrCache);
+  for (int j = tid; j <= n_my; j += kNT) {
+    s_hdr[0][j] = j < n_my ? a.item_strip[i_begin + j] : 0;
+    s_hdr[1][j] = a.item_pair0[i_begin + j];
+    s_hdr[2][j] = a.item_seg0[i_begin + j];
+  }
+  lds_barrier();
+  // item i's header (i clamped to this workgroup's items)
+  auto header = [&](int i) {
+    i = min(max(i - i_begin, 0), n_my - 1);
+    int32_t v[5];
+    v[0] = s_hdr[0][i]; v[1] = s_hdr[1][i]; v[2] = s_hdr[1][i + 1];
+    v[3] = s_hdr[2][i]; v[4] = s_hdr[2][i + 1];
+    ItemHdr h;
+    h.strip = __builtin_amdgcn_readfirstlane(v[0]);
+    h.p0 = __builtin_amdgcn_readfirstlane(v[1]);
+    h.np = __builtin_amdgcn_readfirstlane(v[2]) - h.p0;
+    h.g0 = __builtin_amdgcn_readfirstlane(v[3]);
+    h.nseg = __builtin_amdgcn_readfirstlane(v[4]) - h.g0;
+    // (bitwise or: no branches)
+    const bool bad = (h.strip < 0) | (h.strip >= a.strips) | (h.p0 < 0) | (h.np < 1) |
+                     (h.np > kItemPairs) | (h.p0 + h.np > n_pairs) | (h.g0 < 0) | (h.nseg < 1) |
+                     (h.nseg > h.np) | (h.g0 + h.nseg > n_segs);
+    if (bad) h = ItemHdr{0, 0, 0, 0, 0};  // an inconsistent header becomes an empty item
+    return h;
+  };
+  struct Geo {
+    int64_t origin;
+    int bws, npix;
+  };
+  auto geometry = [&](int strip) {
+    const int32_t sper = a.nhb * a.nwb;
+    const int32_t bn = strip / sper;
+    const int32_t sr = strip - bn * sper;
+    const int32_t hb = sr / a.nwb, wb = sr - hb * a.nwb;
+    const int32_t h0 = hb * a.bh, w0 = wb * a.bw;
+    Geo g;
+    g.bws = min(a.bw, a.W - w0);
+    g.npix = min(a.bh, a.H - h0) * g.bws;
+    g.origin = ((int64_t)bn * a.H + h0) * a.W + w0;
+    return g;
+  };
+  auto vec_addr = [&](const Geo& g, int idx) {
+    const int lp = idx / cvc;
+    const int vi = idx - lp * cvc;
+    const int lh = lp / g.bws;
+    const int64_t row = g.origin + (int64_t)lh * a.W + (lp - lh * g.bws);
+    return reinterpret_cast<const RawT*>(fchunk + row * C + (int64_t)vi * VEC);
+  };
+
+  // Loads are unconditional where they can be, surplus lanes repeating an
+  // in-range address: a load under a branch makes the compiler wait for it
+  // where the branch joins.
+  struct Recs {
+    int32_t rd0[kPP];
+    uint32_t ln[kPP];
+  };
+  auto load_recs = [&](const ItemHdr& h, Recs& r) {
+#pragma unroll
+    for (int q = 0; q < kPP; ++q) {
+      const int k = min(tid * kPP + q, max(h.np - 1, 0));
+      r.rd0[q] = a.pair_rd0[h.p0 + k];
+      r.ln[q] = a.pair_ln[h.p0 + k];
+    }
+  };
+  struct Stage {
+    RawT rv[kRowRegs];
+    int32_t dst[kPP];
+    float dv[kPP][kDepthBurst];
+  };
+  // global loads of an item's rows, segment destinations and depth scores
+  auto issue_stage = [&](const ItemHdr& h, const Recs& r, Stage& st) {
+    const Geo g = geometry(h.strip);
+    const int nvec = g.npix * cvc;
+#pragma unroll
+    for (int u = 0; u < kRowRegs; ++u) st.rv[u] = *vec_addr(g, min(u * kNT + tid, nvec - 1));
+#pragma unroll
+    for (int q = 0; q < kPP; ++q)
+      st.dst[q] = a.seg_dest[h.g0 + min(q * kNT + tid, max(h.nseg - 1, 0))];
+#pragma unroll
+    for (int q = 0; q < kPP; ++q) {
+      const int n = tid * kPP + q < h.np ? (int)(r.ln[q] >> 16) : 0;
+#pragma unroll
+      for (int j = 0; j < kDepthBurst; ++j) {
+        const int64_t p = (int64_t)r.rd0[q] + j * hw;
+        float v = 0.f;
+        if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
+        st.dv[q][j] = v;
+      }
+    }
+  };
+  // an item's rows, destinations and pair records into LDS buffer b
+  auto commit_stage = [&](const ItemHdr& h, const Recs& r, const Stage& st, int b) {
+    const Geo g = geometry(h.strip);
+    const int nvec = g.npix * cvc;
+    RawT* const s_rows = buf_rows(b);
+    PairRec* const s_pr = buf_pr(b);
+    int32_t* const s_dest = buf_dest(b);
+#pragma unroll
+    for (int u = 0; u < kRowRegs; ++u) {
+      const int idx = u * kNT + tid;
+      if (idx < nvec) s_rows[idx] = st.rv[u];
+    }
+    for (int idx = kRowRegs * kNT + tid; idx < nvec; idx += kNT) s_rows[idx] = *vec_addr(g, idx);
+#pragma unroll
+    for (int q = 0; q < kPP; ++q) {
+      const int j = q * kNT + tid;
+      if (j < h.nseg) s_dest[j] = st.dst[q];
+    }
+    float wsum[kPP];
+    int heads = 0;
+#pragma unroll
+    for (int q = 0; q < kPP; ++q) {
+      const bool live = tid * kPP + q < h.np;
+      const int n = live ? (int)(r.ln[q] >> 16) : 0;
+      // (no constant start: an add of 0.f would be folded into the load's branch)
+      float sum = st.dv[q][0];
+#pragma unroll
+      for (int j = 1; j < kDepthBurst; ++j) sum += st.dv[q][j];
+      for (int j = kDepthBurst; j < n; ++j) {
+        const int64_t p = (int64_t)r.rd0[q] + j * hw;
+        if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+      }
+      wsum[q] = sum;
+      heads += (live && (r.ln[q] & kPairHead)) ? 1 : 0;
+    }
+    int seg = group_exclusive_scan(heads, s_scan) - 1;
+#pragma unroll
+    for (int q = 0; q < kPP; ++q) {
+      const int k = tid * kPP + q;
+      if (k < h.np) {
+        const bool head = (r.ln[q] & kPairHead) != 0;
+        if (head) ++seg;
+        const uint32_t lp = r.ln[q] & kPairPixel;
+        const bool ok = lp < (uint32_t)g.npix;
+        PairRec rec;
+        rec.w = ok ? wsum[q] : 0.f;
+        rec.ps = (ok ? lp * (uint32_t)cvc : 0u) |
+                 ((uint32_t)min(max(seg, 0), h.nseg - 1) << kRecSegShift) | (head ? kRecHead : 0u);
+        s_pr[k] = rec;
+      }
+    }
+  };
+
+  // lane group lg of the wave owns an equal range of each item's pairs
+  const int gpw = kWave / cvc;
+  const int G = kWaves * gpw;
+  const int lg = lane / cvc;
+  const int vi = lane - lg * cvc;
+  const int g = wave * gpw + lg;
+  const bool active = lg < gpw;
+  const int64_t col = (int64_t)(cbase + vi) * VEC;
+
+  // sums an item's segments from LDS buffer b and stores each once
+  auto walk_item = [&](const ItemHdr& h, int b) {
+    const RawT* const s_lane = buf_rows(b) + vi;
+    const PairRec* const s_pr = buf_pr(b);
+    const int32_t* const s_dest = buf_dest(b);
+    const int np = h.np;
+    auto range_begin = [&](int gg) { return (gg * np) / G; };  // below 2^31: G <= kNT
+    auto is_head = [&](int k) { return (s_pr[k].ps & kRecHead) != 0; };
+    auto seg_at = [&](int k) { return (int)((s_pr[k].ps & ~kRecHead) >> kRecSegShift); };
+    auto store_seg = [&](int sgi, const float* v) {
+      const int32_t d = s_dest[min(sgi, h.nseg - 1)];
+      if (d >= 0) {
+        if (d < a.cells) Vec<TOut, VEC>::store(out + (int64_t)d * C + col, v);
+      } else {
+        const int64_t sl = (int64_t)(~d);
+        if (sl < a.slot_cap) Vec<float, VEC>::store(a.slots + sl * C + col, v);
+      }
+    };
+
+    int kb = 0, ke = 0, last_seg = -1;
+    bool prev_cont = false, next_cont = false;
+    float acc[VEC], first_sum[VEC], last_sum[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = first_sum[e] = last_sum[e] = 0.f;
+    if (active) {
+      kb = range_begin(g);
+      ke = range_begin(g + 1);
+    }
+    if (kb < ke) {
+      // a range that starts inside a segment owes that segment's part to the
+      // group holding its start (kept in first_sum); one that ends inside a
+      // segment keeps the part in last_sum and adds the other groups' parts
+      prev_cont = !is_head(kb);
+      next_cont = ke < np && !is_head(ke);
+      last_seg = seg_at(ke - 1);
+      int cur = seg_at(kb);
+      bool pend_first = prev_cont;
+      auto end_segment = [&]() {  // segment `cur` has no more pairs in this range
+        if (pend_first) {
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) first_sum[e] = acc[e];
+          pend_first = false;
+        } else {
+          store_seg(cur, acc);
+        }
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+        ++cur;
+      };
+      int k0 = kb;
+      for (; k0 + kUnroll <= ke; k0 += kUnroll) {
+        // records first, then rows: two LDS round trips per kUnroll pairs
+        PairRec r[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) r[u] = s_pr[k0 + u];
+        float x[kUnroll][VEC];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) raw_to_float<TIn, VEC>(s_lane[r[u].ps & kRecOff], x[u]);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+          if ((r[u].ps & kRecHead) && k0 + u != kb) end_segment();
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) acc[e] = fmaf(r[u].w, x[u][e], acc[e]);
+        }
+      }
+      for (; k0 < ke; ++k0) {
+        const PairRec r = s_pr[k0];
+        float x[VEC];
+        raw_to_float<TIn, VEC>(s_lane[r.ps & kRecOff], x);
+        if ((r.ps & kRecHead) && k0 != kb) end_segment();
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = fmaf(r.w, x[e], acc[e]);
+      }
+      // the range's last segment
+      if (pend_first) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) first_sum[e] = acc[e];
+      } else if (next_cont) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) last_sum[e] = acc[e];
+      } else {
+        store_seg(cur, acc);
+      }
+    }
+
+    // segments cut by range boundaries, added in range order
+    lds_barrier();  // every group is done reading the rows, which now hold partials
+    // [G][cvc][VEC]: each group's part of the segment it starts inside
+    float* const part_a = reinterpret_cast<float*>(buf_rows(b));
+    const bool has_last = next_cont && !(prev_cont && seg_at(kb) == last_seg);
+    if (prev_cont) Vec<float, VEC>::store(part_a + ((int64_t)g * cvc + vi) * VEC, first_sum);
+    lds_barrier();
+    if (has_last) {
+      float sum[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) sum[e] = last_sum[e];
+      for (int g2 = g + 1; g2 < G; ++g2) {
+        const int b2 = range_begin(g2), e2 = range_begin(g2 + 1);
+        if (b2 >= e2) continue;
+        if (is_head(b2)) break;
+        float t[VEC];
+        Vec<float, VEC>::load(part_a + ((int64_t)g2 * cvc + vi) * VEC, t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) sum[e] += t[e];
+        // on to the next range only if this one lies wholly inside the segment
+        if (!(seg_at(e2 - 1) == last_seg && e2 < np && !is_head(e2))) break;
+      }
+      store_seg(last_seg, sum);
+    }
+  };
+
+  // ---- software pipeline over the items: while item i is walked from one
+  // LDS buffer, the loads of item i + 1 (issued before the walk) are in
+  // flight and the pair records of item i + 2 are on their way.
+  ItemHdr hc = header(i_begin);
+  ItemHdr hn = header(i_begin + 1);
+  Recs rc, rn;
+  load_recs(hc, rc);
+  load_recs(hn, rn);
+  Stage st;
+  issue_stage(hc, rc, st);
+  commit_stage(hc, rc, st, 0);
+  lds_barrier();
+  int b = 0;
+  for (int i = i_begin; i < i_begin + n_my; ++i) {
+    const ItemHdr hn2 = header(i + 2);
+    Recs rn2;
+    load_recs(hn2, rn2);
+    issue_stage(hn, rn, st);  // item i + 1 (repeats the last item at the end: unused)
+    walk_item(hc, b);
+    if (i + 1 < i_begin + n_my) commit_stage(hn, rn, st, b ^ 1);
+    lds_barrier();
+    hc = hn;
+    hn = hn2;
+    rn = rn2;
+    b ^= 1;
+  }
+}
+
+template <typename TOut, int VEC>
+__global__ __launch_bounds__(kCombThreads) void k_fwd_combine(TOut* __restrict__ out,
+                                                              StripArgs a) {
+  const int32_t* hdr = a.hdr;
+  if (hdr[kHdrOccFound] != a.n_occ || hdr[kHdrOcc] != a.n_occ) return;
+  const int lane = lane_id();
+  const int C = a.C;
+  const int CV = C / VEC;
+  const int cbase = blockIdx.y * kWave;
+  const int cvc = min(kWave, CV - cbase);
+  const int gpw = kWave / cvc;
+  const int lg = lane / cvc;
+  const int vi = lane - lg * cvc;
+  if (lg >= gpw) return;
+  const int64_t j = ((int64_t)blockIdx.x * (kCombThreads / kWave) + threadIdx.x / kWave) * gpw + lg;
+  const int64_t n_comb = min(hdr[kHdrComb], a.n_occ);
+  const int64_t n_empty = min<int64_t>(hdr[kHdrEmpty], a.n_empty);
+  const int64_t col = (int64_t)(cbase + vi) * VEC;
+  if (j < n_comb) {
+    const int64_t cell = a.comb_cell[j];
+    const int64_t s0 = a.comb_slot0[j], s1 = a.comb_slot0[j + 1];
+    if (cell < 0 || cell >= a.cells) return;
+    float sum[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) sum[e] = 0.f;
+    if (s0 < 0 || s1 <= s0 || s1 > a.slot_cap) {
+      // the workspace does not hold this cell's slots: make that visible
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) sum[e] = __builtin_nanf("");
+    } else {
+      int64_t s = s0;
+      for (; s + 4 <= s1; s += 4) {
+        float t[4][VEC];
+#pragma unroll
+        for (int k = 0; k < 4; ++k) Vec<float, VEC>::load(a.slots + (s + k) * C + col, t[k]);
+#pragma unroll
+        for (int k = 0; k < 4; ++k)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) sum[e] += t[k][e];
+      }
+      for (; s < s1; ++s) {
+        float t[VEC];
+        Vec<float, VEC>::load(a.slots + s * C + col, t);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) sum[e] += t[e];
+      }
+    }
+    Vec<TOut, VEC>::store(out + cell * C + col, sum);
+  } else if (j - n_comb < n_empty) {
+    const int64_t cell = a.empty[j - n_comb];
+    if (cell >= 0 && cell < a.cells) store_zero<TOut, VEC>(out + cell * C + col);
+  }
+}
+
+template <typename TOut, int VEC>
+__global__ __launch_bounds__(256) void k_zero_out(TOut* __restrict__ out, int64_t nvec) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < nvec) store_zero<TOut, VEC>(out + i * VEC);
+}
+
+int device_cus() {
+  static int cached[64];  // per device; 0 = not yet queried
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] > 0) return cached[dev];
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  cached[dev] = cus;
+  return cus;
+}
+
+template <typename TIn, typename TOut, int VEC>
+hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void* feat,
+               StripArgs a, void* out, hipStream_t stream) {
+  TOut* o = static_cast<TOut*>(out);
+  const int CV = (int)(d.C / VEC);
+  const unsigned chunks = (unsigned)((CV + kWave - 1) / kWave);
+  // one persistent workgroup per CU (a whole number per die), more when a
+  // workgroup would otherwise get more than kHdrCache items
+  const int64_t per_die_slots = std::max<int64_t>((device_cus() + kXcds - 1) / kXcds,
+                                                  a.items_cap / ((int64_t)kXcds * kHdrCache) + 1);
+  const int blocks = (int)(per_die_slots * kXcds);
+  k_fwd_strips<TIn, TOut, VEC><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
+      static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
+  const int64_t gpw = kWave / (CV < kWave ? CV : kWave);
+  const int64_t entries = (int64_t)a.n_occ + a.n_empty;
+  const int64_t per_block = gpw * (kCombThreads / kWave);
+  const int64_t cblocks = (entries + per_block - 1) / per_block;
+  if (cblocks > 0)
+    k_fwd_combine<TOut, VEC><<<dim3((unsigned)cblocks, chunks), dim3(kCombThreads), 0, stream>>>(
+        o, a);
+  return hipGetLastError();
+}
+
+template <typename TOut, int VEC>
+hipError_t zero_fill(const Dims& d, void* out, hipStream_t stream) {
+  const int64_t nvec = d.cells * (d.C / VEC);
+  k_zero_out<TOut, VEC><<<dim3((unsigned)((nvec + 255) / 256)), dim3(256), 0, stream>>>(
+      static_cast<TOut*>(out), nvec);
+  return hipGetLastError();
+}
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+}  // namespace
+
+size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots) {
+  return (size_t)(n_slots > 0 ? n_slots : 0) * (size_t)d.C * sizeof(float);
+}
+
+hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
+                                    const void* depth, const void* feat, const void* schedule,
+                                    int32_t n_valid, int32_t n_intervals, void* out,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+  const bool al = aligned16(feat) && aligned16(out) && aligned16(workspace);
+  const bool half_in = in_dtype == BEVPOOL_F16;
+  const bool half_out = out_dtype == BEVPOOL_F16;
+  const int vec = half_in ? ((al && d.C % 8 == 0) ? 8 : 1) : ((al && d.C % 4 == 0) ? 4 : 1);
+  if (n_valid == 0 || n_intervals == 0) {
+    if (half_out) return vec == 8 ? zero_fill<half_t, 8>(d, out, stream) : zero_fill<half_t, 1>(d, out, stream);
+    if (vec == 4) return zero_fill<float, 4>(d, out, stream);
+    if (vec == 8) return zero_fill<float, 8>(d, out, stream);
+    return zero_fill<float, 1>(d, out, stream);
+  }
+  const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
+  const char* sc = static_cast<const char*>(schedule);
+  auto S = [&](size_t o) { return reinterpret_cast<const int32_t*>(sc + o); };
+  StripArgs a;
+  a.hdr = S(L.header);
+  a.pair_rd0 = S(L.pair_rd0);
+  a.pair_ln = reinterpret_cast<const uint32_t*>(S(L.pair_ln));
+  a.item_strip = S(L.item_strip);
+  a.item_pair0 = S(L.item_pair0);
+  a.item_seg0 = S(L.item_seg0);
+  a.seg_dest = S(L.seg_dest);
+  a.comb_cell = S(L.comb_cell);
+  a.comb_slot0 = S(L.comb_slot0);
+  a.empty = S(L.empty);
+  a.slots = static_cast<float*>(workspace);
+  a.slot_cap = workspace == nullptr ? 0 : (int64_t)(workspace_bytes / ((size_t)d.C * sizeof(float)));
+  a.n_valid = n_valid;
+  a.n_occ = n_intervals;
+  a.items_cap = (int32_t)L.items_cap;
+  a.C = (int32_t)d.C;
+  a.H = (int32_t)d.H;
+  a.W = (int32_t)d.W;
+  a.bh = (int32_t)L.sd.bh;
+  a.bw = (int32_t)L.sd.bw;
+  a.nhb = (int32_t)L.sd.nhb;
+  a.nwb = (int32_t)L.sd.nwb;
+  a.strips = (int32_t)L.sd.strips;
+  a.hw32 = (int32_t)d.hw;
+  a.P = d.P;
+  a.cells = d.cells;
+  a.n_empty = L.n_empty;
+  if (!half_in) {
+    if (vec == 4) return run<float, float, 4>(d, L.sd, depth, feat, a, out, stream);
+    return run<float, float, 1>(d, L.sd, depth, feat, a, out, stream);
+  }
+  if (half_out) {
+    if (vec == 8) return run<half_t, half_t, 8>(d, L.sd, depth, feat, a, out, stream);
+    return run<half_t, half_t, 1>(d, L.sd, depth, feat, a, out, stream);
+  }
+  if (vec == 8) return run<half_t, float, 8>(d, L.sd, depth, feat, a, out, stream);
+  return run<half_t, float, 1>(d, L.sd, depth, feat, a, out, stream);
+}
+
+}  // namespace bevpool

@@ -50,90 +50,87 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
                           hipStream_t stream);
 
 // ---- schedule ----------------------------------------------------------------
-// A forward schedule regroups the kept points of a plan for the tiled forward
-// kernel.  Definitions:
-//   pair   maximal run of kept points with the same cell, the same pixel and
-//          consecutive depth bins (their depth scores multiply one feature row)
-//   cell   occupied BEV cell; cells are ordered by (b, z, Morton(y, x)) so that
-//          consecutive cells are close in the grid (falls back to the BEV rank
-//          when that key would not fit 31 bits)
-//   tile   consecutive cells, cut where the first pair of a cell crosses a
-//          multiple of kTilePairs / 2, where the cell index crosses a
-//          multiple of tile_max_cells(), and around any cell with more than
-//          kTilePairs / 2 pairs; so a tile of several cells has at most
-//          kTilePairs pairs and at most tile_max_cells() cells
-//   rows   the distinct feature rows of a tile, ascending: the rows the
-//          forward stages in LDS
-//   item   channel slice k of K of a tile; K grows with the tile's staged
-//          bytes (counted at 4 bytes per element, so one schedule serves
-//          both element types)
+// A schedule regroups the kept points of a plan by image strips, for the
+// scheduled forward and backward.  Definitions:
+//   strip    a block of bh x bw feature pixels of one (sample, camera) image;
+//            bh = min(H, R), bw = min(W, max(1, R / bh)) with R =
+//            strip_pixels(C) (strips of the last block row and column are cut
+//            at the image edge).  Strips are numbered (b, n, h / bh, w / bw)
+//            row-major; a pixel's local index in its strip is row-major over
+//            the strip's own width.  A column of pixels views one azimuth, so
+//            a strip's points fall into few BEV cells.
+//   pair     maximal run of kept points of one strip, one cell and one pixel
+//            over consecutive depth bins; pairs are ordered by (strip, BEV
+//            rank, local pixel, depth bin)
+//   item     a run of one strip's pairs: a strip with P pairs is cut into
+//            K = ceil(P / kItemPairs) items, item j starting at pair
+//            floor(j * P / K) of the strip
+//   segment  maximal run of pairs of one cell inside one item
+//   slot     a float32 row of the forward workspace holding one segment's
+//            partial sum; only cells covered by several segments have slots,
+//            numbered by (cell, segment)
 // Device layout (int32 / uint32, 256-byte aligned arrays):
-//   header[16]               counts, see kHdr*
-//   pair_rl[n_valid]         index of the pair's feature row in its tile's rows
-//   pair_dn[n_valid]         first depth bin | (points << 16)
-//   cell_out[n_occ + 1]      BEV rank of each cell in tile order
-//   cell_pair[n_occ + 1]     first pair of each cell (+ end sentinel)
-//   tile_cell[n_occ + 1]     first cell of each tile (+ end sentinel)
-//   tile_row0[n_occ + 1]     first row entry of each tile (+ end sentinel)
-//   rows[n_valid]            feature rank of each row entry
-//   row_dbase[n_valid]       depth rank of each row entry's pixel at depth bin 0
-//   empty[cells - n_occ + 1] BEV rank of each empty cell, ascending
-//   bp_cell[n_valid]         pixel-major pairs (the same pairs sorted by feature
-//   bp_dn[n_valid]             rank, then cell key): BEV rank, and d0 | points << 16
-//   pix_pair0[rows + 1]      first pixel-major pair of each feature row
-//   item_tile[items_cap]     tile of each item, in tile order
-//   item_slice[items_cap]    k | (K << 16)
-//   xcd_begin[kXcds + 1]     first item of each XCD: contiguous item ranges of
-//                            about equal work, so one die's L2 holds the
-//                            feature rows of one region of the grid
-constexpr int kTilePairs = 4096;              // pairs a workgroup holds in LDS at once
-constexpr int kTileThreads = 1024;            // forward workgroup
-constexpr int kTileWindowBytes = 48 * 1024;   // LDS per buffer of staged feature rows (two)
-constexpr int kTileMaxCells = 512;            // cap of tile_max_cells()
-constexpr int kTileItemBytes = 192 * 1024;    // staged feature bytes per item (target)
-constexpr int kHdrPairs = 0, kHdrTiles = 1, kHdrItems = 2, kHdrValid = 3, kHdrOcc = 4,
-              kHdrOccFound = 5, kHdrEmpty = 6, kHdrRowEntries = 7, kHdrWork = 8;
+//   header[16]                  counts, see kHdr*
+//   pair_rd0[n_valid]           depth rank of the pair's first point
+//   pair_ln[n_valid]            local pixel | segment head << 15 | points << 16
+//   item_strip[items_cap]       strip of each item
+//   item_pair0[items_cap + 1]   first pair of each item (+ end sentinel)
+//   item_seg0[items_cap + 1]    first segment of each item (+ end sentinel)
+//   seg_dest[n_valid]           BEV rank of a segment alone in its cell, or
+//                               ~slot (negative) for a cell with several
+//   comb_cell[n_occ + 1]        cells with several segments, ascending
+//   comb_slot0[n_occ + 1]       first slot of each (+ end sentinel: slots)
+//   empty[cells - n_occ + 1]    BEV rank of each empty cell, ascending
+//   bp_cell[n_valid]            pixel-major pairs (the pairs stably sorted by
+//   bp_dn[n_valid]                feature rank): BEV rank, d0 | points << 16
+//   pix_pair0[rows + 1]         first pixel-major pair of each feature row
+constexpr int kItemPairs = 2048;          // most pairs of one forward item
+constexpr int kStripBytes = 32 * 1024;    // staged feature bytes of a strip (4-byte elements)
+constexpr uint32_t kPairHead = 1u << 15;  // pair_ln: first pair of a segment
+constexpr uint32_t kPairPixel = kPairHead - 1;
+constexpr int kHdrPairs = 0, kHdrItems = 1, kHdrSegs = 2, kHdrValid = 3, kHdrOcc = 4,
+              kHdrOccFound = 5, kHdrEmpty = 6, kHdrSlots = 7, kHdrComb = 8, kHdrStrips = 9;
+static_assert(kHdrPairs == BEVPOOL_SCHEDULE_PAIRS && kHdrItems == BEVPOOL_SCHEDULE_ITEMS &&
+                  kHdrSegs == BEVPOOL_SCHEDULE_SEGMENTS && kHdrValid == BEVPOOL_SCHEDULE_KEPT &&
+                  kHdrOcc == BEVPOOL_SCHEDULE_CELLS && kHdrOccFound == BEVPOOL_SCHEDULE_CELLS_FOUND &&
+                  kHdrEmpty == BEVPOOL_SCHEDULE_EMPTY && kHdrSlots == BEVPOOL_SCHEDULE_SLOTS,
+              "header indices are part of the C interface");
 // gfx950 (MI355X) has 8 accelerator complex dies; workgroup i of a launch is
 // dispatched to die i % 8, each die with its own L2.
 constexpr int kXcds = 8;
 
-// Lane groups of the forward kernel.  A slice of `cs` channels is processed
-// in sub-slices of at most 64 vectors of `vec` elements; a lane group has one
-// lane per vector of a sub-slice and as many groups as fit in a wave share it.
-// Each group holds the accumulators of at most tile_max_units(vec) (cell,
-// chunk) units.
-inline int tile_group_lanes(int64_t cs, int vec) {
-  const int64_t g = (cs + vec - 1) / vec;
-  return (int)(g > kWaveLanes ? kWaveLanes : g);
-}
-inline int tile_groups(int64_t cs, int vec) {
-  return (kTileThreads / kWaveLanes) * (kWaveLanes / tile_group_lanes(cs, vec));
-}
-constexpr int tile_max_units(int vec) { return vec == 1 ? 8 : 16 / vec; }
-// Most cells a tile may hold: the (cell, chunk) units of any item, at most
-// one per cell plus one per chunk of a balanced split, must fit the groups'
-// accumulators for every vector width the forward may use (1, 4, 8).
-int tile_max_cells(const Dims& d);
+struct StripDims {
+  int64_t bh, bw;    // strip height and width in pixels
+  int64_t nhb, nwb;  // strips per image column and row
+  int64_t strips;    // B * N * nhb * nwb
+  int64_t pixels;    // bh * bw: most pixels of a strip
+};
+// Most pixels per strip: the staged feature rows of a 64-vector channel
+// chunk (at most 256 four-byte elements per row) fit kStripBytes.
+int64_t strip_pixels(int64_t C);
+StripDims strip_dims(const Dims& d);
 
 struct ScheduleLayout {
-  size_t header, pair_rl, pair_dn, cell_out, cell_pair, tile_cell, tile_row0, rows, row_dbase, empty,
-      bp_cell, bp_dn, pix_pair0, item_tile, item_slice, xcd_begin, total;
+  size_t header, pair_rd0, pair_ln, item_strip, item_pair0, item_seg0, seg_dest, comb_cell,
+      comb_slot0, empty, bp_cell, bp_dn, pix_pair0, total;
   int64_t n_valid, n_occ, n_empty, items_cap;
+  StripDims sd;
   // build workspace
-  size_t ws_ka, ws_va, ws_kb, ws_vb, ws_head, ws_pair_rb, ws_pair_row, ws_flags, ws_tiles,
-      ws_hist, ws_sums, ws_total;
+  size_t ws_ka, ws_va, ws_kb, ws_vb, ws_head, ws_pair_rb, ws_pair_row, ws_pair_dn, ws_flags,
+      ws_strip, ws_tiles, ws_hist, ws_sums, ws_total;
   int64_t ntiles, nscan;
-  int row_bits, key_bits, tile_bits;
-  int morton_level;  // cells keyed by (b*Z + z) << 2L | Morton(y, x); -1: by BEV rank
+  int row_bits, cell_bits, pixel_bits, strip_bits;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
 hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
                            int32_t n_intervals, void* schedule, void* workspace,
                            hipStream_t stream);
+// Float32 workspace rows of the scheduled forward: one per slot.
+size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots);
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
-                                   const void* depth, const void* feat, const void* schedule,
-                                   int32_t n_valid, int32_t n_intervals, void* out,
-                                   hipStream_t stream);
+                                    const void* depth, const void* feat, const void* schedule,
+                                    int32_t n_valid, int32_t n_intervals, void* out,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 // ---- forward ---------------------------------------------------------------
 size_t forward_workspace_bytes(const Dims& d);

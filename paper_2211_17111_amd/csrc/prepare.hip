@@ -335,18 +335,19 @@ __global__ __launch_bounds__(256) void k_interval_lengths(const int32_t* __restr
 
 // ------------------------------------------------------------------ schedule
 //
-// The forward schedule regroups the kept points of a plan into pairs, cells,
-// tiles and items (see internal.h).  Steps, all on the device:
-//   1. stable radix sorts of the plan by feature rank, then by cell key
-//      (Morton order of the cell), giving (cell, pixel, depth rank) order;
-//   2. pair heads and cell heads by ordered compaction;
-//   3. tile heads over the cells;
-//   4. the distinct rows of each tile: pairs sorted by (tile, row), heads of
-//      equal runs, and each pair's index into its tile's row list;
-//   5. the empty cells, by compaction of an occupancy map;
-//   6. items per tile, their work, and per-die item ranges;
-//   7. the pairs again in pixel-major order (for the backward pass), with
-//      the first pair of every feature row.
+// The schedule regroups the kept points of a plan into strips, pairs, items
+// and segments (see internal.h).  Steps, all on the device:
+//   1. stable radix sorts of the plan by local pixel, then by (strip, BEV
+//      rank), giving (strip, cell, pixel, plan position) order;
+//   2. pair heads by ordered compaction, and each pair's point count;
+//   3. the pairs again in pixel-major order (for the backward pass), with
+//      the first pair of every feature row;
+//   4. strip heads over the pairs and the items of every strip;
+//   5. segment heads (item starts and cell changes) and the pair records;
+//   6. segments sorted by cell: a cell covered by several segments gets one
+//      slot per segment, consecutive in segment order; the others are
+//      written directly by the forward;
+//   7. the empty cells, by compaction of an occupancy map.
 
 // Generic ordered compaction over the same 4096-element tiles as the filter:
 // Op provides count(), flag(i), and emit(i, position) (called for flagged i,
@@ -407,27 +408,23 @@ __device__ __forceinline__ int32_t pixel_of(int32_t p, int64_t per_view, int64_t
   return (int32_t)(((int64_t)p / per_view) * hw + (int64_t)p % hw);
 }
 
-// Spreads the low 16 bits of v to the even bit positions.
-__device__ __forceinline__ uint32_t spread_bits(uint32_t v) {
-  v &= 0xffffu;
-  v = (v | (v << 8)) & 0x00ff00ffu;
-  v = (v | (v << 4)) & 0x0f0f0f0fu;
-  v = (v | (v << 2)) & 0x33333333u;
-  v = (v | (v << 1)) & 0x55555555u;
-  return v;
-}
-
-struct CellKey {  // BEV rank -> sort key of its cell
-  int64_t XY;
-  int32_t X;
-  int32_t level;  // -1: the BEV rank itself
-  __device__ int32_t operator()(int32_t rb) const {
-    if (level < 0) return rb;
-    const int32_t bz = (int32_t)(rb / XY);
-    const int32_t r = (int32_t)(rb - (int64_t)bz * XY);
-    const int32_t y = r / X, x = r - y * X;
-    return (int32_t)(((uint32_t)bz << (2 * level)) | spread_bits((uint32_t)x) |
-                     (spread_bits((uint32_t)y) << 1));
+// Strip and local pixel of a feature row.
+struct StripGeom {
+  int64_t hw;
+  int32_t H, W, bh, bw, nhb, nwb;
+  __device__ int32_t strip(int32_t row) const {
+    const int32_t bn = (int32_t)((int64_t)row / hw);
+    const int32_t r = (int32_t)((int64_t)row - (int64_t)bn * hw);
+    const int32_t h = r / W, w = r - h * W;
+    return (bn * nhb + h / bh) * nwb + w / bw;
+  }
+  __device__ int32_t pixel(int32_t row) const {
+    const int32_t bn = (int32_t)((int64_t)row / hw);
+    const int32_t r = (int32_t)((int64_t)row - (int64_t)bn * hw);
+    const int32_t h = r / W, w = r - h * W;
+    const int32_t w0 = (w / bw) * bw;
+    const int32_t bws = min(bw, W - w0);
+    return (h % bh) * bws + (w - w0);
   }
 };
 
@@ -440,25 +437,34 @@ __global__ void k_sched_init(int32_t* __restrict__ hdr, int32_t n_valid, int32_t
   }
 }
 
-__global__ __launch_bounds__(256) void k_row_keys(const int32_t* __restrict__ rd, int64_t n,
-                                                  int64_t per_view, int64_t hw,
-                                                  int32_t* __restrict__ keys,
-                                                  int32_t* __restrict__ vals) {
+// keys = local pixel of every kept point, vals = its plan position
+__global__ __launch_bounds__(256) void k_pixel_keys(const int32_t* __restrict__ rd, int64_t n,
+                                                    int64_t per_view, StripGeom g,
+                                                    int32_t* __restrict__ keys,
+                                                    int32_t* __restrict__ vals) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i < n) {
-    keys[i] = pixel_of(rd[i], per_view, hw);
+    keys[i] = g.pixel(pixel_of(rd[i], per_view, g.hw));
     vals[i] = (int32_t)i;
   }
 }
 
-__global__ __launch_bounds__(256) void k_cell_keys(const int32_t* __restrict__ rb,
-                                                   const int32_t* __restrict__ vals, int64_t n,
-                                                   CellKey key, int32_t* __restrict__ keys) {
+// keys[i] for the point at plan position vals[i]: mode 0 (strip << cell_bits)
+// | BEV rank, mode 1 the BEV rank, mode 2 the strip.
+__global__ __launch_bounds__(256) void k_strip_keys(const int32_t* __restrict__ rd,
+                                                    const int32_t* __restrict__ rb,
+                                                    const int32_t* __restrict__ vals, int64_t n,
+                                                    int64_t per_view, StripGeom g, int cell_bits,
+                                                    int mode, int32_t* __restrict__ keys) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < n) keys[i] = key(rb[vals[i]]);
+  if (i >= n) return;
+  const int32_t a = vals[i];
+  const int32_t s = g.strip(pixel_of(rd[a], per_view, g.hw));
+  keys[i] = mode == 0 ? (int32_t)(((uint32_t)s << cell_bits) | (uint32_t)rb[a])
+                      : (mode == 1 ? rb[a] : s);
 }
 
-struct PairHeads {  // runs of equal (cell, pixel) over consecutive depth bins
+struct PairHeads {  // runs of one cell and pixel over consecutive depth bins
   const int32_t* rd;
   const int32_t* rb;
   const int32_t* vals;  // plan position of each regrouped point
@@ -467,6 +473,7 @@ struct PairHeads {  // runs of equal (cell, pixel) over consecutive depth bins
   int32_t* pair_rb;
   int32_t* pair_row;
   uint32_t* pair_dn;
+  int32_t* pair_rd0;
   int32_t* head_pos;  // regrouped position of each pair's first point
   __device__ int64_t count() const { return hdr[kHdrValid]; }
   __device__ bool flag(int64_t i) const {
@@ -482,6 +489,7 @@ struct PairHeads {  // runs of equal (cell, pixel) over consecutive depth bins
     pair_rb[pos] = rb[a];
     pair_row[pos] = pixel_of(p, per_view, hw);
     pair_dn[pos] = (uint32_t)(((int64_t)p % per_view) / hw);
+    pair_rd0[pos] = p;
     head_pos[pos] = (int32_t)i;
   }
 };
@@ -497,56 +505,16 @@ __global__ __launch_bounds__(256) void k_pair_points(const int32_t* __restrict__
   }
 }
 
-struct CellHeads {  // first pair of every occupied cell
-  const int32_t* pair_rb;
-  const int32_t* hdr;
-  int32_t* cell_out;
-  int32_t* cell_pair;
-  int32_t cap;  // occupied cells the plan declares (n_intervals)
-  __device__ int64_t count() const { return hdr[kHdrPairs]; }
-  __device__ bool flag(int64_t k) const { return k == 0 || pair_rb[k] != pair_rb[k - 1]; }
-  __device__ void emit(int64_t k, int32_t pos) const {
-    if (pos >= cap) return;  // plan inconsistent with n_intervals: never write past the arrays
-    cell_pair[pos] = (int32_t)k;
-    cell_out[pos] = pair_rb[k];
+__global__ __launch_bounds__(256) void k_pair_row_keys(const int32_t* __restrict__ hdr,
+                                                       const int32_t* __restrict__ pair_row,
+                                                       int32_t* __restrict__ keys,
+                                                       int32_t* __restrict__ vals) {
+  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (p < hdr[kHdrPairs]) {
+    keys[p] = pair_row[p];
+    vals[p] = (int32_t)p;
   }
-};
-
-__global__ void k_cells_end(int32_t* __restrict__ hdr, int32_t* __restrict__ cell_pair) {
-  if (threadIdx.x == 0 && blockIdx.x == 0)
-    cell_pair[min(hdr[kHdrOcc], hdr[kHdrOccFound])] = hdr[kHdrPairs];
 }
-
-struct TileHeads {  // first cell of every tile
-  const int32_t* cell_pair;
-  const int32_t* hdr;
-  int32_t* tile_cell;
-  int32_t max_cells;
-  __device__ int64_t count() const {
-    return hdr[kHdrOccFound] == hdr[kHdrOcc] ? hdr[kHdrOcc] : 0;
-  }
-  __device__ bool big(int64_t c) const { return cell_pair[c + 1] - cell_pair[c] > kTilePairs / 2; }
-  __device__ bool flag(int64_t c) const {
-    if (c == 0 || c % max_cells == 0) return true;
-    return big(c) || big(c - 1) || cell_pair[c] / (kTilePairs / 2) != cell_pair[c - 1] / (kTilePairs / 2);
-  }
-  __device__ void emit(int64_t c, int32_t pos) const { tile_cell[pos] = (int32_t)c; }
-};
-
-__global__ void k_tiles_end(const int32_t* __restrict__ hdr, int32_t* __restrict__ tile_cell) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) tile_cell[hdr[kHdrTiles]] = hdr[kHdrOcc];
-}
-
-// Largest index i in [0, n) with a[i] <= v (a ascending, a[0] <= v).
-__device__ __forceinline__ int32_t upper_index(const int32_t* __restrict__ a, int32_t n, int32_t v) {
-  int32_t lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    if (a[mid] <= v) lo = mid; else hi = mid - 1;
-  }
-  return lo;
-}
-
 
 // Pixel-major pairs: gather the cell and depth run of pair vals[q].
 __global__ __launch_bounds__(256) void k_pix_pairs(const int32_t* __restrict__ hdr,
@@ -577,102 +545,169 @@ __global__ __launch_bounds__(256) void k_pix_offsets(const int32_t* __restrict__
   pix_pair0[f] = lo;
 }
 
+struct StripHeads {  // first pair of every strip that has pairs
+  const int32_t* pair_row;
+  const int32_t* hdr;
+  StripGeom g;
+  int32_t* strip_id;
+  int32_t* strip_p0;
+  __device__ int64_t count() const { return hdr[kHdrPairs]; }
+  __device__ bool flag(int64_t k) const {
+    return k == 0 || g.strip(pair_row[k]) != g.strip(pair_row[k - 1]);
+  }
+  __device__ void emit(int64_t k, int32_t pos) const {
+    strip_id[pos] = g.strip(pair_row[k]);
+    strip_p0[pos] = (int32_t)k;
+  }
+};
 
-__global__ __launch_bounds__(256) void k_pair_row_keys(const int32_t* __restrict__ hdr,
-                                                       const int32_t* __restrict__ pair_row,
-                                                       int32_t* __restrict__ keys,
-                                                       int32_t* __restrict__ vals) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p < hdr[kHdrPairs]) {
-    keys[p] = pair_row[p];
-    vals[p] = (int32_t)p;
+__global__ void k_strips_end(const int32_t* __restrict__ hdr, int32_t* __restrict__ strip_p0) {
+  if (threadIdx.x == 0 && blockIdx.x == 0) strip_p0[hdr[kHdrStrips]] = hdr[kHdrPairs];
+}
+
+// Items of every listed strip (0 past the last one, up to cap).
+__global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
+                                                     const int32_t* __restrict__ strip_p0,
+                                                     int64_t cap, int32_t* __restrict__ count) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= cap) return;
+  int32_t k = 0;
+  if (j < hdr[kHdrStrips]) {
+    const int64_t np = (int64_t)strip_p0[j + 1] - strip_p0[j];
+    k = (int32_t)((np + kItemPairs - 1) / kItemPairs);
+  }
+  count[j] = k;
+}
+
+// With the item counts exclusively scanned: item j of a strip with P pairs
+// starts at its pair floor(j * P / K); item_flag marks item starts (item + 1).
+__global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ hdr,
+                                                      const int32_t* __restrict__ strip_id,
+                                                      const int32_t* __restrict__ strip_p0,
+                                                      const int32_t* __restrict__ offset,
+                                                      int64_t items_cap,
+                                                      int32_t* __restrict__ item_strip,
+                                                      int32_t* __restrict__ item_pair0,
+                                                      int32_t* __restrict__ item_flag) {
+  const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (j >= hdr[kHdrStrips]) return;
+  const int64_t p0 = strip_p0[j];
+  const int64_t np = (int64_t)strip_p0[j + 1] - p0;
+  const int64_t K = (np + kItemPairs - 1) / kItemPairs;
+  for (int64_t i = 0; i < K; ++i) {
+    const int64_t item = (int64_t)offset[j] + i;
+    if (item >= items_cap) return;
+    const int64_t first = p0 + (i * np) / K;
+    item_strip[item] = strip_id[j];
+    item_pair0[item] = (int32_t)first;
+    item_flag[first] = (int32_t)(item + 1);
   }
 }
 
-// Tile of every pair (into pair_tile) and the (row, pair) keys of the row sort.
-__global__ __launch_bounds__(256) void k_pair_tiles(const int32_t* __restrict__ hdr,
-                                                    const int32_t* __restrict__ cell_pair,
-                                                    const int32_t* __restrict__ tile_cell,
-                                                    const int32_t* __restrict__ pair_row,
-                                                    int32_t* __restrict__ pair_tile,
-                                                    int32_t* __restrict__ keys,
-                                                    int32_t* __restrict__ vals) {
-  const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (p >= hdr[kHdrPairs] || hdr[kHdrOccFound] != hdr[kHdrOcc]) return;
-  const int32_t c = upper_index(cell_pair, hdr[kHdrOcc], (int32_t)p);
-  pair_tile[p] = upper_index(tile_cell, hdr[kHdrTiles], c);
-  keys[p] = pair_row[p];
-  vals[p] = (int32_t)p;
+__global__ void k_items_end(const int32_t* __restrict__ hdr, int64_t items_cap,
+                            int32_t* __restrict__ item_pair0) {
+  if (threadIdx.x == 0 && blockIdx.x == 0 && hdr[kHdrItems] <= items_cap)
+    item_pair0[hdr[kHdrItems]] = hdr[kHdrPairs];
 }
 
-__global__ __launch_bounds__(256) void k_tile_keys(const int32_t* __restrict__ hdr,
-                                                   const int32_t* __restrict__ vals,
-                                                   const int32_t* __restrict__ pair_tile,
-                                                   int32_t* __restrict__ keys) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q < hdr[kHdrPairs]) keys[q] = pair_tile[vals[q]];
+__device__ __forceinline__ bool segment_head(int64_t k, const int32_t* item_flag,
+                                             const int32_t* pair_rb) {
+  return k == 0 || item_flag[k] != 0 || pair_rb[k] != pair_rb[k - 1];
 }
 
-__device__ __forceinline__ bool row_head(const int32_t* vals, const int32_t* pair_tile,
-                                         const int32_t* pair_row, int64_t q) {
-  if (q == 0) return true;
-  const int32_t a = vals[q], b = vals[q - 1];
-  return pair_tile[a] != pair_tile[b] || pair_row[a] != pair_row[b];
+struct SegHeads {  // first pair of every segment
+  const int32_t* pair_rb;
+  const int32_t* item_flag;
+  const int32_t* hdr;
+  int64_t items_cap;
+  int32_t* item_seg0;
+  int32_t* seg_cell;  // BEV rank of each segment
+  int32_t* seg_id;    // its index (values of the cell sort)
+  __device__ int64_t count() const { return hdr[kHdrPairs]; }
+  __device__ bool flag(int64_t k) const { return segment_head(k, item_flag, pair_rb); }
+  __device__ void emit(int64_t k, int32_t pos) const {
+    seg_cell[pos] = pair_rb[k];
+    seg_id[pos] = pos;
+    const int32_t it = item_flag[k] - 1;
+    if (it >= 0 && it < items_cap) item_seg0[it] = pos;
+  }
+};
+
+__global__ void k_segs_end(const int32_t* __restrict__ hdr, int64_t items_cap,
+                           int32_t* __restrict__ item_seg0) {
+  if (threadIdx.x == 0 && blockIdx.x == 0 && hdr[kHdrItems] <= items_cap)
+    item_seg0[hdr[kHdrItems]] = hdr[kHdrSegs];
 }
 
-// flags[q] = 1 at the first pair of each (tile, row) run, 0 elsewhere (and
-// beyond the pairs, up to cap).
-__global__ __launch_bounds__(256) void k_row_flags(const int32_t* __restrict__ hdr,
-                                                   const int32_t* __restrict__ vals,
-                                                   const int32_t* __restrict__ pair_tile,
-                                                   const int32_t* __restrict__ pair_row,
-                                                   int64_t cap, int32_t* __restrict__ flags) {
+__global__ __launch_bounds__(256) void k_pair_ln(const int32_t* __restrict__ hdr,
+                                                 const int32_t* __restrict__ pair_row,
+                                                 const int32_t* __restrict__ pair_rb,
+                                                 const uint32_t* __restrict__ pair_dn,
+                                                 const int32_t* __restrict__ item_flag, StripGeom g,
+                                                 uint32_t* __restrict__ pair_ln) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= hdr[kHdrPairs]) return;
+  const uint32_t head = segment_head(k, item_flag, pair_rb) ? kPairHead : 0u;
+  pair_ln[k] = ((uint32_t)g.pixel(pair_row[k]) & kPairPixel) | head | (pair_dn[k] & 0xffff0000u);
+}
+
+// Over segments sorted by cell: is segment q one of several of its cell?
+__device__ __forceinline__ bool shared_cell(const int32_t* keys, int64_t q, int64_t n) {
+  return (q > 0 && keys[q - 1] == keys[q]) || (q + 1 < n && keys[q + 1] == keys[q]);
+}
+
+__global__ __launch_bounds__(256) void k_slot_flags(const int32_t* __restrict__ hdr,
+                                                    const int32_t* __restrict__ keys, int64_t cap,
+                                                    int32_t* __restrict__ flags) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (q >= cap) return;
-  flags[q] = (q < hdr[kHdrPairs] && row_head(vals, pair_tile, pair_row, q)) ? 1 : 0;
+  const int64_t n = hdr[kHdrSegs];
+  flags[q] = (q < n && shared_cell(keys, q, n)) ? 1 : 0;
 }
 
-// With flags exclusively scanned: row entry of each sorted pair (kept in
-// flags), the row list (feature rank and the pixel's depth rank at bin 0),
-// and each tile's first entry.
-__global__ __launch_bounds__(256) void k_row_scatter(const int32_t* __restrict__ hdr,
-                                                     const int32_t* __restrict__ vals,
-                                                     const int32_t* __restrict__ pair_tile,
-                                                     const int32_t* __restrict__ pair_row,
-                                                     int32_t* __restrict__ flags,
-                                                     int32_t* __restrict__ rows,
-                                                     int32_t* __restrict__ row_dbase,
-                                                     int32_t* __restrict__ tile_row0,
-                                                     int64_t per_view, int64_t hw) {
+// With the slot flags exclusively scanned into `slot`.
+__global__ __launch_bounds__(256) void k_seg_dest(const int32_t* __restrict__ hdr,
+                                                  const int32_t* __restrict__ keys,
+                                                  const int32_t* __restrict__ vals,
+                                                  const int32_t* __restrict__ slot,
+                                                  int32_t* __restrict__ seg_dest) {
   const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= hdr[kHdrPairs]) return;
-  const int32_t a = vals[q];
-  const bool head = row_head(vals, pair_tile, pair_row, q);
-  const int32_t e = flags[q] + (head ? 1 : 0) - 1;
-  flags[q] = e;
-  if (head) {
-    const int64_t row = pair_row[a];
-    rows[e] = (int32_t)row;
-    row_dbase[e] = (int32_t)((row / hw) * per_view + row % hw);
+  const int64_t n = hdr[kHdrSegs];
+  if (q >= n) return;
+  seg_dest[vals[q]] = shared_cell(keys, q, n) ? ~slot[q] : keys[q];
+}
+
+struct CombHeads {  // cells with several segments: their first slot
+  const int32_t* keys;
+  const int32_t* slot;
+  const int32_t* hdr;
+  int32_t* comb_cell;
+  int32_t* comb_slot0;
+  int64_t cap;
+  __device__ int64_t count() const { return hdr[kHdrSegs]; }
+  __device__ bool flag(int64_t q) const {
+    return (q == 0 || keys[q - 1] != keys[q]) && shared_cell(keys, q, count());
   }
-  if (q == 0 || pair_tile[a] != pair_tile[vals[q - 1]]) tile_row0[pair_tile[a]] = e;
+  __device__ void emit(int64_t q, int32_t pos) const {
+    if (pos >= cap) return;
+    comb_cell[pos] = keys[q];
+    comb_slot0[pos] = slot[q];
+  }
+};
+
+__global__ void k_comb_end(const int32_t* __restrict__ hdr, int64_t cap,
+                           int32_t* __restrict__ comb_slot0) {
+  if (threadIdx.x == 0 && blockIdx.x == 0)
+    comb_slot0[min<int64_t>(hdr[kHdrComb], cap)] = hdr[kHdrSlots];
 }
 
-__global__ void k_rows_end(const int32_t* __restrict__ hdr, int32_t* __restrict__ tile_row0) {
-  if (threadIdx.x == 0 && blockIdx.x == 0) tile_row0[hdr[kHdrTiles]] = hdr[kHdrRowEntries];
-}
-
-__global__ __launch_bounds__(256) void k_pair_rl(const int32_t* __restrict__ hdr,
-                                                 const int32_t* __restrict__ vals,
-                                                 const int32_t* __restrict__ pair_tile,
-                                                 const int32_t* __restrict__ entry,
-                                                 const int32_t* __restrict__ tile_row0,
-                                                 uint32_t* __restrict__ pair_rl) {
-  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (q >= hdr[kHdrPairs]) return;
-  const int32_t a = vals[q];
-  pair_rl[a] = (uint32_t)(entry[q] - tile_row0[pair_tile[a]]);
-}
+struct CellRuns {  // occupied cells: runs of equal cell over sorted segments
+  const int32_t* keys;
+  const int32_t* hdr;
+  __device__ int64_t count() const { return hdr[kHdrSegs]; }
+  __device__ bool flag(int64_t q) const { return q == 0 || keys[q - 1] != keys[q]; }
+  __device__ void emit(int64_t, int32_t) const {}
+};
 
 __global__ __launch_bounds__(256) void k_fill_i32(int32_t* __restrict__ a, int64_t n, int32_t v) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
@@ -680,11 +715,11 @@ __global__ __launch_bounds__(256) void k_fill_i32(int32_t* __restrict__ a, int64
 }
 
 __global__ __launch_bounds__(256) void k_mark_cells(const int32_t* __restrict__ hdr,
-                                                    const int32_t* __restrict__ cell_out,
+                                                    const int32_t* __restrict__ keys,
                                                     int64_t cells, int32_t* __restrict__ occ) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c < min(hdr[kHdrOcc], hdr[kHdrOccFound])) {
-    const int32_t cell = cell_out[c];
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q < hdr[kHdrSegs]) {
+    const int32_t cell = keys[q];
     if (cell >= 0 && cell < cells) occ[cell] = 1;
   }
 }
@@ -700,87 +735,6 @@ struct EmptyCells {  // BEV ranks no kept point maps to, ascending
     if (pos < cap) empty[pos] = (int32_t)i;
   }
 };
-
-struct SliceCounts {  // channel slice counts a tile may take, ascending
-  int32_t k[16];
-  int32_t n;
-};
-
-// Slices of tile t: the fewest allowed K that bring its staged rows (counted
-// at 4 bytes per element) within the per-item target.
-__device__ __forceinline__ int32_t tile_slices(const int32_t* tile_row0, int64_t t, int64_t C,
-                                               const SliceCounts& sk) {
-  const int64_t rows = tile_row0[t + 1] - tile_row0[t];
-  for (int i = 0; i < sk.n; ++i)
-    if (rows * (C / sk.k[i]) * 4 <= kTileItemBytes) return sk.k[i];
-  return sk.k[sk.n - 1];
-}
-
-__global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
-                                                     const int32_t* __restrict__ tile_row0,
-                                                     int64_t C, SliceCounts sk, int64_t cap,
-                                                     int32_t* __restrict__ count) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (t >= cap) return;
-  const bool ok = hdr[kHdrOccFound] == hdr[kHdrOcc] && t < hdr[kHdrTiles];
-  count[t] = ok ? tile_slices(tile_row0, t, C, sk) : 0;
-}
-
-// Items in tile order; work[i] ~ staged row elements + half the pair-row
-// products of the item, in units of 64 elements.
-__global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ hdr,
-                                                      const int32_t* __restrict__ tile_cell,
-                                                      const int32_t* __restrict__ cell_pair,
-                                                      const int32_t* __restrict__ tile_row0,
-                                                      int64_t C, SliceCounts sk,
-                                                      const int32_t* __restrict__ offset,
-                                                      int32_t* __restrict__ item_tile,
-                                                      int32_t* __restrict__ item_slice,
-                                                      int32_t* __restrict__ work) {
-  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (hdr[kHdrOccFound] != hdr[kHdrOcc] || t >= hdr[kHdrTiles]) return;
-  const int32_t K = tile_slices(tile_row0, t, C, sk);
-  const int64_t rows = tile_row0[t + 1] - tile_row0[t];
-  const int64_t pairs = cell_pair[tile_cell[t + 1]] - cell_pair[tile_cell[t]];
-  const int64_t w = ((rows + pairs / 2) * (C / K) + 63) / 64;
-  const int32_t base = offset[t];
-  for (int32_t k = 0; k < K; ++k) {
-    item_tile[base + k] = (int32_t)t;
-    item_slice[base + k] = k | (K << 16);
-    work[base + k] = (int32_t)(w < 0x3fffffff ? w : 0x3fffffff);
-  }
-}
-
-__global__ __launch_bounds__(256) void k_item_work_tail(const int32_t* __restrict__ hdr,
-                                                        int32_t* __restrict__ work, int64_t cap) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < cap && i >= hdr[kHdrItems]) work[i] = 0;
-}
-
-// xcd_begin[x] = first item whose preceding work reaches x/8 of the total,
-// so each die gets a contiguous run of items of about equal work.
-// `cum` holds the exclusive prefix of the per-item work.
-__global__ __launch_bounds__(256) void k_xcd_bounds(const int32_t* __restrict__ cum,
-                                                    const int32_t* __restrict__ hdr,
-                                                    int32_t* __restrict__ xcd_begin) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  const int64_t n = hdr[kHdrItems];
-  const int64_t total = hdr[kHdrWork];
-  if (i == 0) {
-    xcd_begin[0] = 0;
-    xcd_begin[kXcds] = (int32_t)n;
-    if (n == 0)
-      for (int x = 1; x < kXcds; ++x) xcd_begin[x] = 0;
-  }
-  if (i >= n) return;
-  const int64_t lo = i > 0 ? cum[i - 1] : -1;
-  const int64_t hi = cum[i];
-  for (int x = 1; x < kXcds; ++x) {
-    const int64_t b = (total * x + kXcds - 1) / kXcds;
-    if (lo < b && b <= hi) xcd_begin[x] = (int32_t)i;
-    if (i == n - 1 && b > hi) xcd_begin[x] = (int32_t)n;
-  }
-}
 
 inline size_t align_up(size_t v) { return (v + 255) & ~size_t(255); }
 
@@ -895,46 +849,32 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 
 namespace bevpool {
 
-int tile_max_cells(const Dims& d) {
-  int64_t best = kTileMaxCells;
-  for (int vec : {1, 4, 8}) {
-    if (d.C % vec != 0) continue;
-    const int64_t cs = d.C < 64 * vec ? d.C : 64 * vec;
-    const int64_t m = (int64_t)(tile_max_units(vec) - 1) * tile_groups(cs, vec);
-    if (m < best) best = m;
-  }
-  return (int)(best > 0 ? best : 1);
+int64_t strip_pixels(int64_t C) {
+  const int64_t c = C < 256 ? C : 256;
+  const int64_t r = kStripBytes / (4 * c);
+  return r > 0 ? r : 1;
 }
 
-namespace {
-
-SliceCounts slice_counts(const Dims& d) {
-  SliceCounts sk{};
-  sk.n = 0;
-  for (int64_t k = 1; k <= d.C && sk.n < 16; ++k)
-    if (d.C % k == 0 && (k == 1 || (d.C / k) % 8 == 0)) sk.k[sk.n++] = (int32_t)k;
-  return sk;
+StripDims strip_dims(const Dims& d) {
+  StripDims s{};
+  const int64_t R = strip_pixels(d.C);
+  s.bh = std::min<int64_t>(d.H, R);
+  s.bw = std::max<int64_t>(1, std::min<int64_t>(d.W, R / s.bh));
+  s.nhb = (d.H + s.bh - 1) / s.bh;
+  s.nwb = (d.W + s.bw - 1) / s.bw;
+  s.strips = d.B * d.N * s.nhb * s.nwb;
+  s.pixels = s.bh * s.bw;
+  return s;
 }
-
-// Morton level L (2^L >= X, Y) when (b*Z + z) << 2L | Morton(y, x) fits 31
-// bits, else -1.
-int morton_level(const Dims& d) {
-  int L = 0;
-  while ((int64_t(1) << L) < d.X || (int64_t(1) << L) < d.Y) ++L;
-  if (L > 15) return -1;
-  if (bit_length(d.B * d.Z) + 2 * L > 31) return -1;
-  return L;
-}
-
-}  // namespace
 
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals) {
   ScheduleLayout L{};
   L.n_valid = n_valid;
   L.n_occ = n_intervals;
   L.n_empty = d.cells > n_intervals ? d.cells - n_intervals : 0;
-  const SliceCounts sk = slice_counts(d);
-  L.items_cap = (n_intervals + 1) * sk.k[sk.n - 1];
+  L.sd = strip_dims(d);
+  // sum over strips of ceil(P_s / kItemPairs) <= n_pairs / kItemPairs + strips
+  L.items_cap = L.sd.strips + n_valid / kItemPairs + 2;
   const size_t nv = (size_t)(n_valid > 0 ? n_valid : 1);
   const size_t nocc = (size_t)n_intervals + 1;
   size_t off = 0;
@@ -944,26 +884,23 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
     return o;
   };
   L.header = take(16);
-  L.pair_rl = take(nv);
-  L.pair_dn = take(nv);
-  L.cell_out = take(nocc);
-  L.cell_pair = take(nocc);
-  L.tile_cell = take(nocc);
-  L.tile_row0 = take(nocc);
-  L.rows = take(nv);
-  L.row_dbase = take(nv);
+  L.pair_rd0 = take(nv);
+  L.pair_ln = take(nv);
+  L.item_strip = take((size_t)L.items_cap);
+  L.item_pair0 = take((size_t)L.items_cap + 1);
+  L.item_seg0 = take((size_t)L.items_cap + 1);
+  L.seg_dest = take(nv);
+  L.comb_cell = take(nocc);
+  L.comb_slot0 = take(nocc);
   L.empty = take((size_t)L.n_empty + 1);
   L.bp_cell = take(nv);
   L.bp_dn = take(nv);
   L.pix_pair0 = take((size_t)d.rows + 1);
-  L.item_tile = take((size_t)L.items_cap);
-  L.item_slice = take((size_t)L.items_cap);
-  L.xcd_begin = take(kXcds + 1);
   L.total = off;
 
   const int64_t span = std::max<int64_t>((int64_t)nv, d.cells);
   L.ntiles = (span + kPrepTile - 1) / kPrepTile;
-  const int64_t scan_n = std::max<int64_t>(std::max<int64_t>(256 * L.ntiles, L.items_cap), span);
+  const int64_t scan_n = std::max<int64_t>(std::max<int64_t>(256 * L.ntiles, L.sd.strips + 1), span);
   L.nscan = (scan_n + kScanTile - 1) / kScanTile;
   off = 0;
   L.ws_ka = take(nv);
@@ -973,16 +910,17 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.ws_head = take(nv);
   L.ws_pair_rb = take(nv);
   L.ws_pair_row = take(nv);
+  L.ws_pair_dn = take(nv);
   L.ws_flags = take((size_t)span + 1);
-  L.ws_tiles = take((size_t)std::max<int64_t>(L.ntiles, nocc + L.items_cap) + 2);
+  L.ws_strip = take(3 * ((size_t)L.sd.strips + 1));
+  L.ws_tiles = take((size_t)L.ntiles + 2);
   L.ws_hist = take((size_t)(256 * L.ntiles));
   L.ws_sums = take((size_t)L.nscan + 1);
   L.ws_total = off;
   L.row_bits = bit_length(d.rows);
-  L.morton_level = morton_level(d);
-  L.key_bits = L.morton_level < 0 ? bit_length(d.cells)
-                                  : bit_length(d.B * d.Z) + 2 * L.morton_level;
-  L.tile_bits = bit_length(n_intervals + 1);
+  L.cell_bits = bit_length(d.cells);
+  L.pixel_bits = bit_length(L.sd.pixels);
+  L.strip_bits = bit_length(L.sd.strips);
   return L;
 }
 
@@ -998,112 +936,122 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
   int32_t* tiles = W(L.ws_tiles);
   int32_t* sums = W(L.ws_sums);
   int32_t* hist = W(L.ws_hist);
+  int32_t* occ = W(L.ws_flags);
   const dim3 grid((unsigned)L.ntiles), block(kPrepThreads);
   const unsigned g_nv = (unsigned)((n_valid + 255) / 256);
+  const unsigned g_cells = (unsigned)((d.cells + 255) / 256);
+  StripGeom geom;
+  geom.hw = d.hw;
+  geom.H = (int32_t)d.H;
+  geom.W = (int32_t)d.W;
+  geom.bh = (int32_t)L.sd.bh;
+  geom.bw = (int32_t)L.sd.bw;
+  geom.nhb = (int32_t)L.sd.nhb;
+  geom.nwb = (int32_t)L.sd.nwb;
 
   k_sched_init<<<1, 64, 0, stream>>>(hdr, n_valid, n_intervals);
-
-  // empty cells (also when nothing is kept)
-  int32_t* occ = W(L.ws_flags);
-  k_fill_i32<<<(unsigned)((d.cells + 255) / 256), 256, 0, stream>>>(occ, d.cells, 0);
   if (n_valid > 0) {
-    // 1. regroup by (cell key, pixel, plan position)
-    k_row_keys<<<g_nv, 256, 0, stream>>>(rd, n_valid, d.per_view, d.hw, W(L.ws_ka), W(L.ws_va));
-    const bool in_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
-                                       hdr + kHdrValid, L.ntiles, L.row_bits, hist, sums, stream);
-    int32_t* k0 = in_b ? W(L.ws_kb) : W(L.ws_ka);
-    int32_t* v0 = in_b ? W(L.ws_vb) : W(L.ws_va);
-    int32_t* k1 = in_b ? W(L.ws_ka) : W(L.ws_kb);
-    int32_t* v1 = in_b ? W(L.ws_va) : W(L.ws_vb);
-    const CellKey ck{d.X * d.Y, (int32_t)d.X, L.morton_level};
-    k_cell_keys<<<g_nv, 256, 0, stream>>>(rb, v0, n_valid, ck, k0);
-    const bool in_1 = radix_sort_pairs(k0, v0, k1, v1, hdr + kHdrValid, L.ntiles, L.key_bits, hist,
-                                       sums, stream);
-    const int32_t* vals = in_1 ? v1 : v0;
+    // 1. regroup by (strip, cell, local pixel, plan position)
+    int32_t *ck = W(L.ws_ka), *cv = W(L.ws_va), *ak = W(L.ws_kb), *av = W(L.ws_vb);
+    auto sort_current = [&](int bits, const int32_t* n_ptr) {
+      if (radix_sort_pairs(ck, cv, ak, av, n_ptr, L.ntiles, bits, hist, sums, stream)) {
+        std::swap(ck, ak);
+        std::swap(cv, av);
+      }
+    };
+    k_pixel_keys<<<g_nv, 256, 0, stream>>>(rd, n_valid, d.per_view, geom, ck, cv);
+    sort_current(L.pixel_bits, hdr + kHdrValid);
+    if (L.strip_bits + L.cell_bits <= 31) {
+      k_strip_keys<<<g_nv, 256, 0, stream>>>(rd, rb, cv, n_valid, d.per_view, geom, L.cell_bits, 0,
+                                             ck);
+      sort_current(L.strip_bits + L.cell_bits, hdr + kHdrValid);
+    } else {
+      k_strip_keys<<<g_nv, 256, 0, stream>>>(rd, rb, cv, n_valid, d.per_view, geom, L.cell_bits, 1,
+                                             ck);
+      sort_current(L.cell_bits, hdr + kHdrValid);
+      k_strip_keys<<<g_nv, 256, 0, stream>>>(rd, rb, cv, n_valid, d.per_view, geom, L.cell_bits, 2,
+                                             ck);
+      sort_current(L.strip_bits, hdr + kHdrValid);
+    }
+    const int32_t* vals = cv;
 
-    // 2. pairs and cells
+    // 2. pairs
+    int32_t* pair_rb = W(L.ws_pair_rb);
+    int32_t* pair_row = W(L.ws_pair_row);
+    uint32_t* pair_dn = reinterpret_cast<uint32_t*>(W(L.ws_pair_dn));
     int32_t* head_pos = W(L.ws_head);
-    uint32_t* pair_dn = reinterpret_cast<uint32_t*>(S(L.pair_dn));
-    PairHeads ph{rd, rb, vals, hdr, d.per_view, d.hw, W(L.ws_pair_rb), W(L.ws_pair_row), pair_dn,
-                 head_pos};
+    PairHeads ph{rd, rb, vals, hdr, d.per_view, d.hw, pair_rb, pair_row, pair_dn,
+                 S(L.pair_rd0), head_pos};
     k_compact_count<<<grid, block, 0, stream>>>(ph, tiles);
     scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrPairs, stream);
     k_compact_scatter<<<grid, block, 0, stream>>>(ph, tiles);
     k_pair_points<<<g_nv, 256, 0, stream>>>(head_pos, hdr, pair_dn);
-    CellHeads ch{W(L.ws_pair_rb), hdr, S(L.cell_out), S(L.cell_pair), n_intervals};
-    k_compact_count<<<grid, block, 0, stream>>>(ch, tiles);
-    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
-    k_compact_scatter<<<grid, block, 0, stream>>>(ch, tiles);
-    k_cells_end<<<1, 64, 0, stream>>>(hdr, S(L.cell_pair));
 
-    // 7 (done here, while each pair's BEV rank is at hand). Stable sort by
-    // feature rank keeps the cell-key order within a pixel.
-    k_pair_row_keys<<<g_nv, 256, 0, stream>>>(hdr, W(L.ws_pair_row), W(L.ws_ka), W(L.ws_va));
-    const bool x_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
-                                      hdr + kHdrPairs, L.ntiles, L.row_bits, hist, sums, stream);
-    k_pix_pairs<<<g_nv, 256, 0, stream>>>(hdr, x_b ? W(L.ws_vb) : W(L.ws_va), W(L.ws_pair_rb),
-                                          pair_dn, S(L.bp_cell),
+    // 3. pixel-major pairs; a stable sort by feature rank keeps the cell order
+    // within a pixel
+    ck = W(L.ws_ka); cv = W(L.ws_va); ak = W(L.ws_kb); av = W(L.ws_vb);
+    k_pair_row_keys<<<g_nv, 256, 0, stream>>>(hdr, pair_row, ck, cv);
+    sort_current(L.row_bits, hdr + kHdrPairs);
+    k_pix_pairs<<<g_nv, 256, 0, stream>>>(hdr, cv, pair_rb, pair_dn, S(L.bp_cell),
                                           reinterpret_cast<uint32_t*>(S(L.bp_dn)));
-    k_pix_offsets<<<(unsigned)((d.rows + 1 + 255) / 256), 256, 0, stream>>>(
-        hdr, x_b ? W(L.ws_kb) : W(L.ws_ka), d.rows, S(L.pix_pair0));
+    k_pix_offsets<<<(unsigned)((d.rows + 1 + 255) / 256), 256, 0, stream>>>(hdr, ck, d.rows,
+                                                                            S(L.pix_pair0));
 
-    // 3. tiles
-    TileHeads th{S(L.cell_pair), hdr, S(L.tile_cell), tile_max_cells(d)};
-    k_compact_count<<<grid, block, 0, stream>>>(th, tiles);
-    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrTiles, stream);
-    k_compact_scatter<<<grid, block, 0, stream>>>(th, tiles);
-    k_tiles_end<<<1, 64, 0, stream>>>(hdr, S(L.tile_cell));
+    // 4. strips and items
+    const int64_t scap = L.sd.strips + 1;
+    int32_t* strip_id = W(L.ws_strip);
+    int32_t* strip_p0 = strip_id + scap;
+    int32_t* icount = strip_p0 + scap;
+    StripHeads sh{pair_row, hdr, geom, strip_id, strip_p0};
+    k_compact_count<<<grid, block, 0, stream>>>(sh, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrStrips, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(sh, tiles);
+    k_strips_end<<<1, 64, 0, stream>>>(hdr, strip_p0);
+    const unsigned g_s = (unsigned)((scap + 255) / 256);
+    k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, icount);
+    scan_exclusive(icount, scap, sums, hdr + kHdrItems, stream);
+    int32_t* item_flag = W(L.ws_flags);
+    k_fill_i32<<<g_nv, 256, 0, stream>>>(item_flag, n_valid, 0);
+    k_item_scatter<<<g_s, 256, 0, stream>>>(hdr, strip_id, strip_p0, icount, L.items_cap,
+                                            S(L.item_strip), S(L.item_pair0), item_flag);
+    k_items_end<<<1, 64, 0, stream>>>(hdr, L.items_cap, S(L.item_pair0));
 
-    // 4. distinct rows per tile
-    int32_t* pair_tile = W(L.ws_pair_rb);  // cell ranks are no longer needed
-    k_pair_tiles<<<g_nv, 256, 0, stream>>>(hdr, S(L.cell_pair), S(L.tile_cell), W(L.ws_pair_row),
-                                           pair_tile, W(L.ws_ka), W(L.ws_va));
-    const bool r_b = radix_sort_pairs(W(L.ws_ka), W(L.ws_va), W(L.ws_kb), W(L.ws_vb),
-                                      hdr + kHdrPairs, L.ntiles, L.row_bits, hist, sums, stream);
-    int32_t* rk0 = r_b ? W(L.ws_kb) : W(L.ws_ka);
-    int32_t* rv0 = r_b ? W(L.ws_vb) : W(L.ws_va);
-    int32_t* rk1 = r_b ? W(L.ws_ka) : W(L.ws_kb);
-    int32_t* rv1 = r_b ? W(L.ws_va) : W(L.ws_vb);
-    k_tile_keys<<<g_nv, 256, 0, stream>>>(hdr, rv0, pair_tile, rk0);
-    const bool t_1 = radix_sort_pairs(rk0, rv0, rk1, rv1, hdr + kHdrPairs, L.ntiles, L.tile_bits,
-                                      hist, sums, stream);
-    const int32_t* pvals = t_1 ? rv1 : rv0;
-    int32_t* entry = W(L.ws_head);  // pair heads are no longer needed
-    k_row_flags<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, W(L.ws_pair_row), n_valid, entry);
-    scan_exclusive(entry, n_valid, sums, hdr + kHdrRowEntries, stream);
-    k_row_scatter<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, W(L.ws_pair_row), entry,
-                                            S(L.rows), S(L.row_dbase), S(L.tile_row0),
-                                            d.per_view, d.hw);
-    k_rows_end<<<1, 64, 0, stream>>>(hdr, S(L.tile_row0));
-    k_pair_rl<<<g_nv, 256, 0, stream>>>(hdr, pvals, pair_tile, entry, S(L.tile_row0),
-                                        reinterpret_cast<uint32_t*>(S(L.pair_rl)));
-    k_mark_cells<<<(unsigned)((n_intervals + 255) / 256 + 1), 256, 0, stream>>>(hdr, S(L.cell_out),
-                                                                              d.cells, occ);
+    // 5. segments and pair records
+    ck = W(L.ws_ka); cv = W(L.ws_va); ak = W(L.ws_kb); av = W(L.ws_vb);
+    SegHeads gh{pair_rb, item_flag, hdr, L.items_cap, S(L.item_seg0), ck, cv};
+    k_compact_count<<<grid, block, 0, stream>>>(gh, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrSegs, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(gh, tiles);
+    k_segs_end<<<1, 64, 0, stream>>>(hdr, L.items_cap, S(L.item_seg0));
+    k_pair_ln<<<g_nv, 256, 0, stream>>>(hdr, pair_row, pair_rb, pair_dn, item_flag, geom,
+                                        reinterpret_cast<uint32_t*>(S(L.pair_ln)));
+
+    // 6. slots of cells with several segments
+    sort_current(L.cell_bits, hdr + kHdrSegs);
+    int32_t* slot = W(L.ws_head);  // pair heads are no longer needed
+    k_slot_flags<<<g_nv, 256, 0, stream>>>(hdr, ck, n_valid, slot);
+    scan_exclusive(slot, n_valid, sums, hdr + kHdrSlots, stream);
+    k_seg_dest<<<g_nv, 256, 0, stream>>>(hdr, ck, cv, slot, S(L.seg_dest));
+    CombHeads mh{ck, slot, hdr, S(L.comb_cell), S(L.comb_slot0), n_intervals};
+    k_compact_count<<<grid, block, 0, stream>>>(mh, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrComb, stream);
+    k_compact_scatter<<<grid, block, 0, stream>>>(mh, tiles);
+    k_comb_end<<<1, 64, 0, stream>>>(hdr, n_intervals, S(L.comb_slot0));
+    CellRuns cr{ck, hdr};
+    k_compact_count<<<grid, block, 0, stream>>>(cr, tiles);
+    scan_exclusive(tiles, L.ntiles, sums, hdr + kHdrOccFound, stream);
+    k_fill_i32<<<g_cells, 256, 0, stream>>>(occ, d.cells, 0);  // item flags are done
+    k_mark_cells<<<g_nv, 256, 0, stream>>>(hdr, ck, d.cells, occ);
+  } else {
+    k_fill_i32<<<g_cells, 256, 0, stream>>>(occ, d.cells, 0);
   }
 
-  // 5. empty cells
+  // 7. empty cells
   const dim3 cgrid((unsigned)((d.cells + kPrepTile - 1) / kPrepTile));
   EmptyCells ec{occ, d.cells, S(L.empty), L.n_empty};
   k_compact_count<<<cgrid, block, 0, stream>>>(ec, tiles);
   scan_exclusive(tiles, (int64_t)cgrid.x, sums, hdr + kHdrEmpty, stream);
   k_compact_scatter<<<cgrid, block, 0, stream>>>(ec, tiles);
-  if (n_valid == 0) return hipGetLastError();
-
-  // 6. items and per-die ranges
-  const SliceCounts sk = slice_counts(d);
-  const int64_t tcap = n_intervals + 1;
-  int32_t* count = tiles;          // [tcap]: items per tile, then their offsets
-  int32_t* work = tiles + tcap;    // [items_cap]: work per item, then its prefix
-  const unsigned gt = (unsigned)((tcap + 255) / 256);
-  k_item_counts<<<gt, 256, 0, stream>>>(hdr, S(L.tile_row0), d.C, sk, tcap, count);
-  scan_exclusive(count, tcap, sums, hdr + kHdrItems, stream);
-  k_item_scatter<<<gt, 256, 0, stream>>>(hdr, S(L.tile_cell), S(L.cell_pair), S(L.tile_row0), d.C,
-                                         sk, count, S(L.item_tile), S(L.item_slice), work);
-  k_item_work_tail<<<(unsigned)((L.items_cap + 255) / 256), 256, 0, stream>>>(hdr, work,
-                                                                            L.items_cap);
-  scan_exclusive(work, L.items_cap, sums, hdr + kHdrWork, stream);
-  k_xcd_bounds<<<(unsigned)((L.items_cap + 255) / 256), 256, 0, stream>>>(work, hdr,
-                                                                        S(L.xcd_begin));
   return hipGetLastError();
 }
 

@@ -31,7 +31,7 @@ def test_exports_every_declared_symbol(lib):
         "bevpool_version", "bevpool_strerror", "bevpool_last_error",
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
         "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
-        "bevpool_forward_scheduled",
+        "bevpool_forward_scheduled", "bevpool_forward_scheduled_workspace_size",
         "bevpool_backward_workspace_size", "bevpool_backward", "bevpool_backward_scheduled",
     }
     for n in names:
@@ -168,11 +168,17 @@ def test_schedule_validation(lib):
     assert call(wb=wb.value - 1) == EWORKSPACE
     f = lambda **k: lib.bevpool_forward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0), DUMMY, DUMMY,
                                                   k.get("sc", DUMMY), k.get("sb", sb.value), 1000, 100,
-                                                  k.get("out", DUMMY), None)
+                                                  k.get("out", DUMMY), k.get("ws", DUMMY),
+                                                  k.get("wb", 1024), None)
     assert f(i=0, o=1) == EDTYPE
     assert f(sc=None) == EINVAL
     assert f(sb=16) == EINVAL
     assert f(out=None) == EINVAL
+    assert f(ws=None) == EWORKSPACE
+    n = ctypes.c_size_t(0)
+    assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), 10, ctypes.byref(n)) == OK
+    assert n.value == 10 * s.C * 4
+    assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), -1, ctypes.byref(n)) == EINVAL
     b = lambda **k: lib.bevpool_backward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0),
                                                    k.get("g", DUMMY), DUMMY, DUMMY, k.get("sc", DUMMY),
                                                    k.get("sb", sb.value), 1000, 100, DUMMY,

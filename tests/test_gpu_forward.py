@@ -106,21 +106,31 @@ def test_forward_edge_cases(path):
         assert np.all(out.cpu().numpy().reshape(-1, 80)[~occupied] == 0.0), label
 
 
-@pytest.mark.parametrize("case", ["one cell in batches", "many small cells", "wide fp16 channels",
+@pytest.mark.parametrize("case", ["one cell from many strips", "two cells over many items",
+                                  "many small cells", "tall image", "wide fp16 channels",
                                   "wide fp32 channels"])
-def test_forward_tile_paths(case, path):
+def test_forward_strip_paths(case, path):
     """Shapes that drive the scheduled kernel through its less common paths:
-    a single cell with more pairs than one LDS batch, tiles cut by the cell
-    cap, and channel counts needing several 64-lane sub-slices."""
+    a cell summed from many strips' slots, strips cut into several items whose
+    segments span many lane groups, strips cut in height, and channel counts
+    needing several 64-vector chunks."""
     rng = np.random.default_rng(5)
     dtype = "f32"
-    if case == "one cell in batches":
+    if case == "one cell from many strips":
         shape = dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1)
         P = 48000
         coor = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
         coor[rng.random(P) < 0.1] = -1       # some points out of range
+    elif case == "two cells over many items":
+        shape = dict(B=1, N=1, D=40, H=20, W=8, C=8, X=8, Y=8, Z=1)
+        P = 40 * 20 * 8
+        coor = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
+        coor.reshape(40, -1, 3)[1::2, :, 0] = 5   # every point its own pair
     elif case == "many small cells":
         shape = dict(B=1, N=2, D=3, H=30, W=40, C=80, X=64, Y=64, Z=1)
+        coor = random_coor(rng, shape, p_out=0.2)
+    elif case == "tall image":
+        shape = dict(B=2, N=1, D=6, H=150, W=9, C=64, X=16, Y=16, Z=1)
         coor = random_coor(rng, shape, p_out=0.2)
     elif case == "wide fp16 channels":
         shape = dict(B=1, N=2, D=5, H=6, W=7, C=520, X=6, Y=5, Z=1)
@@ -130,7 +140,7 @@ def test_forward_tile_paths(case, path):
         shape = dict(B=1, N=2, D=5, H=6, W=7, C=1024, X=6, Y=5, Z=1)
         coor = random_coor(rng, shape, p_out=0.2)
     data = draw_small(rng, shape, dtype=dtype)
-    _gpu.say(f"forward tile path: {case} {path}")
+    _gpu.say(f"forward strip path: {case} {path}")
     out, _ = _run(data["depth"], data["feat"], coor, shape, path=path)
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
     _gpu.assert_within(out.float().cpu().numpy(), ref, mag, dtype, case)
@@ -243,8 +253,8 @@ def test_schedule_matches_numpy(name):
     _gpu.say(f"schedule vs numpy: {name}")
     want = _check_schedule(frustum_coor(cfg), cfg.shape(), name)
     if name == "headline":
-        # the tiles' rows are shared by several pairs: fewer staged rows than pairs
-        assert want["n"]["row_entries"] < 0.5 * want["n"]["pairs"]
+        # a strip's pairs fall into few cells: far fewer segments than pairs
+        assert want["n"]["segs"] < 0.05 * want["n"]["pairs"]
 
 
 def test_schedule_edge_shapes():
@@ -262,7 +272,12 @@ def test_schedule_edge_shapes():
     P = shape["B"] * shape["N"] * shape["D"] * shape["H"] * shape["W"]
     one = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
     want = _check_schedule(one, shape, "one cell")
-    assert want["n"]["pairs"] > 4096   # one cell processed in several batches
+    assert want["n"]["comb"] == 1 and want["n"]["slots"] == want["n"]["strips"]
+    shape = dict(B=1, N=1, D=40, H=20, W=8, C=8, X=8, Y=8, Z=1)
+    two = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (40 * 20 * 8, 1))
+    two.reshape(shape["D"], -1, 3)[1::2, :, 0] = 5   # every point its own pair
+    want = _check_schedule(two, shape, "two cells")
+    assert want["n"]["items"] > want["n"]["strips"]   # strips cut into several items
 
 
 def test_scheduled_matches_ranges():

@@ -1,0 +1,136 @@
+"""The strip schedule's definitions, executed on the CPU (no GPU).
+
+tests/_sched.py derives the schedule from the oracle's plan with numpy; here a
+plain interpreter walks that schedule the way the scheduled forward does
+(strip rows addressed from the strip number, pair weights from depth runs,
+segments cut by head bits, direct stores versus slots, then the slot
+combination and the empty-cell fill) and the result must equal the oracle's
+forward (section 2.1) to float64 rounding.  This pins the schedule's
+semantics (a wrong strip geometry, pair run, segment cut or slot order fails
+here) before any GPU compares its buffers against it bit for bit.
+"""
+
+import numpy as np
+import pytest
+
+import _sched
+import oracle
+from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
+
+
+def _execute(sch, depth, feat, shape):
+    """Forward from a derived schedule, in float64; also counts the stores of
+    every output row."""
+    B, N, D, H, W, C = (shape[k] for k in "BNDHWC")
+    cells = B * shape["Z"] * shape["Y"] * shape["X"]
+    hw = H * W
+    sd = _sched.strip_dims(shape)
+    dflat = depth.reshape(-1).astype(np.float64)
+    fflat = feat.reshape(-1, C).astype(np.float64)
+    out = np.full((cells, C), np.nan)
+    writes = np.zeros(cells, dtype=np.int64)
+    slots = np.full((sch["n"]["slots"], C), np.nan)
+    per = sd["nhb"] * sd["nwb"]
+    for i in range(sch["n"]["items"]):
+        s = int(sch["item_strip"][i])
+        bn, r = divmod(s, per)
+        hb, wb = divmod(r, sd["nwb"])
+        h0, w0 = hb * sd["bh"], wb * sd["bw"]
+        bws = min(sd["bw"], W - w0)
+        npix = min(sd["bh"], H - h0) * bws
+        rows = [(bn * H + h0 + lp // bws) * W + w0 + lp % bws for lp in range(npix)]
+        p0, p1 = sch["item_pair0"][i], sch["item_pair0"][i + 1]
+        g0, g1 = sch["item_seg0"][i], sch["item_seg0"][i + 1]
+        assert 1 <= p1 - p0 <= _sched.ITEM_PAIRS
+        seg = -1
+        acc = {}
+        for k in range(p0, p1):
+            ln = int(sch["pair_ln"][k])
+            if ln & _sched.PAIR_HEAD:
+                seg += 1
+            assert k > p0 or ln & _sched.PAIR_HEAD
+            lp, n = ln & (_sched.PAIR_HEAD - 1), ln >> 16
+            assert lp < npix and n >= 1
+            rd0 = int(sch["pair_rd0"][k])
+            w = sum(dflat[rd0 + j * hw] for j in range(n))
+            acc[seg] = acc.get(seg, 0.0) + w * fflat[rows[lp]]
+        assert seg + 1 == g1 - g0
+        for j, v in acc.items():
+            dest = int(sch["seg_dest"][g0 + j])
+            if dest >= 0:
+                out[dest] = v
+                writes[dest] += 1
+            else:
+                assert np.isnan(slots[~dest]).all()
+                slots[~dest] = v
+    for j, cell in enumerate(sch["comb_cell"]):
+        a, b = sch["comb_slot0"][j], sch["comb_slot0"][j + 1]
+        assert b - a >= 2
+        out[cell] = slots[a:b].sum(axis=0)
+        writes[cell] += 1
+    out[sch["empty"]] = 0.0
+    writes[sch["empty"]] += 1
+    return out, writes
+
+
+def _check(depth, feat, coor, shape, label):
+    plan = oracle.prepare_ref(coor, shape)
+    sch = _sched.derive(plan, shape)
+    out, writes = _execute(sch, depth, feat, shape)
+    assert (writes == 1).all(), f"{label}: rows written {np.bincount(writes)} times"
+    ref, mag = oracle.forward_ref(depth, feat, coor, shape)
+    ref = ref.reshape(out.shape)
+    mag = mag.reshape(out.shape)
+    assert np.all(np.abs(out - ref) <= 1e-12 * mag + 1e-300), label
+    return sch
+
+
+def test_schedule_model_tiny():
+    cfg = CONFIGS["tiny"]
+    data = draw_inputs(cfg, with_grad=False)
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "tiny")
+    assert sch["n"]["slots"] == 0 or sch["n"]["comb"] > 0
+
+
+def test_schedule_model_bevdet_geometry():
+    cfg = CONFIGS["bevdet"]
+    data = draw_inputs(cfg, with_grad=False)
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "bevdet")
+    # pixel columns see few cells: far fewer segments than pairs
+    assert sch["n"]["segs"] < 0.25 * sch["n"]["pairs"]
+
+
+@pytest.mark.parametrize("shape", [
+    dict(B=2, N=2, D=9, H=7, W=13, C=17, X=12, Y=10, Z=2),
+    dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1),    # strips cut in height
+    dict(B=1, N=2, D=3, H=30, W=40, C=300, X=64, Y=64, Z=1),  # one-pixel-wide strips
+    dict(B=3, N=1, D=4, H=5, W=6, C=16, X=300, Y=7, Z=3),
+])
+def test_schedule_model_random(shape):
+    rng = np.random.default_rng(shape["C"])
+    data = draw_small(rng, shape)
+    _check(data["depth"], data["feat"], random_coor(rng, shape, p_out=0.3), shape, str(shape))
+
+
+def test_schedule_model_one_cell():
+    # every point in one cell: strips of many pairs are cut into several items,
+    # so the cell has one slot per item
+    shape = dict(B=1, N=1, D=40, H=20, W=8, C=8, X=8, Y=8, Z=1)
+    rng = np.random.default_rng(5)
+    data = draw_small(rng, shape)
+    P = shape["D"] * shape["H"] * shape["W"]
+    coor = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
+    # alternate two cells along depth so that every point is its own pair
+    coor.reshape(shape["D"], -1, 3)[1::2, :, 0] = 5
+    sch = _check(data["depth"], data["feat"], coor, shape, "one cell")
+    assert sch["n"]["items"] > sch["n"]["strips"]
+    assert sch["n"]["comb"] == 2
+
+
+def test_strip_dims_budget():
+    # a strip's rows of one 64-vector channel chunk fit the LDS budget
+    for C in (1, 16, 64, 80, 256, 300, 4096):
+        sd = _sched.strip_dims(dict(B=1, N=1, H=40, W=100, C=C))
+        assert sd["pixels"] * 4 * min(C, 256) <= _sched.STRIP_BYTES or sd["pixels"] == 1
+    sd = _sched.strip_dims(dict(B=1, N=6, H=40, W=100, C=80))
+    assert (sd["bh"], sd["bw"], sd["strips"]) == (40, 2, 300)
