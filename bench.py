@@ -108,7 +108,7 @@ def main():
     ap.add_argument("--fwd-launches", type=int, default=320)
     ap.add_argument("--cpu-seconds", type=float, default=10.0,
                     help="minimum CPU time of the oracle sample (0: skip the CPU baseline)")
-    ap.add_argument("--forward", choices=["interval", "strips"], default="interval",
+    ap.add_argument("--forward", choices=["interval", "strips"], default="strips",
                     help="forward entry point timed as the metric: bevpool_forward (interval table) "
                          "or bevpool_forward_scheduled (strip schedule); the other is reported too")
     ap.add_argument("--backward", choices=["plan", "scheduled"], default="scheduled",

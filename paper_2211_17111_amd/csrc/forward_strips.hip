@@ -41,22 +41,30 @@ namespace bevpool {
 
 namespace {
 
-constexpr int kNT = 1024;  // threads of a strip workgroup (one per CU)
+// One workgroup per CU: kLoadWaves waves fetch the next item into one LDS
+// buffer while the other waves walk the current item in the other.
+constexpr int kNT = 1024;
 constexpr int kWaves = kNT / kWave;
-constexpr int kPP = kItemPairs / kNT;  // pair records per thread
-constexpr int kDepthBurst = 4;         // depth scores per pair loaded before any is summed
-constexpr int kRowRegs = kStripBytes / 16 / kNT;  // 16-byte row vectors per thread in flight
+constexpr int kLoadWaves = 4;
+constexpr int kWalkWaves = kWaves - kLoadWaves;
+constexpr int kLoadThreads = kLoadWaves * kWave;
+constexpr int kLP = kItemPairs / kLoadThreads;              // pairs per loading thread
+constexpr int kLoadRows = kStripBytes / 16 / kLoadThreads;  // 16-byte row vectors per loading thread
+constexpr int kDepthBurst = 2;  // depth scores per pair loaded before any is summed
+constexpr int kRowBatch = 8;    // row vectors per loading thread in flight
+constexpr int kPairBatch = 8;   // pair records per loading thread in flight
+static_assert(kLoadRows % kRowBatch == 0 && kLP % kPairBatch == 0, "whole batches");
 constexpr int kBufBytes = kStripBytes + kItemPairs * 12;  // rows | pair records | destinations
 constexpr int kHdrCache = 128;  // item headers of a workgroup kept in LDS
-constexpr int kUnroll = 4;             // pairs per step of the accumulation walk
 constexpr int kCombThreads = 256;
-static_assert(kItemPairs % kNT == 0, "pair records split evenly over the threads");
+static_assert(kItemPairs % kLoadThreads == 0, "pair records split evenly over the loading threads");
 static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
 
 struct StripArgs {
   const int32_t* hdr;
   const int32_t* pair_rd0;
   const uint32_t* pair_ln;
+  const uint16_t* pair_seg;
   const int32_t* item_strip;
   const int32_t* item_pair0;
   const int32_t* item_seg0;
@@ -80,7 +88,7 @@ constexpr uint32_t kRecHead = 1u << 31;  // first pair of a segment
 constexpr int kRecSegShift = 19;
 constexpr uint32_t kRecOff = (1u << kRecSegShift) - 1;
 static_assert(kItemPairs <= (1 << (31 - kRecSegShift)), "segment index fits its field");
-static_assert((int64_t)kStripBytes / 4 * kWave <= kRecOff + 1, "row offset fits its field");
+static_assert(kStripBytes / 2 <= (int)kRecOff + 1, "row offset (in staged elements) fits its field");
 
 // Raw element vector moved between memory and LDS without conversion.
 template <typename T, int VEC>
@@ -95,6 +103,21 @@ template <>
 struct Raw<half_t, 8> {
   typedef half8_t type;
 };
+template <>
+struct Raw<float, 8> {  // two 16-byte vectors per lane
+  typedef float4_t type;
+};
+// 16-byte (or scalar) vectors of one lane's VEC elements
+template <typename T, int VEC>
+constexpr int raw_parts() {
+  return VEC * (int)sizeof(T) > 16 ? VEC * (int)sizeof(T) / 16 : 1;
+}
+// Lanes of a channel chunk: a chunk holds at most 1 KB of each pixel's row,
+// the budget the strip size is computed with.
+template <typename T, int VEC>
+constexpr int chunk_lanes() {
+  return 1024 / (VEC * (int)sizeof(T)) < kWave ? 1024 / (VEC * (int)sizeof(T)) : kWave;
+}
 
 template <typename T, int VEC>
 __device__ __forceinline__ void raw_to_float(const typename Raw<T, VEC>::type& r, float* v);
@@ -113,18 +136,17 @@ __device__ __forceinline__ void raw_to_float<half_t, 8>(const half8_t& r, float*
 #pragma unroll
   for (int e = 0; e < 8; ++e) v[e] = (float)r[e];
 }
-
-// Exclusive scan over the workgroup with LDS-only barriers; `lds` holds kWaves ints.
-__device__ __forceinline__ int group_exclusive_scan(int v, int* lds) {
-  const int lane = lane_id();
-  const int wid = threadIdx.x / kWave;
-  const int inc = wave_inclusive_scan(v);
-  if (lane == kWave - 1) lds[wid] = inc;
-  lds_barrier();
-  int off = 0;
+template <>
+__device__ __forceinline__ void raw_to_float<float, 8>(const float4_t& r, float* v) {
+  v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w;
+}
+// A lane's VEC elements of a staged row: kNV parts at row + part * cvc.
+template <typename TIn, int VEC>
+__device__ __forceinline__ void lane_row(const typename Raw<TIn, VEC>::type* p, int cvc, float* v) {
+  constexpr int kNV = raw_parts<TIn, VEC>();
+  constexpr int kPer = VEC / kNV;
 #pragma unroll
-  for (int w = 0; w < kWaves; ++w) off += (w < wid) ? lds[w] : 0;
-  return off + inc - v;
+  for (int h = 0; h < kNV; ++h) raw_to_float<TIn, VEC>(p[h * cvc], v + h * kPer);
 }
 
 // An item's header, the same for the whole workgroup.
@@ -137,11 +159,14 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
                                                     const TIn* __restrict__ feat,
                                                     TOut* __restrict__ out, StripArgs a) {
   typedef typename Raw<TIn, VEC>::type RawT;
+  constexpr int kUnroll = VEC >= 8 ? 2 : 4;    // pairs per step of the accumulation walk
+  constexpr int kNV = raw_parts<TIn, VEC>();  // staged vectors per lane and row
+  constexpr int kPer = VEC / kNV;            // elements per staged vector
   // two buffers of [rows, then partial sums | pair records | segment destinations]
   __shared__ __attribute__((aligned(16))) char smem[2 * kBufBytes];
-  __shared__ int s_scan[kWaves];
   __shared__ int32_t s_hdr[3][kHdrCache + 1];  // strip, first pair, first segment
   static_assert((int64_t)kWaves * kWave * 8 * sizeof(float) <= kStripBytes, "partial sums fit the row area");
+  static_assert(kItemPairs <= 65535, "pair indices fit 16 bits");
   auto buf_rows = [&](int b) { return reinterpret_cast<RawT*>(smem + b * kBufBytes); };
   auto buf_pr = [&](int b) { return reinterpret_cast<PairRec*>(smem + b * kBufBytes + kStripBytes); };
   auto buf_dest = [&](int b) {
@@ -167,8 +192,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
 
   const int C = a.C;
   const int CV = C / VEC;
-  const int cbase = blockIdx.y * kWave;
-  const int cvc = min(kWave, CV - cbase);
+  constexpr int kLanes = chunk_lanes<TIn, VEC>();
+  const int cbase = blockIdx.y * kLanes;
+  const int cvc = min(kLanes, CV - cbase);
   const int tid = threadIdx.x;
   const int lane = lane_id();
   const int wave = tid / kWave;
@@ -221,144 +247,144 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     g.origin = ((int64_t)bn * a.H + h0) * a.W + w0;
     return g;
   };
+  // staged vector idx of a strip (pixel-major, then each pixel's chunk in
+  // memory order): its address, and its LDS slot [pixel][part][lane]
+  const int rowvec = cvc * kNV;  // staged vectors per pixel
   auto vec_addr = [&](const Geo& g, int idx) {
-    const int lp = idx / cvc;
-    const int vi = idx - lp * cvc;
+    const int lp = idx / rowvec;
+    const int v = idx - lp * rowvec;
     const int lh = lp / g.bws;
     const int64_t row = g.origin + (int64_t)lh * a.W + (lp - lh * g.bws);
-    return reinterpret_cast<const RawT*>(fchunk + row * C + (int64_t)vi * VEC);
+    return reinterpret_cast<const RawT*>(fchunk + row * C + (int64_t)v * kPer);
+  };
+  auto vec_slot = [&](int idx) {
+    if (kNV == 1) return idx;
+    const int lp = idx / rowvec;
+    const int v = idx - lp * rowvec;
+    const int vi = v / kNV;
+    return lp * rowvec + (v - vi * kNV) * cvc + vi;
   };
 
-  // Loads are unconditional where they can be, surplus lanes repeating an
-  // in-range address: a load under a branch makes the compiler wait for it
-  // where the branch joins.
-  struct Recs {
-    int32_t rd0[kPP];
-    uint32_t ln[kPP];
-  };
-  auto load_recs = [&](const ItemHdr& h, Recs& r) {
-#pragma unroll
-    for (int q = 0; q < kPP; ++q) {
-      const int k = min(tid * kPP + q, max(h.np - 1, 0));
-      r.rd0[q] = a.pair_rd0[h.p0 + k];
-      r.ln[q] = a.pair_ln[h.p0 + k];
-    }
-  };
-  struct Stage {
-    RawT rv[kRowRegs];
-    int32_t dst[kPP];
-    float dv[kPP][kDepthBurst];
-  };
-  // global loads of an item's rows, segment destinations and depth scores
-  auto issue_stage = [&](const ItemHdr& h, const Recs& r, Stage& st) {
+  // ---- loading waves: an item's rows, destinations and pair records into
+  // LDS buffer b.  Loads are unconditional where they can be, surplus lanes
+  // repeating an in-range address: a load under a branch makes the compiler
+  // wait for it where the branch joins.
+  const int lt = tid;  // loading thread (waves 0 .. kLoadWaves - 1)
+  auto load_item = [&](const ItemHdr& h, int b) {
     const Geo g = geometry(h.strip);
-    const int nvec = g.npix * cvc;
-#pragma unroll
-    for (int u = 0; u < kRowRegs; ++u) st.rv[u] = *vec_addr(g, min(u * kNT + tid, nvec - 1));
-#pragma unroll
-    for (int q = 0; q < kPP; ++q)
-      st.dst[q] = a.seg_dest[h.g0 + min(q * kNT + tid, max(h.nseg - 1, 0))];
-#pragma unroll
-    for (int q = 0; q < kPP; ++q) {
-      const int n = tid * kPP + q < h.np ? (int)(r.ln[q] >> 16) : 0;
-#pragma unroll
-      for (int j = 0; j < kDepthBurst; ++j) {
-        const int64_t p = (int64_t)r.rd0[q] + j * hw;
-        float v = 0.f;
-        if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
-        st.dv[q][j] = v;
-      }
-    }
-  };
-  // an item's rows, destinations and pair records into LDS buffer b
-  auto commit_stage = [&](const ItemHdr& h, const Recs& r, const Stage& st, int b) {
-    const Geo g = geometry(h.strip);
-    const int nvec = g.npix * cvc;
+    const int nvec = g.npix * rowvec;
     RawT* const s_rows = buf_rows(b);
     PairRec* const s_pr = buf_pr(b);
     int32_t* const s_dest = buf_dest(b);
+    // rows and destinations, kLoadRounds rounds of loads in flight
+    for (int r0 = 0; r0 < kLoadRows; r0 += kRowBatch) {
+      RawT rv[kRowBatch];
 #pragma unroll
-    for (int u = 0; u < kRowRegs; ++u) {
-      const int idx = u * kNT + tid;
-      if (idx < nvec) s_rows[idx] = st.rv[u];
-    }
-    for (int idx = kRowRegs * kNT + tid; idx < nvec; idx += kNT) s_rows[idx] = *vec_addr(g, idx);
+      for (int u = 0; u < kRowBatch; ++u)
+        rv[u] = *vec_addr(g, min((r0 + u) * kLoadThreads + lt, nvec - 1));
 #pragma unroll
-    for (int q = 0; q < kPP; ++q) {
-      const int j = q * kNT + tid;
-      if (j < h.nseg) s_dest[j] = st.dst[q];
-    }
-    float wsum[kPP];
-    int heads = 0;
-#pragma unroll
-    for (int q = 0; q < kPP; ++q) {
-      const bool live = tid * kPP + q < h.np;
-      const int n = live ? (int)(r.ln[q] >> 16) : 0;
-      // (no constant start: an add of 0.f would be folded into the load's branch)
-      float sum = st.dv[q][0];
-#pragma unroll
-      for (int j = 1; j < kDepthBurst; ++j) sum += st.dv[q][j];
-      for (int j = kDepthBurst; j < n; ++j) {
-        const int64_t p = (int64_t)r.rd0[q] + j * hw;
-        if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+      for (int u = 0; u < kRowBatch; ++u) {
+        const int idx = (r0 + u) * kLoadThreads + lt;
+        if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
       }
-      wsum[q] = sum;
-      heads += (live && (r.ln[q] & kPairHead)) ? 1 : 0;
     }
-    int seg = group_exclusive_scan(heads, s_scan) - 1;
+    for (int idx = kLoadRows * kLoadThreads + lt; idx < nvec; idx += kLoadThreads)
+      s_rows[vec_slot(idx)] = *vec_addr(g, idx);
+    for (int j = lt; j < h.nseg; j += kLoadThreads) s_dest[j] = a.seg_dest[h.g0 + j];
+    // pair records and their depth scores, kPairBatch pairs per thread at a time
+    for (int q0 = 0; q0 < kLP; q0 += kPairBatch) {
+      int32_t rd0[kPairBatch];
+      uint32_t ln[kPairBatch];
+      uint32_t sg[kPairBatch];
 #pragma unroll
-    for (int q = 0; q < kPP; ++q) {
-      const int k = tid * kPP + q;
-      if (k < h.np) {
-        const bool head = (r.ln[q] & kPairHead) != 0;
-        if (head) ++seg;
-        const uint32_t lp = r.ln[q] & kPairPixel;
-        const bool ok = lp < (uint32_t)g.npix;
-        PairRec rec;
-        rec.w = ok ? wsum[q] : 0.f;
-        rec.ps = (ok ? lp * (uint32_t)cvc : 0u) |
-                 ((uint32_t)min(max(seg, 0), h.nseg - 1) << kRecSegShift) | (head ? kRecHead : 0u);
-        s_pr[k] = rec;
+      for (int q = 0; q < kPairBatch; ++q) {
+        const int k = h.p0 + min((q0 + q) * kLoadThreads + lt, max(h.np - 1, 0));
+        rd0[q] = a.pair_rd0[k];
+        ln[q] = a.pair_ln[k];
+        sg[q] = a.pair_seg[k];
+      }
+      float dv[kPairBatch][kDepthBurst];
+#pragma unroll
+      for (int q = 0; q < kPairBatch; ++q) {
+        const int n = (q0 + q) * kLoadThreads + lt < h.np ? (int)(ln[q] >> 16) : 0;
+#pragma unroll
+        for (int j = 0; j < kDepthBurst; ++j) {
+          const int64_t p = (int64_t)rd0[q] + j * hw;
+          float v = 0.f;
+          if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
+          dv[q][j] = v;
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < kPairBatch; ++q) {
+        const int k = (q0 + q) * kLoadThreads + lt;
+        if (k < h.np) {
+          const int n = (int)(ln[q] >> 16);
+          // (no constant start: an add of 0.f would be folded into the load's branch)
+          float sum = dv[q][0];
+#pragma unroll
+          for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
+          for (int j = kDepthBurst; j < n; ++j) {
+            const int64_t p = (int64_t)rd0[q] + j * hw;
+            if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+          }
+          const uint32_t lp = ln[q] & kPairPixel;
+          const bool ok = lp < (uint32_t)g.npix;
+          const uint32_t sgc = min(sg[q], (uint32_t)(h.nseg - 1));
+          PairRec rec;
+          rec.w = ok ? sum : 0.f;
+          rec.ps = (ok ? lp * (uint32_t)rowvec : 0u) | (sgc << kRecSegShift) |
+                   ((ln[q] & kPairHead) ? kRecHead : 0u);
+          s_pr[k] = rec;
+        }
       }
     }
   };
 
-  // lane group lg of the wave owns an equal range of each item's pairs
+  // ---- walking waves: lane group lg of walking wave wv owns an equal range
+  // of each item's pairs
   const int gpw = kWave / cvc;
-  const int G = kWaves * gpw;
+  const int G = kWalkWaves * gpw;
+  const int wv = wave - kLoadWaves;
   const int lg = lane / cvc;
   const int vi = lane - lg * cvc;
-  const int g = wave * gpw + lg;
-  const bool active = lg < gpw;
+  const int g = wv * gpw + lg;
+  const bool walker = wave >= kLoadWaves;
+  const bool active = walker && lg < gpw;
   const int64_t col = (int64_t)(cbase + vi) * VEC;
 
-  // sums an item's segments from LDS buffer b and stores each once
+  int kb = 0, ke = 0, last_seg = -1;
+  bool prev_cont = false, next_cont = false;
+  float first_sum[VEC], last_sum[VEC];
+
+  auto store_seg = [&](const ItemHdr& h, const int32_t* s_dest, int sgi, const float* v) {
+    const int32_t d = s_dest[min(sgi, h.nseg - 1)];
+    if (d >= 0) {
+      if (d < a.cells) Vec<TOut, VEC>::store(out + (int64_t)d * C + col, v);
+    } else {
+      const int64_t sl = (int64_t)(~d);
+      if (sl < a.slot_cap) Vec<float, VEC>::store(a.slots + sl * C + col, v);
+    }
+  };
+
+  // sums this group's range of an item's pairs from LDS buffer b; segments
+  // wholly inside the range are stored, the parts of cut ones kept
   auto walk_item = [&](const ItemHdr& h, int b) {
     const RawT* const s_lane = buf_rows(b) + vi;
     const PairRec* const s_pr = buf_pr(b);
     const int32_t* const s_dest = buf_dest(b);
     const int np = h.np;
-    auto range_begin = [&](int gg) { return (gg * np) / G; };  // below 2^31: G <= kNT
     auto is_head = [&](int k) { return (s_pr[k].ps & kRecHead) != 0; };
     auto seg_at = [&](int k) { return (int)((s_pr[k].ps & ~kRecHead) >> kRecSegShift); };
-    auto store_seg = [&](int sgi, const float* v) {
-      const int32_t d = s_dest[min(sgi, h.nseg - 1)];
-      if (d >= 0) {
-        if (d < a.cells) Vec<TOut, VEC>::store(out + (int64_t)d * C + col, v);
-      } else {
-        const int64_t sl = (int64_t)(~d);
-        if (sl < a.slot_cap) Vec<float, VEC>::store(a.slots + sl * C + col, v);
-      }
-    };
-
-    int kb = 0, ke = 0, last_seg = -1;
-    bool prev_cont = false, next_cont = false;
-    float acc[VEC], first_sum[VEC], last_sum[VEC];
+    kb = ke = 0;
+    prev_cont = next_cont = false;
+    last_seg = -1;
+    float acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = first_sum[e] = last_sum[e] = 0.f;
     if (active) {
-      kb = range_begin(g);
-      ke = range_begin(g + 1);
+      kb = (g * np) / G;  // below 2^31: G <= kNT
+      ke = ((g + 1) * np) / G;
     }
     if (kb < ke) {
       // a range that starts inside a segment owes that segment's part to the
@@ -375,13 +401,21 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           for (int e = 0; e < VEC; ++e) first_sum[e] = acc[e];
           pend_first = false;
         } else {
-          store_seg(cur, acc);
+          store_seg(h, s_dest, cur, acc);
         }
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
         ++cur;
       };
-      int k0 = kb;
+      {
+        // the range's first pair never ends a segment
+        const PairRec r = s_pr[kb];
+        float x[VEC];
+        lane_row<TIn, VEC>(s_lane + (r.ps & kRecOff), cvc, x);
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = fmaf(r.w, x[e], acc[e]);
+      }
+      int k0 = kb + 1;
       for (; k0 + kUnroll <= ke; k0 += kUnroll) {
         // records first, then rows: two LDS round trips per kUnroll pairs
         PairRec r[kUnroll];
@@ -389,10 +423,10 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         for (int u = 0; u < kUnroll; ++u) r[u] = s_pr[k0 + u];
         float x[kUnroll][VEC];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) raw_to_float<TIn, VEC>(s_lane[r[u].ps & kRecOff], x[u]);
+        for (int u = 0; u < kUnroll; ++u) lane_row<TIn, VEC>(s_lane + (r[u].ps & kRecOff), cvc, x[u]);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
-          if ((r[u].ps & kRecHead) && k0 + u != kb) end_segment();
+          if (r[u].ps & kRecHead) end_segment();
 #pragma unroll
           for (int e = 0; e < VEC; ++e) acc[e] = fmaf(r[u].w, x[u][e], acc[e]);
         }
@@ -400,8 +434,8 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
       for (; k0 < ke; ++k0) {
         const PairRec r = s_pr[k0];
         float x[VEC];
-        raw_to_float<TIn, VEC>(s_lane[r.ps & kRecOff], x);
-        if ((r.ps & kRecHead) && k0 != kb) end_segment();
+        lane_row<TIn, VEC>(s_lane + (r.ps & kRecOff), cvc, x);
+        if (r.ps & kRecHead) end_segment();
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] = fmaf(r.w, x[e], acc[e]);
       }
@@ -413,12 +447,19 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
 #pragma unroll
         for (int e = 0; e < VEC; ++e) last_sum[e] = acc[e];
       } else {
-        store_seg(cur, acc);
+        store_seg(h, s_dest, cur, acc);
       }
     }
+  };
 
-    // segments cut by range boundaries, added in range order
-    lds_barrier();  // every group is done reading the rows, which now hold partials
+  // segments cut by range boundaries, added in range order (every wave
+  // passes the barriers; walking waves do the work)
+  auto combine_item = [&](const ItemHdr& h, int b) {
+    const PairRec* const s_pr = buf_pr(b);
+    const int32_t* const s_dest = buf_dest(b);
+    const int np = h.np;
+    auto is_head = [&](int k) { return (s_pr[k].ps & kRecHead) != 0; };
+    auto seg_at = [&](int k) { return (int)((s_pr[k].ps & ~kRecHead) >> kRecSegShift); };
     // [G][cvc][VEC]: each group's part of the segment it starts inside
     float* const part_a = reinterpret_cast<float*>(buf_rows(b));
     const bool has_last = next_cont && !(prev_cont && seg_at(kb) == last_seg);
@@ -429,7 +470,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
 #pragma unroll
       for (int e = 0; e < VEC; ++e) sum[e] = last_sum[e];
       for (int g2 = g + 1; g2 < G; ++g2) {
-        const int b2 = range_begin(g2), e2 = range_begin(g2 + 1);
+        const int b2 = (g2 * np) / G, e2 = ((g2 + 1) * np) / G;
         if (b2 >= e2) continue;
         if (is_head(b2)) break;
         float t[VEC];
@@ -439,34 +480,25 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         // on to the next range only if this one lies wholly inside the segment
         if (!(seg_at(e2 - 1) == last_seg && e2 < np && !is_head(e2))) break;
       }
-      store_seg(last_seg, sum);
+      store_seg(h, s_dest, last_seg, sum);
     }
   };
 
-  // ---- software pipeline over the items: while item i is walked from one
-  // LDS buffer, the loads of item i + 1 (issued before the walk) are in
-  // flight and the pair records of item i + 2 are on their way.
-  ItemHdr hc = header(i_begin);
-  ItemHdr hn = header(i_begin + 1);
-  Recs rc, rn;
-  load_recs(hc, rc);
-  load_recs(hn, rn);
-  Stage st;
-  issue_stage(hc, rc, st);
-  commit_stage(hc, rc, st, 0);
+  // ---- the pipeline: item i is walked from buffer b while the loading
+  // waves fill buffer b ^ 1 with item i + 1
+  if (!walker) load_item(header(i_begin), 0);
   lds_barrier();
   int b = 0;
   for (int i = i_begin; i < i_begin + n_my; ++i) {
-    const ItemHdr hn2 = header(i + 2);
-    Recs rn2;
-    load_recs(hn2, rn2);
-    issue_stage(hn, rn, st);  // item i + 1 (repeats the last item at the end: unused)
-    walk_item(hc, b);
-    if (i + 1 < i_begin + n_my) commit_stage(hn, rn, st, b ^ 1);
-    lds_barrier();
-    hc = hn;
-    hn = hn2;
-    rn = rn2;
+    const ItemHdr hc = header(i);
+    if (!walker) {
+      if (i + 1 < i_begin + n_my) load_item(header(i + 1), b ^ 1);
+    } else {
+      walk_item(hc, b);
+    }
+    lds_barrier();  // item i walked (its rows free for partial sums), item i + 1 loaded
+    combine_item(hc, b);
+    lds_barrier();  // buffer b free for item i + 2
     b ^= 1;
   }
 }
@@ -549,7 +581,8 @@ hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void
                StripArgs a, void* out, hipStream_t stream) {
   TOut* o = static_cast<TOut*>(out);
   const int CV = (int)(d.C / VEC);
-  const unsigned chunks = (unsigned)((CV + kWave - 1) / kWave);
+  constexpr int kLanes = chunk_lanes<TIn, VEC>();
+  const unsigned chunks = (unsigned)((CV + kLanes - 1) / kLanes);
   // one persistent workgroup per CU (a whole number per die), more when a
   // workgroup would otherwise get more than kHdrCache items
   const int64_t per_die_slots = std::max<int64_t>((device_cus() + kXcds - 1) / kXcds,
@@ -561,8 +594,9 @@ hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void
   const int64_t entries = (int64_t)a.n_occ + a.n_empty;
   const int64_t per_block = gpw * (kCombThreads / kWave);
   const int64_t cblocks = (entries + per_block - 1) / per_block;
+  const unsigned cchunks = (unsigned)((CV + kWave - 1) / kWave);
   if (cblocks > 0)
-    k_fwd_combine<TOut, VEC><<<dim3((unsigned)cblocks, chunks), dim3(kCombThreads), 0, stream>>>(
+    k_fwd_combine<TOut, VEC><<<dim3((unsigned)cblocks, cchunks), dim3(kCombThreads), 0, stream>>>(
         o, a);
   return hipGetLastError();
 }
@@ -604,6 +638,7 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.hdr = S(L.header);
   a.pair_rd0 = S(L.pair_rd0);
   a.pair_ln = reinterpret_cast<const uint32_t*>(S(L.pair_ln));
+  a.pair_seg = reinterpret_cast<const uint16_t*>(S(L.pair_seg));
   a.item_strip = S(L.item_strip);
   a.item_pair0 = S(L.item_pair0);
   a.item_seg0 = S(L.item_seg0);

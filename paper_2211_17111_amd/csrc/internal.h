@@ -73,6 +73,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //   header[16]                  counts, see kHdr*
 //   pair_rd0[n_valid]           depth rank of the pair's first point
 //   pair_ln[n_valid]            local pixel | segment head << 15 | points << 16
+//   pair_seg[n_valid] (uint16)  the pair's segment within its item
 //   item_strip[items_cap]       strip of each item
 //   item_pair0[items_cap + 1]   first pair of each item (+ end sentinel)
 //   item_seg0[items_cap + 1]    first segment of each item (+ end sentinel)
@@ -111,7 +112,7 @@ int64_t strip_pixels(int64_t C);
 StripDims strip_dims(const Dims& d);
 
 struct ScheduleLayout {
-  size_t header, pair_rd0, pair_ln, item_strip, item_pair0, item_seg0, seg_dest, comb_cell,
+  size_t header, pair_rd0, pair_ln, pair_seg, item_strip, item_pair0, item_seg0, seg_dest, comb_cell,
       comb_slot0, empty, bp_cell, bp_dn, pix_pair0, total;
   int64_t n_valid, n_occ, n_empty, items_cap;
   StripDims sd;

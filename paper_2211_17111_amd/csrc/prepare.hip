@@ -651,6 +651,44 @@ __global__ __launch_bounds__(256) void k_pair_ln(const int32_t* __restrict__ hdr
   pair_ln[k] = ((uint32_t)g.pixel(pair_row[k]) & kPairPixel) | head | (pair_dn[k] & 0xffff0000u);
 }
 
+// flags[k] = 1 at every segment's first pair, 0 elsewhere (up to cap).
+__global__ __launch_bounds__(256) void k_seg_flags(const int32_t* __restrict__ hdr,
+                                                   const int32_t* __restrict__ pair_rb,
+                                                   const int32_t* __restrict__ item_flag,
+                                                   int64_t cap, int32_t* __restrict__ flags) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= cap) return;
+  flags[k] = (k < hdr[kHdrPairs] && segment_head(k, item_flag, pair_rb)) ? 1 : 0;
+}
+
+// Largest index i in [0, n) with a[i] <= v (a ascending, a[0] <= v).
+__device__ __forceinline__ int32_t upper_index(const int32_t* __restrict__ a, int32_t n, int32_t v) {
+  int32_t lo = 0, hi = n - 1;
+  while (lo < hi) {
+    const int32_t mid = (lo + hi + 1) >> 1;
+    if (a[mid] <= v) lo = mid; else hi = mid - 1;
+  }
+  return lo;
+}
+
+// With the segment flags exclusively scanned into `before`: each pair's
+// segment index within its item.
+__global__ __launch_bounds__(256) void k_pair_seg(const int32_t* __restrict__ hdr,
+                                                  const int32_t* __restrict__ before,
+                                                  const int32_t* __restrict__ pair_rb,
+                                                  const int32_t* __restrict__ item_flag,
+                                                  const int32_t* __restrict__ item_pair0,
+                                                  const int32_t* __restrict__ item_seg0,
+                                                  int64_t items_cap, uint16_t* __restrict__ pair_seg) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= hdr[kHdrPairs]) return;
+  const int32_t n_items = (int32_t)min<int64_t>(hdr[kHdrItems], items_cap);
+  if (n_items < 1) return;
+  const int32_t seg = before[k] + (segment_head(k, item_flag, pair_rb) ? 1 : 0) - 1;
+  const int32_t it = upper_index(item_pair0, n_items, (int32_t)k);
+  pair_seg[k] = (uint16_t)(seg - item_seg0[it]);
+}
+
 // Over segments sorted by cell: is segment q one of several of its cell?
 __device__ __forceinline__ bool shared_cell(const int32_t* keys, int64_t q, int64_t n) {
   return (q > 0 && keys[q - 1] == keys[q]) || (q + 1 < n && keys[q + 1] == keys[q]);
@@ -886,6 +924,7 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.header = take(16);
   L.pair_rd0 = take(nv);
   L.pair_ln = take(nv);
+  L.pair_seg = take((nv + 1) / 2);
   L.item_strip = take((size_t)L.items_cap);
   L.item_pair0 = take((size_t)L.items_cap + 1);
   L.item_seg0 = take((size_t)L.items_cap + 1);
@@ -1025,10 +1064,16 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
     k_segs_end<<<1, 64, 0, stream>>>(hdr, L.items_cap, S(L.item_seg0));
     k_pair_ln<<<g_nv, 256, 0, stream>>>(hdr, pair_row, pair_rb, pair_dn, item_flag, geom,
                                         reinterpret_cast<uint32_t*>(S(L.pair_ln)));
+    int32_t* seg_before = W(L.ws_head);  // pair heads are no longer needed
+    k_seg_flags<<<g_nv, 256, 0, stream>>>(hdr, pair_rb, item_flag, n_valid, seg_before);
+    scan_exclusive(seg_before, n_valid, sums, nullptr, stream);
+    k_pair_seg<<<g_nv, 256, 0, stream>>>(hdr, seg_before, pair_rb, item_flag, S(L.item_pair0),
+                                         S(L.item_seg0), L.items_cap,
+                                         reinterpret_cast<uint16_t*>(S(L.pair_seg)));
 
     // 6. slots of cells with several segments
     sort_current(L.cell_bits, hdr + kHdrSegs);
-    int32_t* slot = W(L.ws_head);  // pair heads are no longer needed
+    int32_t* slot = W(L.ws_head);  // segment flags are no longer needed
     k_slot_flags<<<g_nv, 256, 0, stream>>>(hdr, ck, n_valid, slot);
     scan_exclusive(slot, n_valid, sums, hdr + kHdrSlots, stream);
     k_seg_dest<<<g_nv, 256, 0, stream>>>(hdr, ck, cv, slot, S(L.seg_dest));

@@ -35,7 +35,8 @@ def layout(shape, n_valid: int, n_occ: int) -> dict:
     n_empty = max(cells - n_occ, 0)
     icap = sd["strips"] + n_valid // ITEM_PAIRS + 2
     rows = shape["B"] * shape["N"] * shape["H"] * shape["W"]
-    sizes = [("header", 16), ("pair_rd0", nv), ("pair_ln", nv), ("item_strip", icap),
+    sizes = [("header", 16), ("pair_rd0", nv), ("pair_ln", nv), ("pair_seg", (nv + 1) // 2),
+             ("item_strip", icap),
              ("item_pair0", icap + 1), ("item_seg0", icap + 1), ("seg_dest", nv),
              ("comb_cell", nocc), ("comb_slot0", nocc), ("empty", n_empty + 1),
              ("bp_cell", nv), ("bp_dn", nv), ("pix_pair0", rows + 1)]
@@ -60,6 +61,7 @@ def decode(buf: np.ndarray, shape, n_valid: int, n_occ: int) -> dict:
         n=n,
         pair_rd0=arr["pair_rd0"][:np_].astype(np.int64),
         pair_ln=arr["pair_ln"][:np_].view(np.uint32).astype(np.int64),
+        pair_seg=arr["pair_seg"].view(np.uint16)[:np_].astype(np.int64),
         item_strip=arr["item_strip"][:ni].astype(np.int64),
         item_pair0=arr["item_pair0"][:ni + 1].astype(np.int64),
         item_seg0=arr["item_seg0"][:ni + 1].astype(np.int64),
@@ -117,6 +119,8 @@ def derive(plan: dict, shape) -> dict:
     nsegs = seg_p0.size
     item_seg0 = np.searchsorted(seg_p0, item_pair0)
     pair_ln = p_lp | np.where(seg_head, PAIR_HEAD, 0) | (npts << 16)
+    pair_item = np.searchsorted(np.array(item_pair0), np.arange(npairs), side="right") - 1
+    pair_seg = (np.cumsum(seg_head) - 1) - item_seg0[pair_item]
     # slots: segments sorted by cell (stably); cells with several segments
     so = np.argsort(seg_cell, kind="stable")
     keys = seg_cell[so]
@@ -143,7 +147,7 @@ def derive(plan: dict, shape) -> dict:
         n=dict(pairs=int(npairs), items=n_items, segs=int(nsegs), valid=n, occ=int(run_head.sum()),
                occ_found=int(run_head.sum()), empty=int(empty.size), slots=int(shared.sum()),
                comb=int(comb.sum()), strips=int(s_p0.size - 1)),
-        pair_rd0=p_rd0, pair_ln=pair_ln, item_strip=np.array(item_strip, dtype=np.int64),
+        pair_rd0=p_rd0, pair_ln=pair_ln, pair_seg=pair_seg, item_strip=np.array(item_strip, dtype=np.int64),
         item_pair0=np.r_[np.array(item_pair0, dtype=np.int64), npairs],
         item_seg0=np.r_[item_seg0, nsegs].astype(np.int64), seg_dest=seg_dest,
         comb_cell=comb_cell, comb_slot0=comb_slot0, empty=empty,

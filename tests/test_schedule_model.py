@@ -49,6 +49,7 @@ def _execute(sch, depth, feat, shape):
             if ln & _sched.PAIR_HEAD:
                 seg += 1
             assert k > p0 or ln & _sched.PAIR_HEAD
+            assert sch["pair_seg"][k] == seg
             lp, n = ln & (_sched.PAIR_HEAD - 1), ln >> 16
             assert lp < npix and n >= 1
             rd0 = int(sch["pair_rd0"][k])
@@ -134,3 +135,100 @@ def test_strip_dims_budget():
         assert sd["pixels"] * 4 * min(C, 256) <= _sched.STRIP_BYTES or sd["pixels"] == 1
     sd = _sched.strip_dims(dict(B=1, N=6, H=40, W=100, C=80))
     assert (sd["bh"], sd["bw"], sd["strips"]) == (40, 2, 300)
+
+
+def _walk_partition(sch, depth, feat, shape, G):
+    """The scheduled forward's in-item work split, executed on the CPU: an
+    item's pairs are cut into G equal ranges; a range sums its segments,
+    stores the ones it holds whole, keeps the part of a segment it starts
+    inside (handed to the range holding that segment's start) and of one it
+    ends inside (which then adds the following ranges' parts in order)."""
+    B, N, D, H, W, C = (shape[k] for k in "BNDHWC")
+    hw = H * W
+    cells = B * shape["Z"] * shape["Y"] * shape["X"]
+    sd = _sched.strip_dims(shape)
+    dflat = depth.reshape(-1).astype(np.float64)
+    fflat = feat.reshape(-1, C).astype(np.float64)
+    out = np.full((cells, C), np.nan)
+    slots = np.full((sch["n"]["slots"], C), np.nan)
+    per = sd["nhb"] * sd["nwb"]
+
+    def store(dest, v):
+        target = out[dest] if dest >= 0 else slots[~dest]
+        assert np.isnan(target).all()
+        target[:] = v
+
+    for i in range(sch["n"]["items"]):
+        s = int(sch["item_strip"][i])
+        bn, r = divmod(s, per)
+        hb, wb = divmod(r, sd["nwb"])
+        h0, w0 = hb * sd["bh"], wb * sd["bw"]
+        bws = min(sd["bw"], W - w0)
+        p0, p1 = sch["item_pair0"][i], sch["item_pair0"][i + 1]
+        np_ = p1 - p0
+        g0 = sch["item_seg0"][i]
+        ln = sch["pair_ln"][p0:p1]
+        head = (ln & _sched.PAIR_HEAD) != 0
+        seg = sch["pair_seg"][p0:p1]
+        lp = ln & (_sched.PAIR_HEAD - 1)
+        n = ln >> 16
+        rd0 = sch["pair_rd0"][p0:p1]
+        rows = (bn * H + h0 + lp // bws) * W + w0 + lp % bws
+        wts = np.array([sum(dflat[rd0[k] + j * hw] for j in range(n[k])) for k in range(np_)])
+        dest = sch["seg_dest"][g0:]
+        rb = lambda g: (g * np_) // G
+        first, last = {}, {}
+        for g in range(G):
+            kb, ke = rb(g), rb(g + 1)
+            if kb >= ke:
+                continue
+            prev_cont = not head[kb]
+            next_cont = ke < np_ and not head[ke]
+            cur, pend, acc = seg[kb], prev_cont, np.zeros(C)
+            for k in range(kb, ke):
+                if head[k] and k != kb:
+                    if pend:
+                        first[g], pend = acc, False
+                    else:
+                        store(dest[cur], acc)
+                    acc, cur = np.zeros(C), cur + 1
+                acc = acc + wts[k] * fflat[rows[k]]
+            if pend:
+                first[g] = acc
+            elif next_cont:
+                last[g] = (acc, seg[ke - 1])
+            else:
+                store(dest[cur], acc)
+        for g, (v, sg) in last.items():
+            total = v.copy()
+            for g2 in range(g + 1, G):
+                b2, e2 = rb(g2), rb(g2 + 1)
+                if b2 >= e2:
+                    continue
+                if head[b2]:
+                    break
+                total += first[g2]
+                if not (seg[e2 - 1] == sg and e2 < np_ and not head[e2]):
+                    break
+            store(dest[sg], total)
+    for j, c in enumerate(sch["comb_cell"]):
+        out[c] = slots[sch["comb_slot0"][j]:sch["comb_slot0"][j + 1]].sum(axis=0)
+    out[sch["empty"]] = 0.0
+    return out
+
+
+@pytest.mark.parametrize("G", [1, 7, 36, 64, 5000])
+def test_walk_partition_model(G):
+    # every output row written once and equal to the oracle, whatever the
+    # number of ranges (more ranges than pairs included)
+    shape = dict(B=1, N=2, D=12, H=6, W=5, C=8, X=6, Y=6, Z=1)
+    rng = np.random.default_rng(G)
+    data = draw_small(rng, shape)
+    coor = random_coor(rng, shape, p_out=0.2)
+    coor[::3, 0] = coor[0, 0]  # long segments across ranges
+    plan = oracle.prepare_ref(coor, shape)
+    sch = _sched.derive(plan, shape)
+    out = _walk_partition(sch, data["depth"], data["feat"], shape, G)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+    ref = ref.reshape(out.shape)
+    assert np.all(np.abs(out - ref) <= 1e-12 * mag.reshape(out.shape) + 1e-300)
