@@ -20,11 +20,12 @@
 //   1. k_zero_vec clears grad_depth (coalesced), so dropped points are 0;
 //   2. k_bwd_pixels gives each pixel to a group of GS lanes holding its
 //      feature row; lane l of the group takes pair l of the current chunk
-//      and sums that pair's depth scores; the group then walks the chunk,
-//      reading one grad_out row per pair (a pair's points share their cell),
-//      reducing the dot product with the feature row across the group, which
-//      is grad_depth of every point of the pair, and adding the pair's depth
-//      sum times the row to grad_feat.
+//      and sums that pair's depth scores; the group then walks the chunk U
+//      pairs at a time, reading one grad_out row per pair (a pair's points
+//      share their cell), adding the pair's depth sum times the row to
+//      grad_feat, and reducing the U dot products with the feature row across
+//      the group in one butterfly reduce-scatter; each total is grad_depth of
+//      every point of its pair.
 
 #include "device_utils.h"
 #include "internal.h"
@@ -190,19 +191,71 @@ struct PixArgs {
   int32_t C, D, hw;
   int32_t n_pairs;
   int64_t per_view, rows, cells;
+  int32_t blocks;  // logical blocks (the grid is rounded up to a multiple of kXcds)
 };
 
-constexpr int kPixUnroll = 4;  // grad_out rows in flight per group
+// Pixel order and block placement.  Blocks take consecutive pixels of an
+// image row; the XCD-aware mapping gives each XCD a contiguous run of blocks,
+// so that the grad_depth lines written by neighbouring pixels (adjacent in
+// memory) and the grad_out rows of neighbouring rays stay in one L2.
+// (Column-major pixel order was measured slower.)
+constexpr bool kPixXcdMap = true;
+constexpr int kPixUnrollMax = 8;
 
-template <typename TIn, typename TG, int VEC, int NV>
+// grad_out rows in flight per group: up to kPixUnrollMax, within 64 registers
+// of row data (always a power of two)
+constexpr int pix_unroll(int vec, int nv) {
+  return vec * nv >= 64 ? 1 : (64 / (vec * nv) < kPixUnrollMax ? 64 / (vec * nv) : kPixUnrollMax);
+}
+constexpr int kDepthBurst = 2;  // depth scores of a pair loaded before any is summed
+
+// Butterfly reduce-scatter of U per-lane partial sums over a group of GS
+// lanes (both powers of two).  Lane offsets O = GS/2, GS/4, ... : while a lane
+// holds M > 1 values it keeps one half (the upper half when bit O of its group
+// index is set) and adds the partner's copy of that half; once it holds one
+// value the remaining offsets all-reduce it.  Afterwards v[i], i < max(1, U/GS),
+// is the group total of value base + i; lanes that share base differ only in
+// their low bits.  U - 1 + log2(GS/U) shuffles instead of U * log2(GS).
+template <int O, int M, int U>
+struct ReduceScatter {
+  static __device__ __forceinline__ void run(float (&v)[U], int vi, int& base) {
+    if constexpr (O >= 1) {
+      if constexpr (M > 1) {
+        const bool up = (vi & O) != 0;
+#pragma unroll
+        for (int i = 0; i < M / 2; ++i) {
+          const float send = up ? v[i] : v[i + M / 2];
+          const float keep = up ? v[i + M / 2] : v[i];
+          v[i] = keep + __shfl_xor(send, O);
+        }
+        if (up) base += M / 2;
+        ReduceScatter<O / 2, M / 2, U>::run(v, vi, base);
+      } else {
+        v[0] += __shfl_xor(v[0], O);
+        ReduceScatter<O / 2, 1, U>::run(v, vi, base);
+      }
+    }
+  }
+};
+
+template <typename TIn, typename TG, int VEC, int NV, int GS>
 __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
     const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
-    TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a, int GS) {
+    TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a) {
+  constexpr int G = kWave / GS;
+  constexpr int U = pix_unroll(VEC, NV);
+  constexpr int M = U > GS ? U / GS : 1;  // pair totals a lane holds after the reduction
+  constexpr int LPU = GS * M / U;         // lanes holding the same pair totals
   const int lane = lane_id();
-  const int G = kWave / GS;
   const int g = lane / GS;
   const int vi = lane - g * GS;
-  const int64_t f = ((int64_t)blockIdx.x * kBwdWaves + threadIdx.x / kWave) * G + g;
+  int64_t blk = blockIdx.x;
+  if (kPixXcdMap) {  // hardware block b runs on XCD b % kXcds
+    const int64_t per_xcd = gridDim.x / kXcds;
+    blk = (blk % kXcds) * per_xcd + blk / kXcds;
+    if (blk >= a.blocks) return;
+  }
+  const int64_t f = (blk * kBwdWaves + threadIdx.x / kWave) * G + g;
   if (f >= a.rows) return;  // whole groups leave together
   const int C = a.C;
   const int CV = C / VEC;
@@ -228,20 +281,31 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
       const int32_t c = a.bp_cell[pb + vi];
       const uint32_t dn = a.bp_dn[pb + vi];
       const int32_t d0 = (int32_t)(dn & 0xffffu), n = (int32_t)(dn >> 16);
-      if (c >= 0 && c < a.cells && d0 + n <= a.D) {
+      if (c >= 0 && c < a.cells && n >= 1 && d0 + n <= a.D) {
         my_cell = c;
         my_dn = dn;
-        for (int32_t q = 0; q < n; ++q) my_w += to_float(depth[dbase + (int64_t)(d0 + q) * a.hw]);
+        // the first kDepthBurst scores loaded together, the rest (rare) after
+        float dq[kDepthBurst];
+#pragma unroll
+        for (int q = 0; q < kDepthBurst; ++q)  // clamped to the run: always in range
+          dq[q] = to_float(depth[dbase + (int64_t)(d0 + min(q, n - 1)) * a.hw]);
+#pragma unroll
+        for (int q = 1; q < kDepthBurst; ++q) dq[q] = q < n ? dq[q] : 0.f;
+        float wsum = dq[0];  // (no constant start: it would be folded into a load's branch)
+#pragma unroll
+        for (int q = 1; q < kDepthBurst; ++q) wsum += dq[q];
+        for (int32_t q = kDepthBurst; q < n; ++q) wsum += to_float(depth[dbase + (int64_t)(d0 + q) * a.hw]);
+        my_w = wsum;
       }
     }
     const int cnt = min(GS, p_end - pb);
-    for (int j0 = 0; j0 < cnt; j0 += kPixUnroll) {
-      int32_t cell[kPixUnroll];
-      uint32_t dn[kPixUnroll];
-      float w[kPixUnroll];
-      float gv[kPixUnroll][NV][VEC];
+    for (int j0 = 0; j0 < cnt; j0 += U) {
+      int32_t cell[U];
+      uint32_t dn[U];
+      float w[U];
+      float gv[U][NV][VEC];
 #pragma unroll
-      for (int u = 0; u < kPixUnroll; ++u) {
+      for (int u = 0; u < U; ++u) {
         const int src = g * GS + ((j0 + u) & (GS - 1));
         cell[u] = __shfl(my_cell, src);
         dn[u] = (uint32_t)__shfl((int32_t)my_dn, src);
@@ -256,21 +320,34 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
             Vec<TG, VEC>::load(grad_out + (int64_t)cell[u] * C + (int64_t)v * VEC, gv[u][k]);
         }
       }
+      float part[U];
 #pragma unroll
-      for (int u = 0; u < kPixUnroll; ++u) {
-        float part = 0.f;
+      for (int u = 0; u < U; ++u) {
+        float p = 0.f;
 #pragma unroll
         for (int k = 0; k < NV; ++k)
 #pragma unroll
           for (int e = 0; e < VEC; ++e) {
-            part = fmaf(gv[u][k][e], fv[k][e], part);
+            p = fmaf(gv[u][k][e], fv[k][e], p);
             acc[k][e] = fmaf(w[u], gv[u][k][e], acc[k][e]);
           }
-        for (int o = GS >> 1; o > 0; o >>= 1) part += __shfl_xor(part, o);
-        if (cell[u] >= 0) {
-          const int32_t d0 = (int32_t)(dn[u] & 0xffffu), n = (int32_t)(dn[u] >> 16);
-          for (int32_t q = vi; q < n; q += GS)
-            grad_depth[dbase + (int64_t)(d0 + q) * a.hw] = (TIn)part;
+        part[u] = p;
+      }
+      int base = 0;
+      ReduceScatter<GS / 2, U, U>::run(part, vi, base);
+      // lane vi holds the dot products of pairs j0 + base + i; the LPU lanes
+      // sharing them write the pairs' points in turn
+#pragma unroll
+      for (int i = 0; i < M; ++i) {
+        int32_t c = -1;
+        uint32_t d = 0;
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+          if (u == base + i) c = cell[u], d = dn[u];
+        if (c >= 0) {
+          const int32_t d0 = (int32_t)(d & 0xffffu), n = (int32_t)(d >> 16);
+          for (int32_t q = vi & (LPU - 1); q < n; q += LPU)
+            grad_depth[dbase + (int64_t)(d0 + q) * a.hw] = (TIn)part[i];
         }
       }
     }
@@ -282,32 +359,40 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
   }
 }
 
-template <typename TIn, typename TG, int VEC, int NV>
+template <typename TIn, typename TG, int VEC, int NV, int GS>
 hipError_t run_pixels(const Dims& d, const void* grad_out, const void* depth, const void* feat,
                       const PixArgs& a, void* grad_depth, void* grad_feat, hipStream_t stream) {
-  const int CV = (int)d.C / VEC;
-  const int per_lane = (CV + NV - 1) / NV;
-  int GS = 1;
-  while (GS < per_lane) GS <<= 1;
-  const int G = kWave / GS;
+  constexpr int G = kWave / GS;
   const int64_t pix_per_block = (int64_t)G * kBwdWaves;
-  const dim3 grid((unsigned)((d.rows + pix_per_block - 1) / pix_per_block));
-  k_bwd_pixels<TIn, TG, VEC, NV><<<grid, dim3(kBwdThreads), 0, stream>>>(
+  PixArgs b = a;
+  b.blocks = (int32_t)((d.rows + pix_per_block - 1) / pix_per_block);
+  const int64_t nb = kPixXcdMap ? (b.blocks + kXcds - 1) / kXcds * kXcds : b.blocks;
+  k_bwd_pixels<TIn, TG, VEC, NV, GS><<<dim3((unsigned)nb), dim3(kBwdThreads), 0, stream>>>(
       static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
-      static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat),
-      a, GS);
+      static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat), b);
   return hipGetLastError();
 }
 
+// A group of GS lanes (the smallest power of two with GS * NV >= C / VEC)
+// holds a pixel's row; C <= 1024 keeps GS <= 64 for NV = 16.
 template <typename TIn, typename TG, int VEC>
 hipError_t run_pixels_nv(const Dims& d, const void* grad_out, const void* depth, const void* feat,
                          const PixArgs& a, void* grad_depth, void* grad_feat, hipStream_t stream) {
   const int64_t CV = d.C / VEC;
-  if (CV <= 64) return run_pixels<TIn, TG, VEC, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
-  if (CV <= 128) return run_pixels<TIn, TG, VEC, 2>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
-  if (CV <= 256) return run_pixels<TIn, TG, VEC, 4>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
-  if (CV <= 512) return run_pixels<TIn, TG, VEC, 8>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
-  return run_pixels<TIn, TG, VEC, 16>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
+#define BWD_RUN(NV, GS) \
+  return run_pixels<TIn, TG, VEC, NV, GS>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream)
+  if (CV <= 1) BWD_RUN(1, 1);
+  if (CV <= 2) BWD_RUN(1, 2);
+  if (CV <= 4) BWD_RUN(1, 4);
+  if (CV <= 8) BWD_RUN(1, 8);
+  if (CV <= 16) BWD_RUN(1, 16);
+  if (CV <= 32) BWD_RUN(1, 32);
+  if (CV <= 64) BWD_RUN(1, 64);
+  if (CV <= 128) BWD_RUN(2, 64);
+  if (CV <= 256) BWD_RUN(4, 64);
+  if (CV <= 512) BWD_RUN(8, 64);
+  BWD_RUN(16, 64);
+#undef BWD_RUN
 }
 
 template <typename T>
@@ -378,6 +463,7 @@ hipError_t launch_backward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.C = (int32_t)d.C;
   a.D = (int32_t)d.D;
   a.hw = (int32_t)d.hw;
+  a.blocks = 0;
   a.n_pairs = n_valid;  // pairs never outnumber kept points
   a.per_view = d.per_view;
   a.rows = d.rows;

@@ -48,7 +48,10 @@ def test_backward_full(name, path):
     assert np.all(gd.cpu().numpy().reshape(-1)[~kept] == 0.0)
 
 
-@pytest.mark.parametrize("C", [1, 3, 16, 17, 80, 260])
+# C picks the pixel kernel's lane-group size and vectors per lane: with 4-wide
+# (f32) or 8-wide (f16) vectors where C allows, else scalars, these cover
+# groups of 1 to 64 lanes and 1, 2, 4, 8 and 16 vectors per lane
+@pytest.mark.parametrize("C", [1, 3, 7, 16, 17, 24, 80, 200, 260, 600, 1023])
 @pytest.mark.parametrize("dtype,out_dtype", [("f32", "f32"), ("f16", "f16"), ("f16", "f32")])
 def test_backward_random_channels(C, dtype, out_dtype, path):
     shape = dict(B=2, N=2, D=9, H=7, W=13, C=C, X=12, Y=10, Z=2)
@@ -70,8 +73,11 @@ def test_backward_edge_cases(path):
     cases = {
         "no point in range": np.full((P, 3), 9, dtype=np.int32),
         "all points in one cell": np.tile(np.array([[1, 2, 0]], dtype=np.int32), (P, 1)),
+        "cells alternating along depth": np.tile(np.array([[1, 2, 0]], dtype=np.int32), (P, 1)),
         "random": random_coor(rng, shape),
     }
+    # every point its own pair: 70 pairs per pixel, more than one chunk of a lane group
+    cases["cells alternating along depth"].reshape(2, 70, 60, 3)[:, 1::2, :, 0] = 3
     for label, coor in cases.items():
         _gpu.say(f"backward edge case: {label} {path}")
         gd, gf, _ = _run(data, coor, shape, path)
