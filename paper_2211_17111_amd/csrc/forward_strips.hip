@@ -36,6 +36,7 @@
 #include "vec.h"
 
 #include <algorithm>
+#include <type_traits>
 
 namespace bevpool {
 
@@ -48,16 +49,14 @@ constexpr int kWaves = kNT / kWave;
 constexpr int kLoadWaves = 4;
 constexpr int kWalkWaves = kWaves - kLoadWaves;
 constexpr int kLoadThreads = kLoadWaves * kWave;
-constexpr int kLP = kItemPairs / kLoadThreads;              // pairs per loading thread
-constexpr int kLoadRows = kStripBytes / 16 / kLoadThreads;  // 16-byte row vectors per loading thread
 constexpr int kDepthBurst = 2;  // depth scores per pair loaded before any is summed
 constexpr int kRowBatch = 8;    // row vectors per loading thread in flight
 constexpr int kPairBatch = 8;   // pair records per loading thread in flight
-static_assert(kLoadRows % kRowBatch == 0 && kLP % kPairBatch == 0, "whole batches");
 constexpr int kBufBytes = kStripBytes + kItemPairs * 12;  // rows | pair records | destinations
 constexpr int kHdrCache = 128;  // item headers of a workgroup kept in LDS
 constexpr int kCombThreads = 256;
-static_assert(kItemPairs % kLoadThreads == 0, "pair records split evenly over the loading threads");
+static_assert(kItemPairs % kNT == 0 && kItemPairs % kLoadThreads == 0,
+              "pair records split evenly over the loading threads");
 static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
 
 struct StripArgs {
@@ -165,6 +164,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // two buffers of [rows, then partial sums | pair records | segment destinations]
   __shared__ __attribute__((aligned(16))) char smem[2 * kBufBytes];
   __shared__ int32_t s_hdr[3][kHdrCache + 1];  // strip, first pair, first segment
+  __shared__ int4 s_meta[kWalkWaves * kWave];  // each lane group's last walked range
+  __shared__ int32_t s_lsync;                  // arrivals of the loading waves (loader_sync)
+
   static_assert((int64_t)kWaves * kWave * 8 * sizeof(float) <= kStripBytes, "partial sums fit the row area");
   static_assert(kItemPairs <= 65535, "pair indices fit 16 bits");
   auto buf_rows = [&](int b) { return reinterpret_cast<RawT*>(smem + b * kBufBytes); };
@@ -211,6 +213,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     s_hdr[1][j] = a.item_pair0[i_begin + j];
     s_hdr[2][j] = a.item_seg0[i_begin + j];
   }
+  if (tid == 0) s_lsync = 0;
   lds_barrier();
   // item i's header (i clamped to this workgroup's items)
   auto header = [&](int i) {
@@ -265,48 +268,55 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     return lp * rowvec + (v - vi * kNV) * cvc + vi;
   };
 
-  // ---- loading waves: an item's rows, destinations and pair records into
-  // LDS buffer b.  Loads are unconditional where they can be, surplus lanes
-  // repeating an in-range address: a load under a branch makes the compiler
-  // wait for it where the branch joins.
-  const int lt = tid;  // loading thread (waves 0 .. kLoadWaves - 1)
-  auto load_item = [&](const ItemHdr& h, int b) {
+  // ---- an item's rows, destinations and pair records into LDS buffer b, by
+  // threads 0 .. NT - 1 (the loading waves; the whole workgroup for the first
+  // item, which nothing could overlap).  Loads are unconditional where they
+  // can be, surplus lanes repeating an in-range address: a load under a branch
+  // makes the compiler wait for it where the branch joins.
+  const int lt = tid;
+  auto load_item = [&](const ItemHdr& h, int b, auto nt_tag) {
+    constexpr int NT = decltype(nt_tag)::value;
+    constexpr int kLoadRows = kStripBytes / 16 / NT;  // 16-byte row vectors per thread
+    constexpr int kRB = kLoadRows < kRowBatch ? kLoadRows : kRowBatch;
+    constexpr int kLP = kItemPairs / NT;  // pairs per thread
+    constexpr int kPB = kLP < kPairBatch ? kLP : kPairBatch;
+    static_assert(kLoadRows % kRB == 0 && kLP % kPB == 0, "whole batches");
     const Geo g = geometry(h.strip);
     const int nvec = g.npix * rowvec;
     RawT* const s_rows = buf_rows(b);
     PairRec* const s_pr = buf_pr(b);
     int32_t* const s_dest = buf_dest(b);
     // rows and destinations, kLoadRounds rounds of loads in flight
-    for (int r0 = 0; r0 < kLoadRows; r0 += kRowBatch) {
-      RawT rv[kRowBatch];
+    for (int r0 = 0; r0 < kLoadRows; r0 += kRB) {
+      RawT rv[kRB];
 #pragma unroll
-      for (int u = 0; u < kRowBatch; ++u)
-        rv[u] = *vec_addr(g, min((r0 + u) * kLoadThreads + lt, nvec - 1));
+      for (int u = 0; u < kRB; ++u)
+        rv[u] = *vec_addr(g, min((r0 + u) * NT + lt, nvec - 1));
 #pragma unroll
-      for (int u = 0; u < kRowBatch; ++u) {
-        const int idx = (r0 + u) * kLoadThreads + lt;
+      for (int u = 0; u < kRB; ++u) {
+        const int idx = (r0 + u) * NT + lt;
         if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
       }
     }
-    for (int idx = kLoadRows * kLoadThreads + lt; idx < nvec; idx += kLoadThreads)
+    for (int idx = kLoadRows * NT + lt; idx < nvec; idx += NT)
       s_rows[vec_slot(idx)] = *vec_addr(g, idx);
-    for (int j = lt; j < h.nseg; j += kLoadThreads) s_dest[j] = a.seg_dest[h.g0 + j];
-    // pair records and their depth scores, kPairBatch pairs per thread at a time
-    for (int q0 = 0; q0 < kLP; q0 += kPairBatch) {
-      int32_t rd0[kPairBatch];
-      uint32_t ln[kPairBatch];
-      uint32_t sg[kPairBatch];
+    for (int j = lt; j < h.nseg; j += NT) s_dest[j] = a.seg_dest[h.g0 + j];
+    // pair records and their depth scores, kPB pairs per thread at a time
+    for (int q0 = 0; q0 < kLP; q0 += kPB) {
+      int32_t rd0[kPB];
+      uint32_t ln[kPB];
+      uint32_t sg[kPB];
 #pragma unroll
-      for (int q = 0; q < kPairBatch; ++q) {
-        const int k = h.p0 + min((q0 + q) * kLoadThreads + lt, max(h.np - 1, 0));
+      for (int q = 0; q < kPB; ++q) {
+        const int k = h.p0 + min((q0 + q) * NT + lt, max(h.np - 1, 0));
         rd0[q] = a.pair_rd0[k];
         ln[q] = a.pair_ln[k];
         sg[q] = a.pair_seg[k];
       }
-      float dv[kPairBatch][kDepthBurst];
+      float dv[kPB][kDepthBurst];
 #pragma unroll
-      for (int q = 0; q < kPairBatch; ++q) {
-        const int n = (q0 + q) * kLoadThreads + lt < h.np ? (int)(ln[q] >> 16) : 0;
+      for (int q = 0; q < kPB; ++q) {
+        const int n = (q0 + q) * NT + lt < h.np ? (int)(ln[q] >> 16) : 0;
 #pragma unroll
         for (int j = 0; j < kDepthBurst; ++j) {
           const int64_t p = (int64_t)rd0[q] + j * hw;
@@ -316,8 +326,8 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         }
       }
 #pragma unroll
-      for (int q = 0; q < kPairBatch; ++q) {
-        const int k = (q0 + q) * kLoadThreads + lt;
+      for (int q = 0; q < kPB; ++q) {
+        const int k = (q0 + q) * NT + lt;
         if (k < h.np) {
           const int n = (int)(ln[q] >> 16);
           // (no constant start: an add of 0.f would be folded into the load's branch)
@@ -353,12 +363,13 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   const bool active = walker && lg < gpw;
   const int64_t col = (int64_t)(cbase + vi) * VEC;
 
-  int kb = 0, ke = 0, last_seg = -1;
+  int kb = 0, ke = 0, last_seg = -1, first_seg = -1;
+  int32_t last_dest = 0;
   bool prev_cont = false, next_cont = false;
   float first_sum[VEC], last_sum[VEC];
 
-  auto store_seg = [&](const ItemHdr& h, const int32_t* s_dest, int sgi, const float* v) {
-    const int32_t d = s_dest[min(sgi, h.nseg - 1)];
+  // a segment's sum to its destination: a cell of `out`, or (~d) a slot
+  auto store_dest = [&](int32_t d, const float* v) {
     if (d >= 0) {
       if (d < a.cells) Vec<TOut, VEC>::store(out + (int64_t)d * C + col, v);
     } else {
@@ -378,7 +389,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     auto seg_at = [&](int k) { return (int)((s_pr[k].ps & ~kRecHead) >> kRecSegShift); };
     kb = ke = 0;
     prev_cont = next_cont = false;
-    last_seg = -1;
+    last_seg = first_seg = -1;
     float acc[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) acc[e] = first_sum[e] = last_sum[e] = 0.f;
@@ -393,7 +404,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
       prev_cont = !is_head(kb);
       next_cont = ke < np && !is_head(ke);
       last_seg = seg_at(ke - 1);
-      int cur = seg_at(kb);
+      first_seg = seg_at(kb);
+      last_dest = s_dest[min(last_seg, h.nseg - 1)];
+      int cur = first_seg;
       bool pend_first = prev_cont;
       auto end_segment = [&]() {  // segment `cur` has no more pairs in this range
         if (pend_first) {
@@ -401,7 +414,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           for (int e = 0; e < VEC; ++e) first_sum[e] = acc[e];
           pend_first = false;
         } else {
-          store_seg(h, s_dest, cur, acc);
+          store_dest(s_dest[min(cur, h.nseg - 1)], acc);
         }
 #pragma unroll
         for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
@@ -447,60 +460,94 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
 #pragma unroll
         for (int e = 0; e < VEC; ++e) last_sum[e] = acc[e];
       } else {
-        store_seg(h, s_dest, cur, acc);
+        store_dest(s_dest[min(cur, h.nseg - 1)], acc);
       }
     }
   };
 
-  // segments cut by range boundaries, added in range order (every wave
-  // passes the barriers; walking waves do the work)
-  auto combine_item = [&](const ItemHdr& h, int b) {
-    const PairRec* const s_pr = buf_pr(b);
-    const int32_t* const s_dest = buf_dest(b);
-    const int np = h.np;
-    auto is_head = [&](int k) { return (s_pr[k].ps & kRecHead) != 0; };
-    auto seg_at = [&](int k) { return (int)((s_pr[k].ps & ~kRecHead) >> kRecSegShift); };
-    // [G][cvc][VEC]: each group's part of the segment it starts inside
-    float* const part_a = reinterpret_cast<float*>(buf_rows(b));
-    const bool has_last = next_cont && !(prev_cont && seg_at(kb) == last_seg);
-    if (prev_cont) Vec<float, VEC>::store(part_a + ((int64_t)g * cvc + vi) * VEC, first_sum);
-    lds_barrier();
-    if (has_last) {
+  // ---- segments cut by range boundaries, added in range order.  After a
+  // walk every group publishes, in the walked buffer (its rows and records
+  // are no longer read): the part of the segment its range starts inside
+  // (part_first, over the rows), the part of the one it ends inside when it
+  // holds that segment's start (part_last, over the pair records and
+  // destinations), and a record of its range.  The loading waves add the
+  // parts up while the walking waves go on to the next item.
+  constexpr int kMetaPrev = 1, kMetaNext = 2, kMetaLast = 4, kMetaEmpty = 8;
+  static_assert((int64_t)kWalkWaves * kWave * 8 * sizeof(float) <= kItemPairs * 12,
+                "last parts fit the pair records and destinations");
+  auto part_first = [&](int b) { return reinterpret_cast<float*>(smem + b * kBufBytes); };
+  auto part_last = [&](int b) { return reinterpret_cast<float*>(smem + b * kBufBytes + kStripBytes); };
+  auto publish = [&](int b) {
+    if (!active) return;
+    int flags = kMetaEmpty;
+    if (kb < ke) {
+      const bool has_last = next_cont && !(prev_cont && first_seg == last_seg);
+      flags = (prev_cont ? kMetaPrev : 0) | (next_cont ? kMetaNext : 0) | (has_last ? kMetaLast : 0);
+      if (prev_cont) Vec<float, VEC>::store(part_first(b) + ((int64_t)g * cvc + vi) * VEC, first_sum);
+      if (has_last) Vec<float, VEC>::store(part_last(b) + ((int64_t)g * cvc + vi) * VEC, last_sum);
+    }
+    if (vi == 0) s_meta[g] = make_int4(last_seg, last_dest, flags, 0);
+  };
+  // group gg's segment that continues past its range: its part plus the
+  // following ranges' first parts, up to the range where that segment ends;
+  // handled by the lane groups of threads 0 .. nthreads - 1
+  auto combine_parts = [&](int b, int nthreads) {
+    if (lg >= gpw) return;
+    const int n_h = (nthreads / kWave) * gpw;
+    for (int gg = wave * gpw + lg; gg < G; gg += n_h) {
+      const int4 m = s_meta[gg];
+      if (!(m.z & kMetaLast)) continue;
       float sum[VEC];
-#pragma unroll
-      for (int e = 0; e < VEC; ++e) sum[e] = last_sum[e];
-      for (int g2 = g + 1; g2 < G; ++g2) {
-        const int b2 = (g2 * np) / G, e2 = ((g2 + 1) * np) / G;
-        if (b2 >= e2) continue;
-        if (is_head(b2)) break;
+      Vec<float, VEC>::load(part_last(b) + ((int64_t)gg * cvc + vi) * VEC, sum);
+      for (int g2 = gg + 1; g2 < G; ++g2) {
+        const int4 m2 = s_meta[g2];
+        if (m2.z & kMetaEmpty) continue;
+        if (!(m2.z & kMetaPrev)) break;  // range g2 starts a segment
         float t[VEC];
-        Vec<float, VEC>::load(part_a + ((int64_t)g2 * cvc + vi) * VEC, t);
+        Vec<float, VEC>::load(part_first(b) + ((int64_t)g2 * cvc + vi) * VEC, t);
 #pragma unroll
         for (int e = 0; e < VEC; ++e) sum[e] += t[e];
         // on to the next range only if this one lies wholly inside the segment
-        if (!(seg_at(e2 - 1) == last_seg && e2 < np && !is_head(e2))) break;
+        if (!(m2.x == m.x && (m2.z & kMetaNext))) break;
       }
-      store_seg(h, s_dest, last_seg, sum);
+      store_dest(m.y, sum);
     }
   };
 
+  // The loading waves wait for each other (the walking waves are walking,
+  // so no workgroup barrier can be used): each wave's lane 0 counts its
+  // arrival in LDS, then the wave waits until all kLoadWaves have arrived.
+  // Every loading wave runs the same item loop, so every wait ends.
+  int lsync_target = 0;
+  auto loader_sync = [&]() {
+    lsync_target += kLoadWaves;
+    if (lane == 0) __hip_atomic_fetch_add(&s_lsync, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
+    while (__hip_atomic_load(&s_lsync, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP) < lsync_target)
+      __builtin_amdgcn_s_sleep(1);
+  };
+
   // ---- the pipeline: item i is walked from buffer b while the loading
-  // waves fill buffer b ^ 1 with item i + 1
-  if (!walker) load_item(header(i_begin), 0);
+  // waves add up the cut segments of item i - 1 (published in buffer b ^ 1)
+  // and then fill buffer b ^ 1 with item i + 1
+  load_item(header(i_begin), 0, std::integral_constant<int, kNT>{});
   lds_barrier();
   int b = 0;
   for (int i = i_begin; i < i_begin + n_my; ++i) {
-    const ItemHdr hc = header(i);
     if (!walker) {
-      if (i + 1 < i_begin + n_my) load_item(header(i + 1), b ^ 1);
+      if (i > i_begin) {
+        combine_parts(b ^ 1, kLoadThreads);
+        loader_sync();  // every part read before buffer b ^ 1 is refilled
+      }
+      if (i + 1 < i_begin + n_my) load_item(header(i + 1), b ^ 1, std::integral_constant<int, kLoadThreads>{});
     } else {
-      walk_item(hc, b);
+      walk_item(header(i), b);
     }
-    lds_barrier();  // item i walked (its rows free for partial sums), item i + 1 loaded
-    combine_item(hc, b);
-    lds_barrier();  // buffer b free for item i + 2
+    lds_barrier();  // item i walked, item i - 1 combined, item i + 1 loaded
+    if (walker) publish(b);
+    lds_barrier();  // item i's parts published
     b ^= 1;
   }
+  combine_parts(b ^ 1, kNT);  // the last item's, by every wave
 }
 
 template <typename TOut, int VEC>
