@@ -58,6 +58,7 @@ constexpr int kCombThreads = 256;
 static_assert(kItemPairs % kNT == 0 && kItemPairs % kLoadThreads == 0,
               "pair records split evenly over the loading threads");
 static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
+static_assert(kShareItems <= kHdrCache, "a share's item headers fit the cache");
 
 struct StripArgs {
   const int32_t* hdr;
@@ -71,6 +72,7 @@ struct StripArgs {
   const int32_t* comb_cell;
   const int32_t* comb_slot0;
   const int32_t* empty;
+  const int32_t* share_item0;
   float* slots;
   int64_t slot_cap;  // slots the workspace holds
   int32_t n_valid, n_occ, items_cap;
@@ -175,21 +177,34 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     return reinterpret_cast<int32_t*>(smem + b * kBufBytes + kStripBytes + kItemPairs * sizeof(PairRec));
   };
 
+  // This workgroup's items.  Workgroup w = (die, slot) of a die-major
+  // numbering takes share w when the schedule's items were cut at this
+  // launch's workgroups (the same pair count for each), else an equal count
+  // of its die's items; either way a die holds a contiguous run of strips,
+  // so its L2 serves neighbouring strips' shared depth lines.
+  const int xcd = blockIdx.x % kXcds;
+  const int slot = blockIdx.x / kXcds;
+  const int nslots = gridDim.x / kXcds;
+  const int w_idx = xcd * nslots + slot;
   const int32_t* hdr = a.hdr;
+  // (the share bounds are read with the counts; used only if they apply)
+  const int32_t sh_lo = a.share_item0[min(w_idx, kMaxShares)];
+  const int32_t sh_hi = a.share_item0[min(w_idx + 1, kMaxShares)];
   if (hdr[kHdrOccFound] != a.n_occ || hdr[kHdrOcc] != a.n_occ) return;  // uniform
   const int32_t n_items = min(hdr[kHdrItems], a.items_cap);
   const int32_t n_pairs = min(hdr[kHdrPairs], a.n_valid);
   const int32_t n_segs = min(hdr[kHdrSegs], a.n_valid);
-  // This workgroup's items: a contiguous share of its die's contiguous range,
-  // so a die's L2 serves neighbouring strips' shared depth lines.
-  const int xcd = blockIdx.x % kXcds;
-  const int slot = blockIdx.x / kXcds;
-  const int nslots = gridDim.x / kXcds;
-  const int per_die = (n_items + kXcds - 1) / kXcds;
-  const int d_lo = min(xcd * per_die, n_items);
-  const int d_cnt = min(n_items, d_lo + per_die) - d_lo;
-  const int i_begin = d_lo + (int)(((int64_t)slot * d_cnt) / nslots);
-  const int i_end = d_lo + (int)(((int64_t)(slot + 1) * d_cnt) / nslots);
+  int i_begin, i_end;
+  if (hdr[kHdrSharesOk] == 1 && hdr[kHdrShares] == (int32_t)gridDim.x) {
+    i_begin = min(max(sh_lo, 0), n_items);
+    i_end = min(max(sh_hi, i_begin), n_items);
+  } else {
+    const int per_die = (n_items + kXcds - 1) / kXcds;
+    const int d_lo = min(xcd * per_die, n_items);
+    const int d_cnt = min(n_items, d_lo + per_die) - d_lo;
+    i_begin = d_lo + (int)(((int64_t)slot * d_cnt) / nslots);
+    i_end = d_lo + (int)(((int64_t)(slot + 1) * d_cnt) / nslots);
+  }
   if (i_begin >= i_end) return;
 
   const int C = a.C;
@@ -499,16 +514,31 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
       if (!(m.z & kMetaLast)) continue;
       float sum[VEC];
       Vec<float, VEC>::load(part_last(b) + ((int64_t)gg * cvc + vi) * VEC, sum);
-      for (int g2 = gg + 1; g2 < G; ++g2) {
-        const int4 m2 = s_meta[g2];
-        if (m2.z & kMetaEmpty) continue;
-        if (!(m2.z & kMetaPrev)) break;  // range g2 starts a segment
-        float t[VEC];
-        Vec<float, VEC>::load(part_first(b) + ((int64_t)g2 * cvc + vi) * VEC, t);
+      // the following ranges kChain at a time: their records and parts are
+      // read together (past the chain's end they are read and not used)
+      constexpr int kChain = 4;
+      bool go = true;
+      for (int g2 = gg + 1; go && g2 < G; g2 += kChain) {
+        int4 m2[kChain];
+        float t[kChain][VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) sum[e] += t[e];
-        // on to the next range only if this one lies wholly inside the segment
-        if (!(m2.x == m.x && (m2.z & kMetaNext))) break;
+        for (int u = 0; u < kChain; ++u) {
+          const int gi = min(g2 + u, G - 1);
+          m2[u] = s_meta[gi];
+          Vec<float, VEC>::load(part_first(b) + ((int64_t)gi * cvc + vi) * VEC, t[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kChain; ++u) {
+          if (!go || g2 + u >= G || (m2[u].z & kMetaEmpty)) continue;
+          if (!(m2[u].z & kMetaPrev)) {  // range g2 + u starts a segment
+            go = false;
+            continue;
+          }
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) sum[e] += t[u][e];
+          // on to the next range only if this one lies wholly inside the segment
+          if (!(m2[u].x == m.x && (m2[u].z & kMetaNext))) go = false;
+        }
       }
       store_dest(m.y, sum);
     }
@@ -610,19 +640,6 @@ __global__ __launch_bounds__(256) void k_zero_out(TOut* __restrict__ out, int64_
   if (i < nvec) store_zero<TOut, VEC>(out + i * VEC);
 }
 
-int device_cus() {
-  static int cached[64];  // per device; 0 = not yet queried
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
-  if (cached[dev] > 0) return cached[dev];
-  int cus = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
-      cus <= 0)
-    cus = 256;
-  cached[dev] = cus;
-  return cus;
-}
-
 template <typename TIn, typename TOut, int VEC>
 hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void* feat,
                StripArgs a, void* out, hipStream_t stream) {
@@ -632,7 +649,7 @@ hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void
   const unsigned chunks = (unsigned)((CV + kLanes - 1) / kLanes);
   // one persistent workgroup per CU (a whole number per die), more when a
   // workgroup would otherwise get more than kHdrCache items
-  const int64_t per_die_slots = std::max<int64_t>((device_cus() + kXcds - 1) / kXcds,
+  const int64_t per_die_slots = std::max<int64_t>(forward_workgroups() / kXcds,
                                                   a.items_cap / ((int64_t)kXcds * kHdrCache) + 1);
   const int blocks = (int)(per_die_slots * kXcds);
   k_fwd_strips<TIn, TOut, VEC><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
@@ -659,6 +676,21 @@ hipError_t zero_fill(const Dims& d, void* out, hipStream_t stream) {
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
 }  // namespace
+
+int device_cus() {
+  static int cached[64];  // per device; 0 = not yet queried
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) dev = 0;
+  if (cached[dev] > 0) return cached[dev];
+  int cus = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+      cus <= 0)
+    cus = 256;
+  cached[dev] = cus;
+  return cus;
+}
+
+int forward_workgroups() { return (device_cus() + kXcds - 1) / kXcds * kXcds; }
 
 size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots) {
   return (size_t)(n_slots > 0 ? n_slots : 0) * (size_t)d.C * sizeof(float);
@@ -693,6 +725,7 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.comb_cell = S(L.comb_cell);
   a.comb_slot0 = S(L.comb_slot0);
   a.empty = S(L.empty);
+  a.share_item0 = S(L.share_item0);
   a.slots = static_cast<float*>(workspace);
   a.slot_cap = workspace == nullptr ? 0 : (int64_t)(workspace_bytes / ((size_t)d.C * sizeof(float)));
   a.n_valid = n_valid;

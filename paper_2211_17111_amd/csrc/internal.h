@@ -62,9 +62,15 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //   pair     maximal run of kept points of one strip, one cell and one pixel
 //            over consecutive depth bins; pairs are ordered by (strip, BEV
 //            rank, local pixel, depth bin)
-//   item     a run of one strip's pairs: a strip with P pairs is cut into
-//            K = ceil(P / kItemPairs) items, item j starting at pair
-//            floor(j * P / K) of the strip
+//   share    pairs [c_w, c_(w+1)) of all P pairs, w < S: one share per
+//            workgroup of the scheduled forward (S = shares in the header), so
+//            that every workgroup sums about the same number of pairs;
+//            c_w = floor(P * w / S), moved to the start (end) of the strip it
+//            falls in when less than kMinPiece pairs from it
+//   item     a run of one strip's pairs inside one share: a strip is cut at
+//            the share boundaries inside it, and each piece of L pairs into
+//            K = ceil(L / kItemPairs) items, item j starting at pair
+//            floor(j * L / K) of the piece
 //   segment  maximal run of pairs of one cell inside one item
 //   slot     a float32 row of the forward workspace holding one segment's
 //            partial sum; only cells covered by several segments have slots,
@@ -85,12 +91,19 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //   bp_cell[n_valid]            pixel-major pairs (the pairs stably sorted by
 //   bp_dn[n_valid]                feature rank): BEV rank, d0 | points << 16
 //   pix_pair0[rows + 1]         first pixel-major pair of each feature row
+//   share_item0[kMaxShares + 1] first item of each share (+ end sentinel:
+//                               items), for the shares in the header
 constexpr int kItemPairs = 2048;          // most pairs of one forward item
 constexpr int kStripBytes = 32 * 1024;    // staged feature bytes of a strip (4-byte elements)
 constexpr uint32_t kPairHead = 1u << 15;  // pair_ln: first pair of a segment
 constexpr uint32_t kPairPixel = kPairHead - 1;
 constexpr int kHdrPairs = 0, kHdrItems = 1, kHdrSegs = 2, kHdrValid = 3, kHdrOcc = 4,
-              kHdrOccFound = 5, kHdrEmpty = 6, kHdrSlots = 7, kHdrComb = 8, kHdrStrips = 9;
+              kHdrOccFound = 5, kHdrEmpty = 6, kHdrSlots = 7, kHdrComb = 8, kHdrStrips = 9,
+              kHdrShares = 10,     // S, the shares the items are cut at
+              kHdrSharesOk = 11;   // 1 if no share has more than kShareItems items
+constexpr int kMaxShares = 1024;   // most shares (workgroups of the scheduled forward)
+constexpr int kShareItems = 128;   // most items of a share the forward takes as one
+constexpr int kMinPiece = 512;     // share boundaries closer to a strip end move to it
 static_assert(kHdrPairs == BEVPOOL_SCHEDULE_PAIRS && kHdrItems == BEVPOOL_SCHEDULE_ITEMS &&
                   kHdrSegs == BEVPOOL_SCHEDULE_SEGMENTS && kHdrValid == BEVPOOL_SCHEDULE_KEPT &&
                   kHdrOcc == BEVPOOL_SCHEDULE_CELLS && kHdrOccFound == BEVPOOL_SCHEDULE_CELLS_FOUND &&
@@ -113,7 +126,7 @@ StripDims strip_dims(const Dims& d);
 
 struct ScheduleLayout {
   size_t header, pair_rd0, pair_ln, pair_seg, item_strip, item_pair0, item_seg0, seg_dest, comb_cell,
-      comb_slot0, empty, bp_cell, bp_dn, pix_pair0, total;
+      comb_slot0, empty, bp_cell, bp_dn, pix_pair0, share_item0, total;
   int64_t n_valid, n_occ, n_empty, items_cap;
   StripDims sd;
   // build workspace
@@ -123,6 +136,11 @@ struct ScheduleLayout {
   int row_bits, cell_bits, pixel_bits, strip_bits;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
+// Compute units of the current device (cached per device).
+int device_cus();
+// Workgroups of the scheduled forward on the current device: one per CU,
+// a whole number per die; the shares a schedule is cut at.
+int forward_workgroups();
 hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
                            int32_t n_intervals, void* schedule, void* workspace,
                            hipStream_t stream);

@@ -565,42 +565,116 @@ __global__ void k_strips_end(const int32_t* __restrict__ hdr, int32_t* __restric
   if (threadIdx.x == 0 && blockIdx.x == 0) strip_p0[hdr[kHdrStrips]] = hdr[kHdrPairs];
 }
 
+// Share boundary w, floor(P * w / S), moved to the start or end of the strip
+// [a, b) it falls in when within kMinPiece pairs of it, so that no item is
+// a small remnant of a strip.
+__device__ __forceinline__ int64_t snap_bound(int64_t c, int64_t a, int64_t b) {
+  if (c - a < kMinPiece) return a;
+  if (b - c < kMinPiece) return b;
+  return c;
+}
+
+// The items of strip j: its pairs [a, b) are cut at the (snapped) share
+// boundaries inside (a, b), and each piece of L pairs into ceil(L /
+// kItemPairs) items starting at floor(i * L / K) of the piece.  visit(i,
+// first) is called for every item start in order; returns the count.
+template <typename F>
+__device__ int64_t strip_items(int64_t a, int64_t b, int64_t P, int64_t S, F visit) {
+  // shares w with a < floor(P w / S) < b: floor(P w / S) > a  <=>
+  // w >= ceil((a + 1) S / P); floor(P w / S) < b  <=>  w < ceil(b S / P)
+  const int64_t w_lo = ((a + 1) * S + P - 1) / P;
+  const int64_t w_hi = (b * S + P - 1) / P - 1;
+  int64_t n = 0;
+  int64_t q = a;
+  for (int64_t w = w_lo; w <= w_hi + 1; ++w) {
+    const int64_t e = w <= w_hi ? snap_bound((P * w) / S, a, b) : b;  // end of this piece
+    const int64_t L = e - q;
+    if (L > 0) {
+      const int64_t K = (L + kItemPairs - 1) / kItemPairs;
+      for (int64_t i = 0; i < K; ++i) visit(n + i, q + (i * L) / K);
+      n += K;
+      q = e;
+    }
+  }
+  return n;
+}
+
 // Items of every listed strip (0 past the last one, up to cap).
 __global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
                                                      const int32_t* __restrict__ strip_p0,
-                                                     int64_t cap, int32_t* __restrict__ count) {
+                                                     int64_t cap, int64_t shares,
+                                                     int32_t* __restrict__ count) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= cap) return;
   int32_t k = 0;
-  if (j < hdr[kHdrStrips]) {
-    const int64_t np = (int64_t)strip_p0[j + 1] - strip_p0[j];
-    k = (int32_t)((np + kItemPairs - 1) / kItemPairs);
-  }
+  if (j < hdr[kHdrStrips])
+    k = (int32_t)strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares,
+                             [](int64_t, int64_t) {});
   count[j] = k;
 }
 
-// With the item counts exclusively scanned: item j of a strip with P pairs
-// starts at its pair floor(j * P / K); item_flag marks item starts (item + 1).
+// With the item counts exclusively scanned: every item's strip and first
+// pair; item_flag marks item starts (item + 1).
 __global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict__ hdr,
                                                       const int32_t* __restrict__ strip_id,
                                                       const int32_t* __restrict__ strip_p0,
                                                       const int32_t* __restrict__ offset,
-                                                      int64_t items_cap,
+                                                      int64_t items_cap, int64_t shares,
                                                       int32_t* __restrict__ item_strip,
                                                       int32_t* __restrict__ item_pair0,
                                                       int32_t* __restrict__ item_flag) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= hdr[kHdrStrips]) return;
-  const int64_t p0 = strip_p0[j];
-  const int64_t np = (int64_t)strip_p0[j + 1] - p0;
-  const int64_t K = (np + kItemPairs - 1) / kItemPairs;
-  for (int64_t i = 0; i < K; ++i) {
-    const int64_t item = (int64_t)offset[j] + i;
+  const int32_t sid = strip_id[j];
+  const int64_t off = offset[j];
+  strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares, [&](int64_t i, int64_t first) {
+    const int64_t item = off + i;
     if (item >= items_cap) return;
-    const int64_t first = p0 + (i * np) / K;
-    item_strip[item] = strip_id[j];
+    item_strip[item] = sid;
     item_pair0[item] = (int32_t)first;
     item_flag[first] = (int32_t)(item + 1);
+  });
+}
+
+// First item of every share (an item starts at every share boundary inside
+// the pairs), and whether no share holds more than kShareItems items.  One
+// block of kShareThreads threads.
+constexpr int kShareThreads = 1024;
+__global__ __launch_bounds__(kShareThreads) void k_share_items(int32_t* __restrict__ hdr,
+                                                               const int32_t* __restrict__ strip_p0,
+                                                               const int32_t* __restrict__ item_pair0,
+                                                               int64_t items_cap, int32_t shares,
+                                                               int32_t* __restrict__ share_item0) {
+  __shared__ int32_t s_bad;
+  if (threadIdx.x == 0) s_bad = 0;
+  const int64_t P = hdr[kHdrPairs];
+  const int64_t n_items = min<int64_t>(hdr[kHdrItems], items_cap);
+  const int64_t n_strips = hdr[kHdrStrips];
+  for (int w = threadIdx.x; w <= shares; w += kShareThreads) {
+    int64_t c = (P * w) / shares;
+    if (c > 0 && c < P) {  // the strip holding pair c: the last one starting at or before it
+      int64_t lo = 0, hi = n_strips;
+      while (hi - lo > 1) {
+        const int64_t mid = (lo + hi) >> 1;
+        if (strip_p0[mid] <= c) lo = mid; else hi = mid;
+      }
+      c = snap_bound(c, strip_p0[lo], strip_p0[lo + 1]);
+    }
+    // lower bound of c among the item starts
+    int64_t lo = 0, hi = n_items;
+    while (lo < hi) {
+      const int64_t mid = (lo + hi) >> 1;
+      if (item_pair0[mid] < c) lo = mid + 1; else hi = mid;
+    }
+    share_item0[w] = (int32_t)lo;
+  }
+  __syncthreads();
+  for (int w = threadIdx.x; w < shares; w += kShareThreads)
+    if (share_item0[w + 1] - share_item0[w] > kShareItems) s_bad = 1;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    hdr[kHdrShares] = shares;
+    hdr[kHdrSharesOk] = s_bad ? 0 : 1;
   }
 }
 
@@ -911,8 +985,9 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.n_occ = n_intervals;
   L.n_empty = d.cells > n_intervals ? d.cells - n_intervals : 0;
   L.sd = strip_dims(d);
-  // sum over strips of ceil(P_s / kItemPairs) <= n_pairs / kItemPairs + strips
-  L.items_cap = L.sd.strips + n_valid / kItemPairs + 2;
+  // pieces (strips cut at shares) number at most strips + shares - 1, and
+  // the sum over pieces of ceil(L / kItemPairs) <= n_pairs / kItemPairs + pieces
+  L.items_cap = L.sd.strips + n_valid / kItemPairs + kMaxShares + 2;
   const size_t nv = (size_t)(n_valid > 0 ? n_valid : 1);
   const size_t nocc = (size_t)n_intervals + 1;
   size_t off = 0;
@@ -935,6 +1010,7 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.bp_cell = take(nv);
   L.bp_dn = take(nv);
   L.pix_pair0 = take((size_t)d.rows + 1);
+  L.share_item0 = take((size_t)kMaxShares + 1);
   L.total = off;
 
   const int64_t span = std::max<int64_t>((int64_t)nv, d.cells);
@@ -1047,13 +1123,16 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
     k_compact_scatter<<<grid, block, 0, stream>>>(sh, tiles);
     k_strips_end<<<1, 64, 0, stream>>>(hdr, strip_p0);
     const unsigned g_s = (unsigned)((scap + 255) / 256);
-    k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, icount);
+    const int32_t shares = (int32_t)std::min<int64_t>(forward_workgroups(), kMaxShares);
+    k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, shares, icount);
     scan_exclusive(icount, scap, sums, hdr + kHdrItems, stream);
     int32_t* item_flag = W(L.ws_flags);
     k_fill_i32<<<g_nv, 256, 0, stream>>>(item_flag, n_valid, 0);
-    k_item_scatter<<<g_s, 256, 0, stream>>>(hdr, strip_id, strip_p0, icount, L.items_cap,
+    k_item_scatter<<<g_s, 256, 0, stream>>>(hdr, strip_id, strip_p0, icount, L.items_cap, shares,
                                             S(L.item_strip), S(L.item_pair0), item_flag);
     k_items_end<<<1, 64, 0, stream>>>(hdr, L.items_cap, S(L.item_pair0));
+    k_share_items<<<1, kShareThreads, 0, stream>>>(hdr, strip_p0, S(L.item_pair0), L.items_cap, shares,
+                                                   S(L.share_item0));
 
     // 5. segments and pair records
     ck = W(L.ws_ka); cv = W(L.ws_va); ak = W(L.ws_kb); av = W(L.ws_vb);

@@ -14,7 +14,11 @@ ALIGN = 256
 ITEM_PAIRS = 2048
 STRIP_BYTES = 32 * 1024
 PAIR_HEAD = 1 << 15
-HDR = dict(pairs=0, items=1, segs=2, valid=3, occ=4, occ_found=5, empty=6, slots=7, comb=8, strips=9)
+MAX_SHARES = 1024
+SHARE_ITEMS = 128
+MIN_PIECE = 512
+HDR = dict(pairs=0, items=1, segs=2, valid=3, occ=4, occ_found=5, empty=6, slots=7, comb=8, strips=9,
+           shares=10, shares_ok=11)
 
 
 def strip_dims(shape) -> dict:
@@ -33,13 +37,14 @@ def layout(shape, n_valid: int, n_occ: int) -> dict:
     nv = max(n_valid, 1)
     nocc = n_occ + 1
     n_empty = max(cells - n_occ, 0)
-    icap = sd["strips"] + n_valid // ITEM_PAIRS + 2
+    icap = sd["strips"] + n_valid // ITEM_PAIRS + MAX_SHARES + 2
     rows = shape["B"] * shape["N"] * shape["H"] * shape["W"]
     sizes = [("header", 16), ("pair_rd0", nv), ("pair_ln", nv), ("pair_seg", (nv + 1) // 2),
              ("item_strip", icap),
              ("item_pair0", icap + 1), ("item_seg0", icap + 1), ("seg_dest", nv),
              ("comb_cell", nocc), ("comb_slot0", nocc), ("empty", n_empty + 1),
-             ("bp_cell", nv), ("bp_dn", nv), ("pix_pair0", rows + 1)]
+             ("bp_cell", nv), ("bp_dn", nv), ("pix_pair0", rows + 1),
+             ("share_item0", MAX_SHARES + 1)]
     off, out = 0, {}
     for name, n in sizes:
         out[name] = (off // 4, n)
@@ -72,11 +77,34 @@ def decode(buf: np.ndarray, shape, n_valid: int, n_occ: int) -> dict:
         bp_cell=arr["bp_cell"][:np_].astype(np.int64),
         bp_dn=arr["bp_dn"][:np_].view(np.uint32).astype(np.int64),
         pix_pair0=arr["pix_pair0"].astype(np.int64),
+        share_item0=arr["share_item0"][:n["shares"] + 1].astype(np.int64) if n["shares"] > 0
+        else np.zeros(0, dtype=np.int64),
     )
 
 
-def derive(plan: dict, shape) -> dict:
-    """The schedule of a plan, by the definitions, in numpy."""
+def snap(c: int, a: int, b: int) -> int:
+    """A share boundary c inside strip [a, b), moved to a strip end closer
+    than MIN_PIECE pairs."""
+    return a if c - a < MIN_PIECE else (b if b - c < MIN_PIECE else c)
+
+
+def strip_items(a: int, b: int, P: int, S: int) -> list:
+    """First pairs of the items of a strip with pairs [a, b): cut at the
+    (snapped) share boundaries floor(P w / S) inside it, each piece of L pairs
+    into ceil(L / ITEM_PAIRS) items at floor(i L / K) of the piece."""
+    raw = [c for c in ((P * w) // S for w in range(1, S)) if a < c < b]
+    cuts = sorted({snap(c, a, b) for c in raw} - {a, b})
+    starts = []
+    for q, e in zip([a] + cuts, cuts + [b]):
+        L = e - q
+        K = -(-L // ITEM_PAIRS)
+        starts += [q + (i * L) // K for i in range(K)]
+    return starts
+
+
+def derive(plan: dict, shape, shares: int = 1) -> dict:
+    """The schedule of a plan, by the definitions, in numpy; items cut at
+    `shares` equal shares of the pairs."""
     rd = plan["ranks_depth"].astype(np.int64)
     rb = plan["ranks_bev"].astype(np.int64)
     H, W, D = shape["H"], shape["W"], shape["D"]
@@ -99,16 +127,14 @@ def derive(plan: dict, shape) -> dict:
     p_rb, p_row, p_strip, p_lp, p_rd0 = rb[hp], row[hp], strip[hp], lp[hp], rd[hp]
     p_d0 = (p_rd0 % per_view) // hw
     npairs = hp.size
-    # items: a strip of P pairs -> K = ceil(P / ITEM_PAIRS) items at floor(j * P / K)
+    # items: strips cut at the shares, pieces cut into at most ITEM_PAIRS
     s_head = np.r_[True, p_strip[1:] != p_strip[:-1]]
     s_p0 = np.r_[np.flatnonzero(s_head), npairs]
     item_strip, item_pair0 = [], []
     for j in range(s_p0.size - 1):
-        P = int(s_p0[j + 1] - s_p0[j])
-        K = -(-P // ITEM_PAIRS)
-        for i in range(K):
-            item_strip.append(int(p_strip[s_p0[j]]))
-            item_pair0.append(int(s_p0[j]) + (i * P) // K)
+        st = strip_items(int(s_p0[j]), int(s_p0[j + 1]), int(npairs), shares)
+        item_strip += [int(p_strip[s_p0[j]])] * len(st)
+        item_pair0 += st
     item_start = np.zeros(npairs, dtype=bool)
     item_start[item_pair0] = True
     seg_head = item_start.copy()
@@ -143,12 +169,21 @@ def derive(plan: dict, shape) -> dict:
     n_rows = shape["B"] * shape["N"] * H * W
     pix_pair0 = np.searchsorted(p_row[po], np.arange(n_rows + 1), side="left")
     n_items = len(item_pair0)
+    def bound(w):
+        c = (npairs * w) // shares
+        if 0 < c < npairs:
+            j = int(np.searchsorted(s_p0, c, side="right")) - 1
+            c = snap(c, int(s_p0[j]), int(s_p0[j + 1]))
+        return c
+    bounds = [bound(w) for w in range(shares + 1)]
+    share_item0 = np.searchsorted(np.array(item_pair0, dtype=np.int64), bounds, side="left")
+    shares_ok = int(np.diff(share_item0).max() <= SHARE_ITEMS)
     return dict(
         n=dict(pairs=int(npairs), items=n_items, segs=int(nsegs), valid=n, occ=int(run_head.sum()),
                occ_found=int(run_head.sum()), empty=int(empty.size), slots=int(shared.sum()),
-               comb=int(comb.sum()), strips=int(s_p0.size - 1)),
+               comb=int(comb.sum()), strips=int(s_p0.size - 1), shares=shares, shares_ok=shares_ok),
         pair_rd0=p_rd0, pair_ln=pair_ln, pair_seg=pair_seg, item_strip=np.array(item_strip, dtype=np.int64),
         item_pair0=np.r_[np.array(item_pair0, dtype=np.int64), npairs],
         item_seg0=np.r_[item_seg0, nsegs].astype(np.int64), seg_dest=seg_dest,
         comb_cell=comb_cell, comb_slot0=comb_slot0, empty=empty,
-        bp_cell=bp_cell, bp_dn=bp_dn, pix_pair0=pix_pair0)
+        bp_cell=bp_cell, bp_dn=bp_dn, pix_pair0=pix_pair0, share_item0=share_item0.astype(np.int64))

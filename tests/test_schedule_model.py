@@ -74,9 +74,9 @@ def _execute(sch, depth, feat, shape):
     return out, writes
 
 
-def _check(depth, feat, coor, shape, label):
+def _check(depth, feat, coor, shape, label, shares=1):
     plan = oracle.prepare_ref(coor, shape)
-    sch = _sched.derive(plan, shape)
+    sch = _sched.derive(plan, shape, shares=shares)
     out, writes = _execute(sch, depth, feat, shape)
     assert (writes == 1).all(), f"{label}: rows written {np.bincount(writes)} times"
     ref, mag = oracle.forward_ref(depth, feat, coor, shape)
@@ -86,17 +86,19 @@ def _check(depth, feat, coor, shape, label):
     return sch
 
 
-def test_schedule_model_tiny():
+@pytest.mark.parametrize("shares", [1, 256])
+def test_schedule_model_tiny(shares):
     cfg = CONFIGS["tiny"]
     data = draw_inputs(cfg, with_grad=False)
-    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "tiny")
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "tiny", shares)
     assert sch["n"]["slots"] == 0 or sch["n"]["comb"] > 0
 
 
-def test_schedule_model_bevdet_geometry():
+@pytest.mark.parametrize("shares", [1, 256])
+def test_schedule_model_bevdet_geometry(shares):
     cfg = CONFIGS["bevdet"]
     data = draw_inputs(cfg, with_grad=False)
-    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "bevdet")
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "bevdet", shares)
     # pixel columns see few cells: far fewer segments than pairs
     assert sch["n"]["segs"] < 0.25 * sch["n"]["pairs"]
 
@@ -107,10 +109,53 @@ def test_schedule_model_bevdet_geometry():
     dict(B=1, N=2, D=3, H=30, W=40, C=300, X=64, Y=64, Z=1),  # one-pixel-wide strips
     dict(B=3, N=1, D=4, H=5, W=6, C=16, X=300, Y=7, Z=3),
 ])
-def test_schedule_model_random(shape):
+@pytest.mark.parametrize("shares", [1, 8, 1000])
+def test_schedule_model_random(shape, shares):
     rng = np.random.default_rng(shape["C"])
     data = draw_small(rng, shape)
-    _check(data["depth"], data["feat"], random_coor(rng, shape, p_out=0.3), shape, str(shape))
+    _check(data["depth"], data["feat"], random_coor(rng, shape, p_out=0.3), shape, str(shape), shares)
+
+
+@pytest.mark.parametrize("shares", [1, 3, 8, 64, 5000])
+def test_shares_cut_items(shares):
+    # every share boundary starts an item, so share w's items hold exactly its
+    # pairs [floor(P w / S), floor(P (w + 1) / S)); items stay inside one strip
+    # and hold at most ITEM_PAIRS pairs
+    cfg = CONFIGS["bevdet"]
+    plan = oracle.prepare_ref(frustum_coor(cfg), cfg.shape())
+    sch = _sched.derive(plan, cfg.shape(), shares=shares)
+    P = sch["n"]["pairs"]
+    ip0 = sch["item_pair0"]
+    si = sch["share_item0"]
+    assert si.size == shares + 1 and si[0] == 0 and si[-1] == sch["n"]["items"]
+    s_p0 = np.r_[ip0[:-1][np.r_[True, sch["item_strip"][1:] != sch["item_strip"][:-1]]], P]
+    def bound(w):  # floor(P w / S), moved to a strip end closer than MIN_PIECE
+        c = (P * w) // shares
+        if 0 < c < P:
+            j = np.searchsorted(s_p0, c, side="right") - 1
+            a, b = s_p0[j], s_p0[j + 1]
+            c = a if c - a < _sched.MIN_PIECE else (b if b - c < _sched.MIN_PIECE else c)
+        return c
+    for w in range(shares):
+        lo, hi = bound(w), bound(w + 1)
+        assert lo <= hi
+        if lo < hi:
+            assert ip0[si[w]] == lo and ip0[si[w + 1]] == hi
+        else:
+            assert si[w] == si[w + 1]
+        assert hi - lo <= P // shares + 1 + 2 * _sched.MIN_PIECE
+    # a share cut inside a strip leaves at least MIN_PIECE pairs on each side
+    for w in range(1, shares):
+        c = bound(w)
+        j = np.searchsorted(s_p0, c, side="right") - 1
+        assert c == s_p0[j] or min(c - s_p0[j], s_p0[j + 1] - c) >= _sched.MIN_PIECE
+    assert np.all(np.diff(ip0) >= 1) and np.all(np.diff(ip0) <= _sched.ITEM_PAIRS)
+    # every strip starts an item
+    strip_p0 = ip0[:-1][np.r_[True, sch["item_strip"][1:] != sch["item_strip"][:-1]]]
+    base = _sched.derive(plan, cfg.shape(), shares=1)
+    assert np.array_equal(strip_p0, base["item_pair0"][:-1][np.r_[True, base["item_strip"][1:] !=
+                                                                   base["item_strip"][:-1]]])
+    assert sch["n"]["shares_ok"] == int(np.diff(si).max() <= _sched.SHARE_ITEMS)
 
 
 def test_schedule_model_one_cell():
