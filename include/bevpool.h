@@ -161,9 +161,13 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
  * (the frustum points of a pixel column lie in one vertical plane, so a
  * strip's points fall into few BEV cells).  Within a strip, kept points of one
  * pixel in one cell over consecutive depth bins form a pair: their depth
- * scores are summed first and the pixel's feature row is read once.  A
- * strip's pairs are cut into items of at most a few thousand pairs, and an
- * item's pairs into segments (one per cell).  A cell covered by one segment
+ * scores are summed first and the pixel's feature row is read once.  The
+ * pairs are cut into equal shares, one per workgroup of the scheduled forward
+ * on the device the schedule is built on (its compute units); a strip's pairs
+ * are cut at those shares and into items of at most a few thousand pairs, and
+ * an item's pairs into segments (one per cell).  A schedule built on one
+ * device gives the same results on another; only the balance of the work
+ * over the workgroups depends on the device.  A cell covered by one segment
  * is written directly; a cell covered by several has one partial-sum slot per
  * segment in the forward's workspace, added in a fixed order.
  *
