@@ -11,8 +11,9 @@ The metric is the forward latency.  It is measured separately from the steps,
 cold: the forward is launched over R rotating buffer sets (depth, feature,
 plan, output) whose total size is several times the 256 MB Infinity Cache, so
 every launch reads its inputs from HBM.  Each launch is bracketed by HIP
-events on the stream it runs on.  The achieved bandwidth divides the
-algorithmic bytes of one forward by that latency.  --forward picks the entry
+events on the stream it runs on; the latency is the median over the
+launches (mean and percentiles are reported beside it).  The achieved
+bandwidth divides the algorithmic bytes of one forward by that latency.  --forward picks the entry
 point timed as the metric (interval-table or strip-schedule forward); the
 other one is timed the same way and reported beside it.
 
@@ -261,13 +262,15 @@ def main():
     cold_oth, cold_oth_region = timed_forwards(args.fwd_launches, lambda i: sets[i % len(sets)],
                                                paths[other_name])
     log(f"{args.forward} forward back-to-back region: cold {cold_region * 1e3:.2f} us/launch, warm "
-        f"{warm_region * 1e3:.2f}; {other_name} forward cold {cold_oth.mean() * 1e3:.2f} us "
+        f"{warm_region * 1e3:.2f}; {other_name} forward cold median {np.median(cold_oth) * 1e3:.2f} us "
         f"(region {cold_oth_region * 1e3:.2f})")
-    fwd_ms = float(cold.mean())
+    # the median per launch (a rare host stall before a launch lands in its
+    # events and would move a mean)
+    fwd_ms = float(np.median(cold))
     min_bytes = forward_min_bytes(cfg, nv, ni)
     achieved = min_bytes / (fwd_ms * 1e-3) / 1e9
-    log(f"forward cold mean {fwd_ms * 1e3:.2f} us (p10 {np.percentile(cold, 10) * 1e3:.2f}, p50 "
-        f"{np.median(cold) * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
+    log(f"forward cold median {fwd_ms * 1e3:.2f} us (p10 {np.percentile(cold, 10) * 1e3:.2f}, mean "
+        f"{cold.mean() * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
         f"{warm.mean() * 1e3:.2f} us; {min_bytes / 1e6:.2f} MB -> {achieved:.0f} GB/s")
 
     traffic = None
@@ -332,8 +335,8 @@ def main():
                      "algorithmic_bytes": min_bytes, "kernel": FORWARD_KERNELS[args.forward]},
         "cpu_baseline": cpu,
         "detail": {
-            "forward_cold_ms": {"mean": fwd_ms, "p10": float(np.percentile(cold, 10)),
-                                "p50": float(np.median(cold)), "p90": float(np.percentile(cold, 90)),
+            "forward_cold_ms": {"mean": float(cold.mean()), "p10": float(np.percentile(cold, 10)),
+                                "p50": fwd_ms, "p90": float(np.percentile(cold, 90)),
                                 "launches": int(cold.size), "rotating_sets": len(sets),
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
             "forward_cold_region_ms_per_launch": cold_region,
@@ -342,7 +345,8 @@ def main():
             "forward_warm_region_ms_per_launch": warm_region,
             "forward_path": args.forward,
             "backward_path": args.backward,
-            f"forward_{other_name}_cold_ms": float(cold_oth.mean()),
+            f"forward_{other_name}_cold_ms": {"p50": float(np.median(cold_oth)),
+                                              "mean": float(cold_oth.mean())},
             f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
             "prepare_plus_forward_ms": prep_ms + fwd_in_step_ms, "step_wall_ms": wall_ms,
