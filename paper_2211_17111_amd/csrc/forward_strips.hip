@@ -55,6 +55,7 @@ constexpr int kPairBatch = 8;   // pair records per loading thread in flight
 constexpr int kBufBytes = kStripBytes + kItemPairs * 12;  // rows | pair records | destinations
 constexpr int kHdrCache = 128;  // item headers of a workgroup kept in LDS
 constexpr int kCombThreads = 256;
+static_assert(kStripBytes % (16 * kLoadThreads) == 0, "row vectors split evenly over the loading threads");
 static_assert(kItemPairs % kNT == 0 && kItemPairs % kLoadThreads == 0,
               "pair records split evenly over the loading threads");
 static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
@@ -366,6 +367,86 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     }
   };
 
+  // ---- the loading waves' item loads, with the item's pair records (depth
+  // rank, pixel and run) read one item ahead into registers (fetch_pairs):
+  // the depth gathers, which need them, then go out first, beside the row
+  // loads, and the LDS stores follow.
+  constexpr int kLPL = kItemPairs / kLoadThreads;  // pairs per loading thread
+  constexpr int kRowsL = kStripBytes / 16 / kLoadThreads;  // row vectors per loading thread
+  constexpr int kRowsH = kRowsL / 2;  // row vectors per batch
+  static_assert(kRowsL % 2 == 0, "two row batches");
+  struct PairPf {
+    int32_t rd0[kLPL];
+    uint32_t ln[kLPL];
+  };
+  auto fetch_pairs = [&](const ItemHdr& h, PairPf& pf) {
+#pragma unroll
+    for (int q = 0; q < kLPL; ++q) {
+      const int k = h.p0 + min(q * kLoadThreads + lt, max(h.np - 1, 0));
+      pf.rd0[q] = a.pair_rd0[k];
+      pf.ln[q] = a.pair_ln[k];
+    }
+  };
+  auto load_item_pf = [&](const ItemHdr& h, int b, const PairPf& pf) {
+    const Geo g = geometry(h.strip);
+    const int nvec = g.npix * rowvec;
+    RawT* const s_rows = buf_rows(b);
+    PairRec* const s_pr = buf_pr(b);
+    int32_t* const s_dest = buf_dest(b);
+    float dv[kLPL][kDepthBurst];
+#pragma unroll
+    for (int q = 0; q < kLPL; ++q) {
+      const int n = q * kLoadThreads + lt < h.np ? (int)(pf.ln[q] >> 16) : 0;
+#pragma unroll
+      for (int j = 0; j < kDepthBurst; ++j) {
+        const int64_t p = (int64_t)pf.rd0[q] + j * hw;
+        float v = 0.f;
+        if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
+        dv[q][j] = v;
+      }
+    }
+    uint32_t sg[kLPL];
+#pragma unroll
+    for (int q = 0; q < kLPL; ++q) sg[q] = a.pair_seg[h.p0 + min(q * kLoadThreads + lt, max(h.np - 1, 0))];
+#pragma unroll
+    for (int r0 = 0; r0 < kRowsL; r0 += kRowsH) {
+      RawT rv[kRowsH];
+#pragma unroll
+      for (int u = 0; u < kRowsH; ++u) rv[u] = *vec_addr(g, min((r0 + u) * kLoadThreads + lt, nvec - 1));
+#pragma unroll
+      for (int u = 0; u < kRowsH; ++u) {
+        const int idx = (r0 + u) * kLoadThreads + lt;
+        if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
+      }
+    }
+    for (int idx = kRowsL * kLoadThreads + lt; idx < nvec; idx += kLoadThreads)
+      s_rows[vec_slot(idx)] = *vec_addr(g, idx);
+    for (int j = lt; j < h.nseg; j += kLoadThreads) s_dest[j] = a.seg_dest[h.g0 + j];
+#pragma unroll
+    for (int q = 0; q < kLPL; ++q) {
+      const int k = q * kLoadThreads + lt;
+      if (k < h.np) {
+        const int n = (int)(pf.ln[q] >> 16);
+        // (no constant start: an add of 0.f would be folded into the load's branch)
+        float sum = dv[q][0];
+#pragma unroll
+        for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
+        for (int j = kDepthBurst; j < n; ++j) {
+          const int64_t p = (int64_t)pf.rd0[q] + j * hw;
+          if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+        }
+        const uint32_t lp = pf.ln[q] & kPairPixel;
+        const bool ok = lp < (uint32_t)g.npix;
+        const uint32_t sgc = min(sg[q], (uint32_t)(h.nseg - 1));
+        PairRec rec;
+        rec.w = ok ? sum : 0.f;
+        rec.ps = (ok ? lp * (uint32_t)rowvec : 0u) | (sgc << kRecSegShift) |
+                 ((pf.ln[q] & kPairHead) ? kRecHead : 0u);
+        s_pr[k] = rec;
+      }
+    }
+  };
+
   // ---- walking waves: lane group lg of walking wave wv owns an equal range
   // of each item's pairs
   const int gpw = kWave / cvc;
@@ -559,7 +640,11 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // ---- the pipeline: item i is walked from buffer b while the loading
   // waves add up the cut segments of item i - 1 (published in buffer b ^ 1)
   // and then fill buffer b ^ 1 with item i + 1
+  // (records are read ahead where the walk leaves the registers for them)
+  constexpr bool kPrefetch = VEC < 8;
   load_item(header(i_begin), 0, std::integral_constant<int, kNT>{});
+  PairPf pf;  // the second item's records
+  if (kPrefetch && !walker && i_begin + 1 < i_begin + n_my) fetch_pairs(header(i_begin + 1), pf);
   lds_barrier();
   int b = 0;
   for (int i = i_begin; i < i_begin + n_my; ++i) {
@@ -568,7 +653,12 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         combine_parts(b ^ 1, kLoadThreads);
         loader_sync();  // every part read before buffer b ^ 1 is refilled
       }
-      if (i + 1 < i_begin + n_my) load_item(header(i + 1), b ^ 1, std::integral_constant<int, kLoadThreads>{});
+      if (kPrefetch) {
+        if (i + 1 < i_begin + n_my) load_item_pf(header(i + 1), b ^ 1, pf);
+        if (i + 2 < i_begin + n_my) fetch_pairs(header(i + 2), pf);
+      } else if (i + 1 < i_begin + n_my) {
+        load_item(header(i + 1), b ^ 1, std::integral_constant<int, kLoadThreads>{});
+      }
     } else {
       walk_item(header(i), b);
     }
