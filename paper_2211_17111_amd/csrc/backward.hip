@@ -470,6 +470,10 @@ hipError_t launch_backward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.cells = d.cells;
   const bool al = aligned16(grad_out) && aligned16(feat) && aligned16(grad_feat);
   if (f32) {
+    // 8 channels per lane where C allows: smaller lane groups, so more pixels
+    // (and their independent load chains) per wave
+    if (al && d.C % 8 == 0)
+      return run_pixels_nv<float, float, 8>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
     if (al && d.C % 4 == 0)
       return run_pixels_nv<float, float, 4>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
     return run_pixels_nv<float, float, 1>(d, grad_out, depth, feat, a, grad_depth, grad_feat, stream);
