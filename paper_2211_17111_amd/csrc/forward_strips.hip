@@ -591,13 +591,13 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     if (lg >= gpw) return;
     const int n_h = (nthreads / kWave) * gpw;
     for (int gg = wave * gpw + lg; gg < G; gg += n_h) {
+      // the range's record and part and the following ranges' records and
+      // parts, kChain at a time, are read together (whether or not the
+      // range holds a cut segment; past the chain's end they are not used)
+      constexpr int kChain = 4;
       const int4 m = s_meta[gg];
-      if (!(m.z & kMetaLast)) continue;
       float sum[VEC];
       Vec<float, VEC>::load(part_last(b) + ((int64_t)gg * cvc + vi) * VEC, sum);
-      // the following ranges kChain at a time: their records and parts are
-      // read together (past the chain's end they are read and not used)
-      constexpr int kChain = 4;
       bool go = true;
       for (int g2 = gg + 1; go && g2 < G; g2 += kChain) {
         int4 m2[kChain];
@@ -608,6 +608,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           m2[u] = s_meta[gi];
           Vec<float, VEC>::load(part_first(b) + ((int64_t)gi * cvc + vi) * VEC, t[u]);
         }
+        if (!(m.z & kMetaLast)) break;
 #pragma unroll
         for (int u = 0; u < kChain; ++u) {
           if (!go || g2 + u >= G || (m2[u].z & kMetaEmpty)) continue;
@@ -621,7 +622,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           if (!(m2[u].x == m.x && (m2[u].z & kMetaNext))) go = false;
         }
       }
-      store_dest(m.y, sum);
+      if (m.z & kMetaLast) store_dest(m.y, sum);
     }
   };
 
