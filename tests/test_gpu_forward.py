@@ -295,3 +295,52 @@ def test_scheduled_matches_ranges():
     assert torch.equal(b, c)
     # both within float32 rounding of each other relative to the output scale
     assert float((a - b).abs().max()) <= 1e-4 * float(a.abs().max())
+
+
+def test_scheduled_workspace_reuse():
+    """One workspace serves a run of forwards over two plans of one shape, with
+    new inputs each time: every result equals a fresh workspace's bit for bit
+    (the workspace is scratch)."""
+    cfg = CONFIGS["bevdet"]
+    shape = cfg.shape()
+    rng = np.random.default_rng(5)
+    plans = [_gpu.run_prepare(c, shape) for c in (frustum_coor(cfg), random_coor(rng, shape, p_out=0.3))]
+    scheds = [bp.schedule(p) for p in plans]
+    n = max(bp.bevpool_forward_scheduled_workspace_size(shape, s.n_slots) for s in scheds)
+    ws = torch.full((n,), 0xFF, dtype=torch.uint8, device=_gpu.DEV)  # NaN rows before the first use
+    for t in range(4):
+        _gpu.say(f"workspace reuse: forward {t}")
+        data = draw_inputs(cfg, seed=100 + t, with_grad=False)
+        d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+        s = scheds[t % 2]
+        fresh = bp.forward_scheduled(d, f, s)
+        reused = bp.forward_scheduled(d, f, s, workspace=ws)
+        torch.cuda.synchronize()
+        assert s.n_slots > 0
+        assert torch.equal(fresh, reused), t
+
+
+def test_scheduled_small_workspace_nan():
+    """A workspace one slot short: the cell holding the last slot comes out
+    NaN and every other cell as with a full workspace."""
+    cfg = CONFIGS["bevdet"]
+    shape = cfg.shape()
+    data = draw_inputs(cfg, with_grad=False)
+    plan = _gpu.run_prepare(frustum_coor(cfg), shape)
+    sched = bp.schedule(plan)
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    full = bp.forward_scheduled(d, f, sched)
+    n = bp.bevpool_forward_scheduled_workspace_size(shape, sched.n_slots)
+    small = torch.zeros(n - 4 * shape["C"], dtype=torch.uint8, device=_gpu.DEV)
+    out = bp.forward_scheduled(d, f, sched, workspace=small)
+    torch.cuda.synchronize()
+    sch = _sched.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
+    comb, c0 = sch["comb_cell"], sch["comb_slot0"]
+    assert comb.size > 0
+    short = comb[c0[1:] > sched.n_slots - 1]  # cells whose slots the workspace lacks
+    assert short.size == 1
+    got, want = out.reshape(-1, shape["C"]).cpu(), full.reshape(-1, shape["C"]).cpu()
+    mask = torch.zeros(got.shape[0], dtype=torch.bool)
+    mask[torch.from_numpy(short)] = True
+    assert bool(torch.isnan(got[mask]).all())
+    assert torch.equal(got[~mask], want[~mask])
