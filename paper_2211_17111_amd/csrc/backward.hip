@@ -200,7 +200,7 @@ struct PixArgs {
 // memory) and the grad_out rows of neighbouring rays stay in one L2.
 // (Column-major pixel order was measured slower.)
 constexpr bool kPixXcdMap = true;
-constexpr int kPixUnrollMax = 8;
+constexpr int kPixUnrollMax = 4;
 
 // grad_out rows in flight per group: up to kPixUnrollMax, within 64 registers
 // of row data (always a power of two)
