@@ -281,7 +281,8 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
       const int32_t c = a.bp_cell[pb + vi];
       const uint32_t dn = a.bp_dn[pb + vi];
       const int32_t d0 = (int32_t)(dn & 0xffffu), n = (int32_t)(dn >> 16);
-      if (c >= 0 && c < a.cells && n >= 1 && d0 + n <= a.D) {
+      // (bitwise: a short-circuit test of c first would delay the load of dn)
+      if ((c >= 0) & (c < a.cells) & (n >= 1) & (d0 + n <= a.D)) {
         my_cell = c;
         my_dn = dn;
         // the first kDepthBurst scores loaded together, the rest (rare) after
