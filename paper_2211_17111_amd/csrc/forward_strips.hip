@@ -11,18 +11,21 @@
 // reads its row from LDS, and only the cells a strip shares with its
 // neighbours need a second pass.
 //
-//   k_fwd_strips   one workgroup per (item, channel chunk of up to 64 vectors):
-//     1. copies the strip's feature rows (this chunk) into LDS with 16-byte
-//        loads; meanwhile loads the item's pair records and gathers their
-//        depth scores; each pair's weight (the sum of its points' scores),
-//        local pixel and segment go to LDS;
-//     2. cuts the item's pairs into equal ranges, one per lane group (one lane
-//        per vector of the chunk); each group sums weight x feature row over
-//        its range, reading both from LDS, and finishes a segment when the
-//        next pair belongs to another;
-//     3. a segment cut by range boundaries is added up in range order from
-//        partial sums left in LDS.  Each segment's sum is stored once: into
-//        `out` when the segment alone covers its cell, else into its slot.
+//   k_fwd_strips   one persistent workgroup per compute unit and channel
+//                  chunk (up to 64 vectors), taking one share of the items
+//                  (a contiguous run of strips) and two LDS item buffers:
+//     1. loading waves fill one buffer with the next item: the strip's feature
+//        rows (this chunk, 16-byte loads), the item's pair records, each
+//        pair's weight (the sum of its points' depth scores, gathered) and
+//        the segment destinations;
+//     2. meanwhile walking waves sum the current item from the other buffer:
+//        its pairs are cut into equal ranges, one per lane group (one lane per
+//        vector of the chunk); each group sums weight x feature row over its
+//        range, reading both from LDS, and stores each segment it holds whole;
+//     3. a segment cut by range boundaries is added up in range order by the
+//        loading waves from partial sums the walkers leave in the walked
+//        buffer.  Each segment's sum is stored once: into `out` when the
+//        segment alone covers its cell, else into its slot.
 //   k_fwd_combine  one lane group per cell covered by several segments (adds
 //                  its slots in segment order and stores the cell) or per
 //                  empty cell (stores zeros).
@@ -149,6 +152,13 @@ __device__ __forceinline__ void lane_row(const typename Raw<TIn, VEC>::type* p, 
   constexpr int kPer = VEC / kNV;
 #pragma unroll
   for (int h = 0; h < kNV; ++h) raw_to_float<TIn, VEC>(p[h * cvc], v + h * kPer);
+}
+
+// The largest batch of at most m loads that divides n loads.
+constexpr int whole_batch(int n, int m) {
+  int b = n < m ? n : m;
+  while (b > 1 && n % b != 0) --b;
+  return b > 0 ? b : 1;
 }
 
 // An item's header, the same for the whole workgroup.
@@ -293,9 +303,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   auto load_item = [&](const ItemHdr& h, int b, auto nt_tag) {
     constexpr int NT = decltype(nt_tag)::value;
     constexpr int kLoadRows = kStripBytes / 16 / NT;  // 16-byte row vectors per thread
-    constexpr int kRB = kLoadRows < kRowBatch ? kLoadRows : kRowBatch;
+    constexpr int kRB = whole_batch(kLoadRows, kRowBatch);
     constexpr int kLP = kItemPairs / NT;  // pairs per thread
-    constexpr int kPB = kLP < kPairBatch ? kLP : kPairBatch;
+    constexpr int kPB = whole_batch(kLP, kPairBatch);
     static_assert(kLoadRows % kRB == 0 && kLP % kPB == 0, "whole batches");
     const Geo g = geometry(h.strip);
     const int nvec = g.npix * rowvec;
