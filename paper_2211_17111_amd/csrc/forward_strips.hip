@@ -699,10 +699,19 @@ __global__ __launch_bounds__(kCombThreads) void k_fwd_combine(TOut* __restrict__
   const int64_t n_comb = min(hdr[kHdrComb], a.n_occ);
   const int64_t n_empty = min<int64_t>(hdr[kHdrEmpty], a.n_empty);
   const int64_t col = (int64_t)(cbase + vi) * VEC;
+  if (j >= n_comb + n_empty) return;
+  // Both roles' records are read at once, unconditionally (clamped index),
+  // so that a cell and its slot range arrive together: a load behind a test
+  // of the cell would cost another round trip.
+  const int64_t jc = min(j, n_comb > 0 ? n_comb - 1 : 0);
+  const int64_t cell_c = a.comb_cell[jc];
+  const int64_t s0 = a.comb_slot0[jc], s1 = a.comb_slot0[jc + 1];
+  const int64_t cell_e = a.empty[min(max(j - n_comb, (int64_t)0), n_empty > 0 ? n_empty - 1 : 0)];
+  // (an empty asm reading all four values: the compiler would otherwise move
+  // each load into the branch that uses it, behind the previous one's test)
+  asm volatile("" ::"v"((int32_t)cell_c), "v"((int32_t)s0), "v"((int32_t)s1), "v"((int32_t)cell_e));
   if (j < n_comb) {
-    const int64_t cell = a.comb_cell[j];
-    const int64_t s0 = a.comb_slot0[j], s1 = a.comb_slot0[j + 1];
-    if (cell < 0 || cell >= a.cells) return;
+    if (cell_c < 0 || cell_c >= a.cells) return;
     float sum[VEC];
 #pragma unroll
     for (int e = 0; e < VEC; ++e) sum[e] = 0.f;
@@ -721,17 +730,24 @@ __global__ __launch_bounds__(kCombThreads) void k_fwd_combine(TOut* __restrict__
 #pragma unroll
           for (int e = 0; e < VEC; ++e) sum[e] += t[k][e];
       }
-      for (; s < s1; ++s) {
-        float t[VEC];
-        Vec<float, VEC>::load(a.slots + s * C + col, t);
+      // the last 1-3 slots (most cells have 2 or 3), loaded together
+      const int rest = (int)(s1 - s);
+      float t[3][VEC];
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) sum[e] += t[e];
+      for (int k = 0; k < 3; ++k) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) t[k][e] = 0.f;
+        if (k < rest) Vec<float, VEC>::load(a.slots + (s + k) * C + col, t[k]);
       }
+#pragma unroll
+      for (int k = 0; k < 3; ++k)
+        if (k < rest)
+#pragma unroll
+          for (int e = 0; e < VEC; ++e) sum[e] += t[k][e];
     }
-    Vec<TOut, VEC>::store(out + cell * C + col, sum);
-  } else if (j - n_comb < n_empty) {
-    const int64_t cell = a.empty[j - n_comb];
-    if (cell >= 0 && cell < a.cells) store_zero<TOut, VEC>(out + cell * C + col);
+    Vec<TOut, VEC>::store(out + cell_c * C + col, sum);
+  } else if (cell_e >= 0 && cell_e < a.cells) {
+    store_zero<TOut, VEC>(out + cell_e * C + col);
   }
 }
 
