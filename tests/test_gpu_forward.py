@@ -297,6 +297,30 @@ def test_scheduled_matches_ranges():
     assert float((a - b).abs().max()) <= 1e-4 * float(a.abs().max())
 
 
+@pytest.mark.parametrize("name", ["bevdet", "headline"])
+def test_scheduled_without_shares(name):
+    """A schedule whose items were not cut for this launch's workgroups (here:
+    its header says a share is too long) is walked with an equal count of
+    each die's items instead; only the balance changes, so the result is the
+    same bit for bit."""
+    import copy
+    cfg = CONFIGS[name]
+    _gpu.say(f"forward without shares: {name}")
+    data = draw_inputs(cfg, with_grad=False)
+    plan = _gpu.run_prepare(frustum_coor(cfg), cfg.shape())
+    sched = bp.schedule(plan)
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    want = bp.forward_scheduled(d, f, sched)
+    other = copy.copy(sched)
+    other.buffer = sched.buffer.clone()
+    hdr = other.buffer[:64].view(torch.int32)
+    assert int(hdr[_sched.HDR["shares_ok"]]) == 1
+    hdr[_sched.HDR["shares_ok"]] = 0
+    got = bp.forward_scheduled(d, f, other)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
+
+
 def test_scheduled_workspace_reuse():
     """One workspace serves a run of forwards over two plans of one shape, with
     new inputs each time: every result equals a fresh workspace's bit for bit
