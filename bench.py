@@ -13,9 +13,11 @@ plan, output) whose total size is several times the 256 MB Infinity Cache, so
 every launch reads its inputs from HBM.  Each launch is bracketed by HIP
 events on the stream it runs on; the latency is the median over the
 launches (mean and percentiles are reported beside it).  The achieved
-bandwidth divides the algorithmic bytes of one forward by that latency.  --forward picks the entry
-point timed as the metric (interval-table or strip-schedule forward); the
-other one is timed the same way and reported beside it.
+bandwidth divides the algorithmic bytes of one forward by that latency.
+--forward picks the entry point timed as the metric (interval-table or
+strip-schedule forward); the other one is timed the same way and reported
+beside it.  So is a plain device copy that reads and writes the same number
+of bytes: the bandwidth one launch of this size reaches at best.
 
 The CPU baseline is the float64 oracle timed on the host: whole forwards of
 the same workload, repeated until a minimum CPU time is spent, reported as the
@@ -273,6 +275,21 @@ def main():
         f"{cold.mean() * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
         f"{warm.mean() * 1e3:.2f} us; {min_bytes / 1e6:.2f} MB -> {achieved:.0f} GB/s")
 
+    # ---- the achievable ceiling at this size: a plain device copy (torch's
+    # copy kernel) that reads and writes the forward's algorithmic bytes, timed
+    # the same way (cold: as many buffer pairs as sets, cycled)
+    half = (min_bytes // 2 + 255) // 256 * 256
+    pairs = [(torch.empty(half, dtype=torch.uint8, device=dev), torch.empty(half, dtype=torch.uint8, device=dev))
+             for _ in range(len(sets))]
+    copy_cold, _ = timed_forwards(args.fwd_launches, lambda i: pairs[i % len(pairs)],
+                                  lambda pr: pr[1].copy_(pr[0]))
+    host_us.pop()  # (the copy's enqueue time is not the forward's)
+    copy_ms = float(np.median(copy_cold))
+    copy_gbs = 2 * half / (copy_ms * 1e-3) / 1e9
+    del pairs
+    log(f"copy of the same bytes ({2 * half / 1e6:.2f} MB read + written), cold median "
+        f"{copy_ms * 1e3:.2f} us -> {copy_gbs:.0f} GB/s ({copy_gbs / HBM_PEAK_GBS * 100:.1f}% of peak)")
+
     traffic = None
     if os.path.exists(PMC_FILE):
         # the summary's figures sit on its one line that holds a JSON object
@@ -340,6 +357,8 @@ def main():
                                 "launches": int(cold.size), "rotating_sets": len(sets),
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
             "forward_cold_region_ms_per_launch": cold_region,
+            "copy_same_bytes_cold": {"p50_ms": copy_ms, "gbs": round(copy_gbs, 1), "bytes": 2 * half,
+                                     "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4)},
             "forward_warm_ms": float(warm.mean()),
             "forward_host_enqueue_us": host_us,
             "forward_warm_region_ms_per_launch": warm_region,
