@@ -200,12 +200,14 @@ struct PixArgs {
 // memory) and the grad_out rows of neighbouring rays stay in one L2.
 // (Column-major pixel order was measured slower.)
 constexpr bool kPixXcdMap = true;
-constexpr int kPixUnrollMax = 4;
-
-// grad_out rows in flight per group: up to kPixUnrollMax, within 64 registers
-// of row data (always a power of two)
-constexpr int pix_unroll(int vec, int nv) {
-  return vec * nv >= 64 ? 1 : (64 / (vec * nv) < kPixUnrollMax ? 64 / (vec * nv) : kPixUnrollMax);
+// grad_out rows in flight per group: up to umax, within 64 registers of row
+// data (always a power of two).  umax is 4 when the launch has waves enough
+// to fill every SIMD several times over (kPixManyWaves per CU): then the
+// extra waves that fewer registers allow hide the load latency better than
+// longer steps; else 8.
+constexpr int kPixManyWaves = 8;
+constexpr int pix_unroll(int vec, int nv, int umax) {
+  return vec * nv >= 64 ? 1 : (64 / (vec * nv) < umax ? 64 / (vec * nv) : umax);
 }
 constexpr int kDepthBurst = 2;  // depth scores of a pair loaded before any is summed
 
@@ -238,12 +240,12 @@ struct ReduceScatter {
   }
 };
 
-template <typename TIn, typename TG, int VEC, int NV, int GS>
+template <typename TIn, typename TG, int VEC, int NV, int GS, int UMAX>
 __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
     const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
     TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a) {
   constexpr int G = kWave / GS;
-  constexpr int U = pix_unroll(VEC, NV);
+  constexpr int U = pix_unroll(VEC, NV, UMAX);
   constexpr int M = U > GS ? U / GS : 1;  // pair totals a lane holds after the reduction
   constexpr int LPU = GS * M / U;         // lanes holding the same pair totals
   const int lane = lane_id();
@@ -368,9 +370,16 @@ hipError_t run_pixels(const Dims& d, const void* grad_out, const void* depth, co
   PixArgs b = a;
   b.blocks = (int32_t)((d.rows + pix_per_block - 1) / pix_per_block);
   const int64_t nb = kPixXcdMap ? (b.blocks + kXcds - 1) / kXcds * kXcds : b.blocks;
-  k_bwd_pixels<TIn, TG, VEC, NV, GS><<<dim3((unsigned)nb), dim3(kBwdThreads), 0, stream>>>(
-      static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
-      static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat), b);
+  const bool many = (d.rows + G - 1) / G >= (int64_t)kPixManyWaves * device_cus();
+  auto launch = [&](auto kern) {
+    kern<<<dim3((unsigned)nb), dim3(kBwdThreads), 0, stream>>>(
+        static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
+        static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat), b);
+  };
+  if (many)
+    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 4>);
+  else
+    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 8>);
   return hipGetLastError();
 }
 
