@@ -28,9 +28,12 @@ constexpr int kMaxBuckets = 1 << kMaxDigitBits;
 // ------------------------------------------------------------------ scan
 // In-place exclusive scan of int32 data in three launches.
 
+// Each block scans its tile and leaves the tile's total in sums; a scan of
+// one tile also writes the total to total_out (if given), with no second pass.
 __global__ __launch_bounds__(kScanThreads) void k_scan_local(int32_t* __restrict__ data,
                                                              int64_t n,
-                                                             int32_t* __restrict__ sums) {
+                                                             int32_t* __restrict__ sums,
+                                                             int32_t* __restrict__ total_out) {
   __shared__ int lds[kScanThreads / kWave];
   const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
   int v[kScanItems];
@@ -49,7 +52,10 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_local(int32_t* __restrict
     if (i < n) data[i] = off;
     off += v[k];
   }
-  if (threadIdx.x == 0) sums[blockIdx.x] = total;
+  if (threadIdx.x == 0) {
+    sums[blockIdx.x] = total;
+    if (gridDim.x == 1 && total_out != nullptr) *total_out = total;
+  }
 }
 
 __global__ __launch_bounds__(kScanThreads) void k_scan_top(int32_t* __restrict__ sums, int64_t nb,
@@ -92,9 +98,15 @@ __global__ __launch_bounds__(kScanThreads) void k_scan_add(int32_t* __restrict__
 void scan_exclusive(int32_t* data, int64_t n, int32_t* sums, int32_t* total_out,
                     hipStream_t stream) {
   const int64_t nb = (n + kScanTile - 1) / kScanTile;
-  k_scan_local<<<dim3((unsigned)nb), dim3(kScanThreads), 0, stream>>>(data, n, sums);
-  k_scan_top<<<dim3(1), dim3(kScanThreads), 0, stream>>>(sums, nb, total_out);
-  if (nb > 1) k_scan_add<<<dim3((unsigned)nb), dim3(kScanThreads), 0, stream>>>(data, n, sums);
+  if (nb == 0) {  // (an empty input: only its zero total)
+    k_scan_top<<<dim3(1), dim3(kScanThreads), 0, stream>>>(sums, 0, total_out);
+    return;
+  }
+  k_scan_local<<<dim3((unsigned)nb), dim3(kScanThreads), 0, stream>>>(data, n, sums, total_out);
+  if (nb > 1) {
+    k_scan_top<<<dim3(1), dim3(kScanThreads), 0, stream>>>(sums, nb, total_out);
+    k_scan_add<<<dim3((unsigned)nb), dim3(kScanThreads), 0, stream>>>(data, n, sums);
+  }
 }
 
 // ------------------------------------------------------------------ filter

@@ -51,7 +51,12 @@ def test_graph_replays_match_eager():
         bp.bevpool_forward_scheduled(shape, code, code, depth, feat, sched, sb, nv, ni, out, ws_f, fb)
         bp.bevpool_backward_scheduled(shape, code, code, grad_out, depth, feat, sched, sb, nv, ni, gd, gf)
 
+    # (the plan and schedule arrays are written only up to their counts: every
+    # output is cleared before the eager run as before each replay, so that
+    # the regions nothing writes compare equal)
     outputs = (rd, rf, rb, st, ln, cnt, sched, out, gd, gf)
+    for t in outputs:
+        t.zero_()
     run()
     torch.cuda.synchronize()
     want = [t.clone() for t in outputs]
@@ -68,7 +73,7 @@ def test_graph_replays_match_eager():
         run()
     torch.cuda.synchronize()
     for k in range(3):
-        for t in outputs:  # eager work between replays: clear every output
+        for t in outputs:  # eager work between replays: clear every output again
             t.zero_()
         torch.cuda.synchronize()
         g.replay()
