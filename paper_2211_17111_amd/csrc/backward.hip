@@ -17,7 +17,9 @@
 //
 // From a schedule (bevpool_backward_scheduled), which lists every pixel's
 // pairs (a cell and a run of consecutive depth bins):
-//   1. k_zero_vec clears grad_depth (coalesced), so dropped points are 0;
+//   1. k_zero_vec clears grad_depth (coalesced), so dropped points are 0 (in
+//      a launch too small to fill the GPU, k_bwd_pixels writes those zeros
+//      itself instead, from a mask of the depth bins its pairs cover);
 //   2. k_bwd_pixels gives each pixel to a group of GS lanes holding its
 //      feature row; lane l of the group takes pair l of the current chunk
 //      and sums that pair's depth scores; the group then walks the chunk U
@@ -206,6 +208,13 @@ constexpr bool kPixXcdMap = true;
 // extra waves that fewer registers allow hide the load latency better than
 // longer steps; else 8.
 constexpr int kPixManyWaves = 8;
+// Depth bins the pixel kernel tracks itself (one bit each, in registers): for
+// D up to this, in a launch too small to fill the GPU, each pixel's lane group
+// also writes the zeros of its dropped points, so that no separate clearing
+// launch is needed (in a large launch the extra registers would cost more
+// waves than that launch saves).
+constexpr int kPixMaskWords = 4;
+constexpr int kPixMaskBits = 32 * kPixMaskWords;
 constexpr int pix_unroll(int vec, int nv, int umax) {
   return vec * nv >= 64 ? 1 : (64 / (vec * nv) < umax ? 64 / (vec * nv) : umax);
 }
@@ -240,7 +249,7 @@ struct ReduceScatter {
   }
 };
 
-template <typename TIn, typename TG, int VEC, int NV, int GS, int UMAX>
+template <typename TIn, typename TG, int VEC, int NV, int GS, int UMAX, int MW>
 __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
     const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
     TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a) {
@@ -273,6 +282,11 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
   const int32_t p_begin = max(a.pix_pair0[f], 0);
   const int32_t p_end = min(a.pix_pair0[f + 1], a.n_pairs);
   const int64_t dbase = (f / a.hw) * a.per_view + f % a.hw;  // depth rank at bin 0
+  // (MW > 0) the depth bins this pixel's pairs cover: each lane marks its own
+  // pairs' runs; the other bins are dropped points, cleared at the end
+  uint32_t kept[MW > 0 ? MW : 1];
+#pragma unroll
+  for (int w = 0; w < (MW > 0 ? MW : 1); ++w) kept[w] = 0u;
 
   for (int32_t pb = p_begin; pb < p_end; pb += GS) {
     // lane vi: pair pb + vi -- its cell, depth run and summed depth score
@@ -287,6 +301,12 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
       if ((c >= 0) & (c < a.cells) & (n >= 1) & (d0 + n <= a.D)) {
         my_cell = c;
         my_dn = dn;
+#pragma unroll
+        for (int w = 0; w < MW; ++w) {  // bins [d0, d0 + n) of word w
+          const int lo = max(d0, 32 * w), hi = min(d0 + n, 32 * w + 32);
+          const int len = hi - lo;
+          if (len > 0) kept[w] |= (len >= 32 ? ~0u : ((1u << len) - 1u)) << (lo - 32 * w);
+        }
         // the first kDepthBurst scores loaded together, the rest (rare) after
         float dq[kDepthBurst];
 #pragma unroll
@@ -355,11 +375,38 @@ __global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
       }
     }
   }
+  if (MW > 0) {
+    // the group's covered bins (an OR over its lanes), then lane vi clears
+    // the uncovered bins vi, vi + GS, ...: addresses no pair writes
+#pragma unroll
+    for (int w = 0; w < MW; ++w)
+#pragma unroll
+      for (int o = GS / 2; o > 0; o >>= 1) kept[w] |= (uint32_t)__shfl_xor((int)kept[w], o);
+    for (int b = vi; b < a.D; b += GS) {
+      uint32_t word = 0u;
+#pragma unroll
+      for (int w = 0; w < MW; ++w) word = (b >> 5) == w ? kept[w] : word;
+      if (!((word >> (b & 31)) & 1u)) grad_depth[dbase + (int64_t)b * a.hw] = (TIn)0.f;
+    }
+  }
 #pragma unroll
   for (int k = 0; k < NV; ++k) {
     const int v = vi + k * GS;
     if (v < CV) Vec<TIn, VEC>::store(grad_feat + f * C + (int64_t)v * VEC, acc[k]);
   }
+}
+
+template <typename T>
+hipError_t zero_fill(T* a, int64_t n, hipStream_t stream) {
+  if (n <= 0) return hipSuccess;
+  if ((reinterpret_cast<uintptr_t>(a) & 15u) == 0 && n % (16 / sizeof(T)) == 0) {
+    constexpr int V = 16 / sizeof(T);
+    const int64_t nvec = n / V;
+    k_zero_vec<T, V><<<dim3((unsigned)((nvec + 255) / 256)), dim3(256), 0, stream>>>(a, nvec);
+  } else {
+    k_zero_vec<T, 1><<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream>>>(a, n);
+  }
+  return hipGetLastError();
 }
 
 template <typename TIn, typename TG, int VEC, int NV, int GS>
@@ -376,10 +423,19 @@ hipError_t run_pixels(const Dims& d, const void* grad_out, const void* depth, co
         static_cast<const TG*>(grad_out), static_cast<const TIn*>(depth),
         static_cast<const TIn*>(feat), static_cast<TIn*>(grad_depth), static_cast<TIn*>(grad_feat), b);
   };
+  // dropped points: zeros written by the pixel kernel (small launch, D within
+  // its bin mask), else by a clearing launch before it
+  const bool mask = !many && d.D <= kPixMaskBits;
+  if (!mask) {
+    const hipError_t e = zero_fill(static_cast<TIn*>(grad_depth), d.P, stream);
+    if (e != hipSuccess) return e;
+  }
   if (many)
-    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 4>);
+    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 4, 0>);
+  else if (mask)
+    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 8, kPixMaskWords>);
   else
-    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 8>);
+    launch(k_bwd_pixels<TIn, TG, VEC, NV, GS, 8, 0>);
   return hipGetLastError();
 }
 
@@ -405,18 +461,6 @@ hipError_t run_pixels_nv(const Dims& d, const void* grad_out, const void* depth,
 #undef BWD_RUN
 }
 
-template <typename T>
-hipError_t zero_fill(T* a, int64_t n, hipStream_t stream) {
-  if (n <= 0) return hipSuccess;
-  if ((reinterpret_cast<uintptr_t>(a) & 15u) == 0 && n % (16 / sizeof(T)) == 0) {
-    constexpr int V = 16 / sizeof(T);
-    const int64_t nvec = n / V;
-    k_zero_vec<T, V><<<dim3((unsigned)((nvec + 255) / 256)), dim3(256), 0, stream>>>(a, nvec);
-  } else {
-    k_zero_vec<T, 1><<<dim3((unsigned)((n + 255) / 256)), dim3(256), 0, stream>>>(a, n);
-  }
-  return hipGetLastError();
-}
 
 inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
@@ -458,12 +502,14 @@ hipError_t launch_backward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                      const void* schedule, int32_t n_valid, int32_t n_intervals,
                                      void* grad_depth, void* grad_feat, hipStream_t stream) {
   const bool f32 = in_dtype == BEVPOOL_F32;
-  hipError_t e = f32 ? zero_fill(static_cast<float*>(grad_depth), d.P, stream)
-                     : zero_fill(static_cast<half_t*>(grad_depth), d.P, stream);
-  if (e != hipSuccess) return e;
-  if (n_valid == 0 || n_intervals == 0)  // no kept point: grad_feat is zero too
+  if (n_valid == 0 || n_intervals == 0) {  // no kept point: both gradients are zero
+    hipError_t e = f32 ? zero_fill(static_cast<float*>(grad_depth), d.P, stream)
+                       : zero_fill(static_cast<half_t*>(grad_depth), d.P, stream);
+    if (e != hipSuccess) return e;
     return f32 ? zero_fill(static_cast<float*>(grad_feat), d.rows * d.C, stream)
                : zero_fill(static_cast<half_t*>(grad_feat), d.rows * d.C, stream);
+  }
+  // (grad_depth's dropped points are cleared by run_pixels)
   const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
   const char* sc = static_cast<const char*>(schedule);
   PixArgs a;
