@@ -68,6 +68,17 @@ def forward_min_bytes(cfg, n_valid, n_intervals) -> int:
     return s_in * n_valid + s_in * feat + 8 * n_valid + 12 * n_intervals + s_out * cfg.cells * cfg.C
 
 
+def backward_min_bytes(cfg, n_valid, n_intervals) -> int:
+    """Algorithmic HBM bytes of one backward: the occupied cells' grad_out rows,
+    the whole feature once, depth of kept points, two ranks per kept point and
+    the interval table, all of grad_depth and all of grad_feat."""
+    s_in = 4 if cfg.dtype == "f32" else 2
+    s_out = 4 if cfg.out_dtype == "f32" else 2
+    feat = cfg.B * cfg.N * cfg.H * cfg.W * cfg.C
+    return (s_out * n_intervals * cfg.C + s_in * feat + s_in * n_valid + 8 * n_valid + 12 * n_intervals
+            + s_in * cfg.P + s_in * feat)
+
+
 def source_digest() -> str:
     h = hashlib.sha256()
     for f in FORWARD_SOURCES:
@@ -228,7 +239,11 @@ def main():
     prep_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     fwd_in_step_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    bwd_bytes = backward_min_bytes(cfg, nv, ni)
+    bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
     step_ms = float(np.mean([e[0].elapsed_time(e[3]) for e in evs]))
+    log(f"backward {bwd_ms * 1e3:.1f} us: {bwd_bytes / 1e6:.2f} MB -> {bwd_gbs:.0f} GB/s "
+        f"({bwd_gbs / HBM_PEAK_GBS * 100:.1f}% of peak)")
     log(f"step {step_ms:.4f} ms (wall {wall_ms:.4f}): prepare {prep_ms:.4f} fwd {fwd_in_step_ms:.4f} "
         f"bwd {bwd_ms:.4f}")
 
@@ -368,6 +383,9 @@ def main():
                                               "mean": float(cold_oth.mean())},
             f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
+            "backward_roofline": {"algorithmic_bytes": bwd_bytes, "achieved_gbs": round(bwd_gbs, 1),
+                                  "peak_gbs": HBM_PEAK_GBS, "frac": round(bwd_gbs / HBM_PEAK_GBS, 4),
+                                  "time": "mean over the steps of the step's backward (HIP events)"},
             "prepare_plus_forward_ms": prep_ms + fwd_in_step_ms, "step_wall_ms": wall_ms,
             "paper_context": "0.82 ms at 640x1600 (abstract), hardware not stated; 15.1x the previous "
                              "fastest implementation",
