@@ -68,6 +68,13 @@ def forward_min_bytes(cfg, n_valid, n_intervals) -> int:
     return s_in * n_valid + s_in * feat + 8 * n_valid + 12 * n_intervals + s_out * cfg.cells * cfg.C
 
 
+def prepare_min_bytes(cfg, n_valid, n_intervals) -> int:
+    """Algorithmic HBM bytes of one prepare: the voxel index of every frustum
+    point read once, three ranks per kept point and the interval table written
+    once (the sort's passes are not counted)."""
+    return 12 * cfg.P + 12 * n_valid + 8 * n_intervals + 8
+
+
 def backward_min_bytes(cfg, n_valid, n_intervals) -> int:
     """Algorithmic HBM bytes of one backward: the occupied cells' grad_out rows,
     the whole feature once, depth of kept points, two ranks per kept point and
@@ -216,7 +223,10 @@ def main():
         s = sets[i % len(sets)]
         if ev is not None:
             ev[0].record(stream)
-        prepare(s)
+        plan(s)
+        if ev is not None:
+            ev[4].record(stream)
+        bp.bevpool_schedule(shape, s.rd, s.rb, nv, ni, s.sched, sched_bytes, ws_s, ws_s_bytes, stream)
         if ev is not None:
             ev[1].record(stream)
         forward(s)
@@ -229,7 +239,7 @@ def main():
     for i in range(args.warmup):
         step(i)
     torch.cuda.synchronize()
-    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(args.steps)]
     t0 = time.perf_counter()
     torch.cuda.synchronize()
     for i in range(args.steps):
@@ -239,6 +249,12 @@ def main():
     prep_ms = float(np.mean([e[0].elapsed_time(e[1]) for e in evs]))
     fwd_in_step_ms = float(np.mean([e[1].elapsed_time(e[2]) for e in evs]))
     bwd_ms = float(np.mean([e[2].elapsed_time(e[3]) for e in evs]))
+    plan_ms = float(np.mean([e[0].elapsed_time(e[4]) for e in evs]))
+    sched_ms = float(np.mean([e[4].elapsed_time(e[1]) for e in evs]))
+    plan_bytes = prepare_min_bytes(cfg, nv, ni)
+    plan_gbs = plan_bytes / (plan_ms * 1e-3) / 1e9
+    log(f"prepare {plan_ms * 1e3:.1f} us ({plan_bytes / 1e6:.2f} MB -> {plan_gbs:.0f} GB/s), "
+        f"schedule build {sched_ms * 1e3:.1f} us")
     bwd_bytes = backward_min_bytes(cfg, nv, ni)
     bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
     step_ms = float(np.mean([e[0].elapsed_time(e[3]) for e in evs]))
@@ -383,6 +399,10 @@ def main():
                                               "mean": float(cold_oth.mean())},
             f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
+            "prepare_only_ms": plan_ms, "schedule_build_ms": sched_ms,
+            "prepare_roofline": {"algorithmic_bytes": plan_bytes, "achieved_gbs": round(plan_gbs, 1),
+                                 "peak_gbs": HBM_PEAK_GBS, "frac": round(plan_gbs / HBM_PEAK_GBS, 4),
+                                 "time": "mean over the steps of the step's prepare (HIP events)"},
             "backward_roofline": {"algorithmic_bytes": bwd_bytes, "achieved_gbs": round(bwd_gbs, 1),
                                   "peak_gbs": HBM_PEAK_GBS, "frac": round(bwd_gbs / HBM_PEAK_GBS, 4),
                                   "time": "mean over the steps of the step's backward (HIP events)"},
