@@ -229,7 +229,6 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   const int64_t hw = a.hw32;
   const TIn* const fchunk = feat + (int64_t)cbase * VEC;
 
-  // item i's header (i clamped to this workgroup's items)
   // Item headers, copied to LDS once (the launch gives no workgroup more
   // than kHdrCache items; scalar loads share their wait counter with LDS
   // reads, so loading headers inside the pipeline would stall every walk).
