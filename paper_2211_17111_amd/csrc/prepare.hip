@@ -219,6 +219,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_radix_scatter(
     int32_t* __restrict__ feat_out, const int32_t* __restrict__ n_ptr, int shift, int bits,
     const int32_t* __restrict__ hist_off, int64_t ntiles, int64_t per_view, int64_t hw) {
   __shared__ int cnt[kWavesPerTile][kMaxBuckets];
+  __shared__ int s_delta[kMaxBuckets];  // per digit: global offset minus start in the tile
+  __shared__ int s_scan[kWavesPerTile];
+  __shared__ int32_t s_key[kPrepTile], s_val[kPrepTile];
   const int64_t n = *n_ptr;
   if ((int64_t)blockIdx.x * kPrepTile >= n) return;  // uniform over the block
   const int nbuckets = 1 << bits;
@@ -251,14 +254,26 @@ __global__ __launch_bounds__(kPrepThreads) void k_radix_scatter(
     kreg[r] = key;
     vreg[r] = val;
   }
+  // The tile is written out sorted by digit through LDS, so that lanes store
+  // consecutive positions of one digit's run: element i of the LDS tile goes
+  // to its digit's global offset plus i minus the digit's start in the tile.
+  // (Positions are those of a direct scatter; only the store order differs.)
   __syncthreads();
-  if (threadIdx.x < nbuckets) {
-    int s = 0;
+  static_assert(kMaxBuckets == kPrepThreads, "one thread per digit");
+  const int t = threadIdx.x;
+  int tot_d = 0;  // digit t: each wave's offset within the digit, and its tile count
+  if (t < nbuckets) {
     for (int w = 0; w < kWavesPerTile; ++w) {
-      const int c = cnt[w][threadIdx.x];
-      cnt[w][threadIdx.x] = s;
-      s += c;
+      const int c = cnt[w][t];
+      cnt[w][t] = tot_d;
+      tot_d += c;
     }
+  }
+  int tile_total;
+  const int start_d = block_exclusive_scan<kPrepThreads>(tot_d, s_scan, &tile_total);
+  if (t < nbuckets) {
+    for (int w = 0; w < kWavesPerTile; ++w) cnt[w][t] += start_d;
+    s_delta[t] = hist_off[(int64_t)t * ntiles + blockIdx.x] - start_d;
   }
   __syncthreads();
 #pragma unroll
@@ -266,13 +281,22 @@ __global__ __launch_bounds__(kPrepThreads) void k_radix_scatter(
     const int64_t e = base + r * kWave + lane;
     if (e < n) {
       const uint32_t digit = ((uint32_t)kreg[r] >> shift) & mask;
-      const int pos = hist_off[(int64_t)digit * ntiles + blockIdx.x] + cnt[wid][digit] + rank[r];
-      keys_out[pos] = kreg[r];
-      vals_out[pos] = vreg[r];
-      if (feat_out != nullptr) {
-        const int64_t p = vreg[r];
-        feat_out[pos] = (int32_t)((p / per_view) * hw + p % hw);
-      }
+      const int lpos = cnt[wid][digit] + rank[r];
+      s_key[lpos] = kreg[r];
+      s_val[lpos] = vreg[r];
+    }
+  }
+  __syncthreads();
+  const int n_tile = (int)min<int64_t>(kPrepTile, n - (int64_t)blockIdx.x * kPrepTile);
+  for (int i = t; i < n_tile; i += kPrepThreads) {
+    const int32_t key = s_key[i];
+    const int32_t val = s_val[i];
+    const int pos = s_delta[((uint32_t)key >> shift) & mask] + i;
+    keys_out[pos] = key;
+    vals_out[pos] = val;
+    if (feat_out != nullptr) {
+      const int64_t p = val;
+      feat_out[pos] = (int32_t)((p / per_view) * hw + p % hw);
     }
   }
 }
