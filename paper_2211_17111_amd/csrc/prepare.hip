@@ -294,9 +294,9 @@ __global__ __launch_bounds__(kPrepThreads) void k_radix_scatter(
     const int pos = s_delta[((uint32_t)key >> shift) & mask] + i;
     keys_out[pos] = key;
     vals_out[pos] = val;
-    if (feat_out != nullptr) {
-      const int64_t p = val;
-      feat_out[pos] = (int32_t)((p / per_view) * hw + p % hw);
+    if (feat_out != nullptr) {  // (32-bit: p, D*H*W and H*W are below 2^31)
+      const uint32_t u = (uint32_t)val, pv = (uint32_t)per_view, h = (uint32_t)hw;
+      feat_out[pos] = (int32_t)((u / pv) * h + u % h);
     }
   }
 }
@@ -440,8 +440,11 @@ __global__ __launch_bounds__(kPrepThreads) void k_compact_scatter(Op op,
   }
 }
 
+// (32-bit unsigned arithmetic: p, D*H*W and H*W are below 2^31, and 64-bit
+// division costs several times more)
 __device__ __forceinline__ int32_t pixel_of(int32_t p, int64_t per_view, int64_t hw) {
-  return (int32_t)(((int64_t)p / per_view) * hw + (int64_t)p % hw);
+  const uint32_t u = (uint32_t)p, pv = (uint32_t)per_view, h = (uint32_t)hw;
+  return (int32_t)((u / pv) * h + u % h);
 }
 
 // Strip and local pixel of a feature row.
@@ -449,14 +452,14 @@ struct StripGeom {
   int64_t hw;
   int32_t H, W, bh, bw, nhb, nwb;
   __device__ int32_t strip(int32_t row) const {
-    const int32_t bn = (int32_t)((int64_t)row / hw);
-    const int32_t r = (int32_t)((int64_t)row - (int64_t)bn * hw);
+    const int32_t bn = (int32_t)((uint32_t)row / (uint32_t)hw);  // (row, H*W < 2^31)
+    const int32_t r = row - bn * (int32_t)hw;
     const int32_t h = r / W, w = r - h * W;
     return (bn * nhb + h / bh) * nwb + w / bw;
   }
   __device__ int32_t pixel(int32_t row) const {
-    const int32_t bn = (int32_t)((int64_t)row / hw);
-    const int32_t r = (int32_t)((int64_t)row - (int64_t)bn * hw);
+    const int32_t bn = (int32_t)((uint32_t)row / (uint32_t)hw);  // (row, H*W < 2^31)
+    const int32_t r = row - bn * (int32_t)hw;
     const int32_t h = r / W, w = r - h * W;
     const int32_t w0 = (w / bw) * bw;
     const int32_t bws = min(bw, W - w0);
@@ -524,7 +527,7 @@ struct PairHeads {  // runs of one cell and pixel over consecutive depth bins
     const int32_t p = rd[a];
     pair_rb[pos] = rb[a];
     pair_row[pos] = pixel_of(p, per_view, hw);
-    pair_dn[pos] = (uint32_t)(((int64_t)p % per_view) / hw);
+    pair_dn[pos] = ((uint32_t)p % (uint32_t)per_view) / (uint32_t)hw;
     pair_rd0[pos] = p;
     head_pos[pos] = (int32_t)i;
   }
