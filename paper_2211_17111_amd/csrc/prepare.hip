@@ -127,7 +127,7 @@ __device__ __forceinline__ int32_t bev_rank_or_drop(const int32_t* __restrict__ 
   const int32_t z = coor[3 * p + 2];
   const bool in = (x >= 0) & (x < g.X) & (y >= 0) & (y < g.Y) & (z >= 0) & (z < g.Z);
   if (!in) return -1;
-  const int64_t b = p / g.per_sample;
+  const int64_t b = (uint32_t)p / (uint32_t)g.per_sample;  // (32-bit: P < 2^31)
   return (int32_t)(((b * g.Z + z) * g.Y + y) * g.X + x);
 }
 
