@@ -159,6 +159,30 @@ def test_backward_paths_agree_on_poisoned_outputs():
     assert float((gf - gf2).abs().max()) <= 1e-5 * float(gf2.abs().max()) + 1e-6
 
 
+@pytest.mark.parametrize("D", [31, 32, 33, 128, 129, 150])
+def test_backward_scheduled_dropped_points_poisoned(D):
+    """In a small launch the scheduled backward writes the zeros of dropped
+    points itself from a mask of the depth bins each pixel's pairs cover, when
+    D fits the mask, else through a clearing launch: NaN-poisoned outputs come
+    back equal to the oracle on both sides of the mask's word and size limits."""
+    shape = dict(B=1, N=1, D=D, H=5, W=6, C=16, X=6, Y=6, Z=1)
+    rng = np.random.default_rng(D)
+    coor = random_coor(rng, shape, p_out=0.4)
+    data = draw_small(rng, shape)
+    _gpu.say(f"backward dropped points poisoned: D={D}")
+    plan = _gpu.run_prepare(coor, shape)
+    sched = bp.schedule(plan)
+    g, d, f = (_gpu.to_dev(data[k]) for k in ("grad_out", "depth", "feat"))
+    gd = torch.full_like(d, float("nan"))
+    gf = torch.full_like(f, float("nan"))
+    bp.bevpool_backward_scheduled(shape, bp.BEVPOOL_F32, bp.BEVPOOL_F32, g, d, f, sched.buffer,
+                                  sched.buffer.numel(), plan.n_valid, plan.n_intervals, gd, gf)
+    torch.cuda.synchronize()
+    rgd, rgf, mgd, mgf = oracle.backward_ref(data["grad_out"], data["depth"], data["feat"], coor, shape)
+    _gpu.assert_within(gd.cpu().numpy(), rgd, mgd, "f32", f"D={D} grad_depth")
+    _gpu.assert_within(gf.cpu().numpy(), rgf, mgf, "f32", f"D={D} grad_feat")
+
+
 def test_autograd_wrapper_tiny():
     cfg = CONFIGS["tiny"]
     coor = frustum_coor(cfg)
