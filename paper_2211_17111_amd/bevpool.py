@@ -426,20 +426,29 @@ def backward_scheduled(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.
 
 
 class BevPoolFunction(torch.autograd.Function):
-    """Autograd wrapper: forward pools, backward returns grad_depth, grad_feat."""
+    """Autograd wrapper: forward pools, backward returns grad_depth, grad_feat.
+    Given a Schedule it runs the scheduled forward and backward, given a Plan
+    the plan-only ones (same results within float32 rounding)."""
 
     @staticmethod
-    def forward(ctx, depth, feat, plan: Plan, out_dtype=None):
+    def forward(ctx, depth, feat, plan, out_dtype=None):
         ctx.plan = plan
         ctx.save_for_backward(depth, feat)
+        if isinstance(plan, Schedule):
+            return forward_scheduled(depth, feat, plan, out_dtype)
         return forward(depth, feat, plan, out_dtype)
 
     @staticmethod
     def backward(ctx, grad_out):
         depth, feat = ctx.saved_tensors
-        gd, gf = backward(grad_out.contiguous(), depth, feat, ctx.plan)
+        if isinstance(ctx.plan, Schedule):
+            gd, gf = backward_scheduled(grad_out.contiguous(), depth, feat, ctx.plan)
+        else:
+            gd, gf = backward(grad_out.contiguous(), depth, feat, ctx.plan)
         return gd, gf, None, None
 
 
-def bev_pool(depth, feat, plan: Plan, out_dtype=None):
+def bev_pool(depth, feat, plan, out_dtype=None):
+    """Differentiable pooling of depth x feat into the BEV grid; `plan` is a
+    Plan (from prepare) or a Schedule (from schedule, the faster paths)."""
     return BevPoolFunction.apply(depth, feat, plan, out_dtype)

@@ -183,14 +183,18 @@ def test_backward_scheduled_dropped_points_poisoned(D):
     _gpu.assert_within(gf.cpu().numpy(), rgf, mgf, "f32", f"D={D} grad_feat")
 
 
-def test_autograd_wrapper_tiny():
+@pytest.mark.parametrize("use_schedule", [False, True])
+def test_autograd_wrapper_tiny(use_schedule):
+    """bev_pool with a Plan (plan-only paths) or a Schedule (scheduled paths)."""
     cfg = CONFIGS["tiny"]
     coor = frustum_coor(cfg)
     data = draw_inputs(cfg)
     plan = _gpu.run_prepare(coor, cfg.shape())
     depth = _gpu.to_dev(data["depth"]).requires_grad_(True)
     feat = _gpu.to_dev(data["feat"]).requires_grad_(True)
-    out = bp.bev_pool(depth, feat, plan)
+    out = bp.bev_pool(depth, feat, bp.schedule(plan) if use_schedule else plan)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
+    _gpu.assert_within(out.detach().cpu().numpy(), ref, mag, "f32", "autograd out")
     out.backward(_gpu.to_dev(data["grad_out"]))
     rgd, rgf, mgd, mgf = oracle.backward_ref(data["grad_out"], data["depth"], data["feat"], coor,
                                              cfg.shape())
