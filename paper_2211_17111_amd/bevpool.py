@@ -392,13 +392,28 @@ def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, 
     return out
 
 
-def backward(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor, plan: Plan,
-             workspace: torch.Tensor | None = None, stream=None):
-    sd = plan.shape
-    B, N, D, H, W, C = (sd[k] for k in ("B", "N", "D", "H", "W", "C"))
+def _check_grad_inputs(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor, sd: dict):
+    """grad_out must have out's shape (B, Z, Y, X, C) and a dtype the library
+    accepts with depth's (float32 with float32; float16 or float32 with
+    float16); depth and feat the plan's shapes."""
+    B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
     _require(grad_out, "grad_out")
     _require(depth, "depth")
     _require(feat, "feat", depth.dtype)
+    if depth.dtype not in _DTYPE_CODE or grad_out.dtype not in _DTYPE_CODE:
+        raise ValueError(f"unsupported dtypes depth {depth.dtype}, grad_out {grad_out.dtype}")
+    if depth.dtype == torch.float32 and grad_out.dtype != torch.float32:
+        raise ValueError("float32 inputs need a float32 grad_out")
+    if tuple(depth.shape) != (B, N, D, H, W) or tuple(feat.shape) != (B, N, H, W, C):
+        raise ValueError("depth/feat shapes do not match the plan")
+    if tuple(grad_out.shape) != (B, Z, Y, X, C):
+        raise ValueError(f"grad_out must be {(B, Z, Y, X, C)}, got {tuple(grad_out.shape)}")
+
+
+def backward(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.Tensor, plan: Plan,
+             workspace: torch.Tensor | None = None, stream=None):
+    sd = plan.shape
+    _check_grad_inputs(grad_out, depth, feat, sd)
     gd = torch.empty_like(depth)
     gf = torch.empty_like(feat)
     ws_bytes = bevpool_backward_workspace_size(sd)
@@ -414,9 +429,7 @@ def backward_scheduled(grad_out: torch.Tensor, depth: torch.Tensor, feat: torch.
                        sched: Schedule, stream=None):
     plan = sched.plan
     sd = plan.shape
-    _require(grad_out, "grad_out")
-    _require(depth, "depth")
-    _require(feat, "feat", depth.dtype)
+    _check_grad_inputs(grad_out, depth, feat, sd)
     gd = torch.empty_like(depth)
     gf = torch.empty_like(feat)
     bevpool_backward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[grad_out.dtype], grad_out,

@@ -51,7 +51,9 @@ def assert_plan_equal(got: dict, ref: dict, label: str = ""):
                                  f"gpu {g[bad[0]]} vs oracle {r[bad[0]]}")
 
 
-def assert_within(gpu, ref, mag, dtype: str, label: str = ""):
+def assert_within(gpu, ref, mag, dtype: str, label: str = "", log: bool = False) -> float:
+    """Every element within tol * sum|terms| + 1e-6 of the oracle; returns the
+    worst ratio err / bound (printed when ``log``)."""
     gpu = np.asarray(gpu, dtype=np.float64)
     ref = np.asarray(ref, dtype=np.float64)
     mag = np.asarray(mag, dtype=np.float64)
@@ -63,6 +65,10 @@ def assert_within(gpu, ref, mag, dtype: str, label: str = ""):
         i = np.unravel_index(np.argmax(np.where(bad, err / bound, 0)), err.shape)
         raise AssertionError(f"{label}: {int(bad.sum())} elements out of tolerance; worst at {i}: "
                              f"gpu {gpu[i]} oracle {ref[i]} |terms| {mag[i]}")
+    worst = float((err / bound).max()) if err.size else 0.0
+    if log:
+        say(f"{label}: {err.size} elements within tolerance, worst err/bound {worst:.3e}")
+    return worst
 
 
 def torch_dtype(name: str):
