@@ -50,8 +50,8 @@ HBM_PEAK_GBS = 8000.0
 MALL_BYTES = 256 * 2 ** 20
 PMC_FILE = os.path.join(ROOT, "profiles", "forward_headline_traffic.txt")
 # kernels of each forward path (the interval path is two launches, timed together)
-FORWARD_KERNELS = {"interval": "k_fwd_ranges+k_fwd_cells", "strips": "k_fwd_pieces+k_fwd_cross"}
-FORWARD_SOURCES = ("forward.hip", "forward_pieces.hip", "internal.h", "vec.h", "device_utils.h")
+FORWARD_KERNELS = {"interval": "k_fwd_ranges+k_fwd_cells", "strips": "k_fwd_strips+k_fwd_combine"}
+FORWARD_SOURCES = ("forward.hip", "forward_strips.hip", "internal.h", "vec.h", "device_utils.h")
 
 
 def log(msg):
@@ -191,14 +191,13 @@ def main():
     for s in sets:
         prepare(s)
     torch.cuda.synchronize()
-    header = sets[0].sched[:64].view(torch.int32).cpu().tolist()
-    n_slots = header[7]
+    n_slots = int(sets[0].sched[:64].view(torch.int32)[7])
     ws_fs_bytes = bp.bevpool_forward_scheduled_workspace_size(shape, n_slots)
     ws_fs = torch.empty(max(ws_fs_bytes, 16), dtype=torch.uint8, device=dev)
     log(f"schedule: {n_slots} slots ({ws_fs_bytes / 2**20:.1f} MiB workspace)")
 
     def forward_strips(s):
-        bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, header,
+        bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, nv, ni,
                                      s.out, ws_fs, ws_fs_bytes, stream)
 
     def forward_interval(s):

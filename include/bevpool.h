@@ -154,54 +154,51 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
 
 /*
  * Schedule (optional): a regrouping of the plan of section 2.1, built once
- * offline like the plan itself, for the scheduled forward and backward.
+ * offline like the plan itself.
  *
- * The feature map of every (sample, camera) image is cut into strips of 4
- * adjacent columns (all rows).  A column's frustum points lie in one
- * vertical plane, so as the depth grows they cross the BEV cells one after
- * another; within a strip, kept points of one pixel in one cell over
- * consecutive depth bins form a pair (their depth scores are summed before
- * the pixel's feature row is used).  The cells a strip reaches are cut into
- * pieces (one workgroup of the forward each); the cells of one column of a
- * piece are cut into blocks of 12 whose pixel x cell weights form a small
- * dense matrix.  A cell reached from several strips gets one partial-sum
- * slot per strip in the forward's workspace, added in strip order.  The
- * pairs are also listed pixel by pixel for the backward.
- *
- * Limits of the schedule (the plan-only calls have none): D <= 2048 and
- * 48 * H <= 8192 (H <= 170); bevpool_schedule_size returns BEVPOOL_EINVAL
- * beyond them.
+ * The schedule regroups the kept points of a plan by image strips: blocks of
+ * bh x bw feature pixels of one camera image, normally whole pixel columns
+ * (the frustum points of a pixel column lie in one vertical plane, so a
+ * strip's points fall into few BEV cells).  Within a strip, kept points of one
+ * pixel in one cell over consecutive depth bins form a pair: their depth
+ * scores are summed first and the pixel's feature row is read once.  The
+ * pairs are cut into equal shares, one per workgroup of the scheduled forward
+ * on the device the schedule is built on (its compute units); a strip's pairs
+ * are cut at those shares and into items of at most a few thousand pairs, and
+ * an item's pairs into segments (one per cell).  A schedule built on one
+ * device gives the same results on another; only the balance of the work
+ * over the workgroups depends on the device.  A cell covered by one segment
+ * is written directly; a cell covered by several has one partial-sum slot per
+ * segment in the forward's workspace, added in a fixed order.
  *
  * bevpool_schedule_size gives the schedule buffer size and the build
  * workspace size for a plan with n_valid kept points and n_intervals
  * occupied cells.  bevpool_schedule reads the first n_valid entries of
  * ranks_depth and ranks_bev of a plan from bevpool_prepare and writes the
  * schedule (device memory owned by the caller).  Enqueued on `stream`;
- * deterministic (the same plan always gives the same bytes).  The schedule
- * starts with BEVPOOL_SCHEDULE_HEADER int32 counts, indexed by
- * bevpool_schedule_count; the rest is opaque.  The caller reads the header
- * back once after the build has completed and passes that host copy to every
- * bevpool_forward_scheduled call: the launch is sized from it.
+ * deterministic.  The schedule starts with BEVPOOL_SCHEDULE_HEADER int32
+ * counts, indexed by bevpool_schedule_count; the rest is opaque.  A caller
+ * reads the header back once (after the build has completed) to size the
+ * forward's workspace.
  *
  * bevpool_forward_scheduled computes exactly what bevpool_forward computes
  * (same layouts, dtypes and zero-filled empty cells, every element of `out`
- * written once, no atomics, bitwise reproducible) from the schedule and its
- * header.  Its workspace holds the slots:
- * bevpool_forward_scheduled_workspace_size bytes for the header's
- * BEVPOOL_SCHEDULE_SLOTS count (float32 rows of C; may be 0 bytes and NULL
- * when that count is 0); a smaller workspace is BEVPOOL_EWORKSPACE and a
- * header whose counts are inconsistent with each other, with the shape or
- * with schedule_bytes is BEVPOOL_EINVAL, both before any HIP call.  If the
- * device copy of the header does not equal `header` (a header from another
- * schedule), every element of `out` is written as NaN.  The workspace
- * contents are scratch: one forward at a time per workspace; the schedule is
- * only read, so concurrent forwards may share it.
+ * written once, no atomics, bitwise reproducible) from the schedule alone;
+ * n_valid and n_intervals must be the values the schedule was built with.
+ * Its workspace holds the slots: bevpool_forward_scheduled_workspace_size
+ * bytes for the header's BEVPOOL_SCHEDULE_SLOTS count (float32 rows of C;
+ * may be 0 bytes and NULL when that count is 0).  The workspace contents are
+ * scratch: one forward at a time per workspace; the schedule is only read, so
+ * concurrent forwards may share it.  The size cannot be checked without
+ * reading the schedule: cells whose slots lie beyond a too small workspace
+ * are written as NaN (nothing is written outside the workspace).  A schedule
+ * whose cell count does not match n_intervals leaves `out` unwritten.
  */
 #define BEVPOOL_SCHEDULE_HEADER 16
 enum bevpool_schedule_count {
   BEVPOOL_SCHEDULE_PAIRS = 0,
-  BEVPOOL_SCHEDULE_PIECES = 1,      /* workgroups of the scheduled forward */
-  BEVPOOL_SCHEDULE_BLOCKS = 2,
+  BEVPOOL_SCHEDULE_ITEMS = 1,
+  BEVPOOL_SCHEDULE_SEGMENTS = 2,
   BEVPOOL_SCHEDULE_KEPT = 3,        /* n_valid the schedule was built with */
   BEVPOOL_SCHEDULE_CELLS = 4,       /* n_intervals the schedule was built with */
   BEVPOOL_SCHEDULE_CELLS_FOUND = 5, /* occupied cells found in the plan */
@@ -219,8 +216,9 @@ int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t
                                               size_t* bytes);
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
-                              size_t schedule_bytes, const int32_t* header, void* out,
-                              void* workspace, size_t workspace_bytes, void* stream);
+                              size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                              void* out, void* workspace, size_t workspace_bytes,
+                              void* stream);
 
 /*
  * Gradients of bevpool_forward (not in the paper; chain rule):

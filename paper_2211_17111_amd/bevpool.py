@@ -75,8 +75,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_scheduled.restype = ctypes.c_int
     lib.bevpool_forward_scheduled_workspace_size.restype = ctypes.c_int
     lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
-    lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz,
-                                              ctypes.POINTER(i32), vp, vp, sz, vp]
+    lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
+                                              vp, vp, sz, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -209,29 +209,15 @@ def bevpool_forward_scheduled_workspace_size(shape, n_slots) -> int:
     return n.value
 
 
-SCHEDULE_HEADER = 16
-
-
-def _header(header):
-    """A host int32[16] copy of a schedule header (list, tuple, array or tensor)."""
-    if header is None:
-        return None
-    if isinstance(header, torch.Tensor):
-        header = header.cpu().tolist()
-    vals = [int(v) for v in header]
-    if len(vals) != SCHEDULE_HEADER:
-        raise ValueError(f"a schedule header has {SCHEDULE_HEADER} counts, got {len(vals)}")
-    return (ctypes.c_int32 * SCHEDULE_HEADER)(*vals)
-
-
 def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
-                              header, out, workspace, workspace_bytes, stream=None) -> None:
+                              n_valid, n_intervals, out, workspace, workspace_bytes,
+                              stream=None) -> None:
     lib = load_library()
     s = make_shape(shape)
     _check(lib, lib.bevpool_forward_scheduled(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
                                               _ptr(feat), _ptr(schedule), int(schedule_bytes),
-                                              _header(header), _ptr(out), _ptr(workspace),
-                                              int(workspace_bytes), _stream(stream)),
+                                              int(n_valid), int(n_intervals), _ptr(out),
+                                              _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
 
 
@@ -352,7 +338,7 @@ class Schedule:
     counts: list[int]
 
     def header(self) -> list[int]:
-        """The 16 header counts (pairs, pieces, blocks, kept points, cells, cells found,
+        """The 16 header counts (pairs, items, segments, kept points, cells, cells found,
         empty cells, slots, ...), read back from the device."""
         return self.buffer[:64].view(torch.int32).cpu().tolist()
 
@@ -401,7 +387,7 @@ def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, 
     if workspace is None:
         workspace = forward_scheduled_workspace(sched)
     bevpool_forward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, sched.buffer,
-                              sched.buffer.numel(), sched.counts, out, workspace,
+                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, out, workspace,
                               workspace.numel() * workspace.element_size(), stream)
     return out
 

@@ -21,8 +21,7 @@ LIB_NAME = "libbevpool.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
 ARCH = "gfx950"
-SOURCES = ["prepare.hip", "schedule.hip", "forward.hip", "forward_pieces.hip", "backward.hip",
-           "api.cpp"]
+SOURCES = ["prepare.hip", "forward.hip", "forward_strips.hip", "backward.hip", "api.cpp"]
 
 # No fast-math and no flush-to-zero on the GPU path; packed fp32 ops off.
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

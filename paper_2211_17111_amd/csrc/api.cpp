@@ -201,24 +201,12 @@ static int check_counts(const bevpool::Dims& d, int32_t n_valid, int32_t n_inter
   return BEVPOOL_OK;
 }
 
-static int check_schedule_shape(const bevpool::Dims& d) {
-  if (d.D > bevpool::kSchedMaxD)
-    return fail(BEVPOOL_EINVAL, "a schedule addresses at most %d depth bins: D = %lld",
-                bevpool::kSchedMaxD, (long long)d.D);
-  if (bevpool::sched_tc_max(d.H) < 1)
-    return fail(BEVPOOL_EINVAL, "a schedule's weight blocks need 48*H <= %d: H = %lld",
-                bevpool::kSchedEntries, (long long)d.H);
-  return BEVPOOL_OK;
-}
-
 int bevpool_schedule_size(const bevpool_shape* shape, int32_t n_valid, int32_t n_intervals,
                           size_t* schedule_bytes, size_t* workspace_bytes) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);
   if (st != BEVPOOL_OK) return st;
   st = check_counts(d, n_valid, n_intervals);
-  if (st != BEVPOOL_OK) return st;
-  st = check_schedule_shape(d);
   if (st != BEVPOOL_OK) return st;
   REQUIRE_PTR(schedule_bytes);
   REQUIRE_PTR(workspace_bytes);
@@ -237,13 +225,14 @@ int bevpool_schedule(const bevpool_shape* shape, const int32_t* ranks_depth,
   if (st != BEVPOOL_OK) return st;
   st = check_counts(d, n_valid, n_intervals);
   if (st != BEVPOOL_OK) return st;
-  st = check_schedule_shape(d);
-  if (st != BEVPOOL_OK) return st;
   if (n_valid > 0) {
     REQUIRE_PTR(ranks_depth);
     REQUIRE_PTR(ranks_bev);
   }
   REQUIRE_PTR(schedule);
+  if (d.D > 65535)
+    return fail(BEVPOOL_EINVAL, "the schedule stores depth bins in 16 bits: D = %lld > 65535",
+                (long long)d.D);
   const bevpool::ScheduleLayout L = bevpool::schedule_layout(d, n_valid, n_intervals);
   if (schedule_bytes < L.total)
     return fail(BEVPOOL_EINVAL, "schedule needs %zu bytes, got %zu", L.total, schedule_bytes);
@@ -266,64 +255,32 @@ int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t
   return ok();
 }
 
-// The host copy of a schedule's header: counts consistent with each other,
-// with the shape and with the buffer size.
-static int check_schedule_header(const bevpool::Dims& d, const int32_t* h, size_t schedule_bytes) {
-  using namespace bevpool;
-  const int32_t nv = h[kSHdrValid], ni = h[kSHdrOcc];
-  int st = check_counts(d, nv, ni);
-  if (st != BEVPOOL_OK) return st;
-  if (nv == 0) return BEVPOOL_OK;
-  const ScheduleLayout L = schedule_layout(d, nv, ni);
-  if (schedule_bytes < L.total)
-    return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu its header needs",
-                schedule_bytes, L.total);
-  if (h[kSHdrOccFound] != ni)
-    return fail(BEVPOOL_EINVAL, "schedule header: %d cells found, %d in the plan",
-                h[kSHdrOccFound], ni);
-  const int64_t np = h[kSHdrPairs];
-  const int64_t tcmax = sched_tc_max(d.H);
-  const bool ok_counts =
-      np >= 1 && np <= nv && h[kSHdrPieces] >= 1 && h[kSHdrPieces] <= L.piece_cap &&
-      h[kSHdrTCs] >= h[kSHdrPieces] && h[kSHdrTCs] <= np && h[kSHdrCCs] >= h[kSHdrTCs] &&
-      h[kSHdrCCs] <= np && h[kSHdrBlocks] >= h[kSHdrPieces] && h[kSHdrBlocks] <= h[kSHdrCCs] &&
-      h[kSHdrEmpty] == d.cells - ni && h[kSHdrSlots] >= 0 && h[kSHdrSlots] <= h[kSHdrTCs] &&
-      h[kSHdrComb] >= 0 && h[kSHdrComb] <= ni && h[kSHdrMaxEnt] >= 1 &&
-      h[kSHdrMaxEnt] <= kSchedEntries && h[kSHdrMaxBlk] >= 1 &&
-      h[kSHdrMaxBlk] <= kSchedSW * (tcmax + kSchedK - 1) / kSchedK && h[kSHdrMaxPix] >= 1 &&
-      h[kSHdrMaxPix] <= d.H * kSchedSW && h[kSHdrMaxRec] >= 1 && h[kSHdrMaxRec] <= kSchedEntries &&
-      h[kSHdrPixrec] >= 1 && h[kSHdrPixrec] <= L.pixrec_cap;
-  if (!ok_counts) return fail(BEVPOOL_EINVAL, "schedule header counts are inconsistent");
-  return BEVPOOL_OK;
-}
-
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
-                              size_t schedule_bytes, const int32_t* header, void* out,
-                              void* workspace, size_t workspace_bytes, void* stream) {
+                              size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);
   if (st != BEVPOOL_OK) return st;
   st = check_dtypes(in_dtype, out_dtype);
   if (st != BEVPOOL_OK) return st;
+  st = check_counts(d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
   REQUIRE_PTR(out);
-  REQUIRE_PTR(header);
-  st = check_schedule_shape(d);
-  if (st != BEVPOOL_OK) return st;
-  st = check_schedule_header(d, header, schedule_bytes);
-  if (st != BEVPOOL_OK) return st;
-  if (header[bevpool::kSHdrValid] > 0) {
+  if (n_intervals > 0) {
     REQUIRE_PTR(depth);
     REQUIRE_PTR(feat);
     REQUIRE_PTR(schedule);
-    const size_t need =
-        bevpool::forward_scheduled_workspace_bytes(d, header[bevpool::kSHdrSlots]);
-    if (workspace_bytes < need || (need > 0 && workspace == nullptr))
-      return fail(BEVPOOL_EWORKSPACE, "forward needs %zu workspace bytes (%d slots), got %zu at %p",
-                  need, header[bevpool::kSHdrSlots], workspace_bytes, workspace);
+    const size_t need = bevpool::schedule_layout(d, n_valid, n_intervals).total;
+    if (schedule_bytes < need)
+      return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
+                  schedule_bytes, need);
+    if (workspace == nullptr && workspace_bytes > 0)
+      return fail(BEVPOOL_EWORKSPACE, "workspace of %zu bytes at NULL", workspace_bytes);
   }
   return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, depth, feat, schedule,
-                                                    header, out, workspace, workspace_bytes,
+                                                    n_valid, n_intervals, out, workspace,
+                                                    workspace_bytes,
                                                     static_cast<hipStream_t>(stream)),
                   "bevpool_forward_scheduled");
 }
@@ -388,8 +345,6 @@ int bevpool_backward_scheduled(const bevpool_shape* shape, int in_dtype, int out
   REQUIRE_PTR(grad_feat);
   if (n_valid > 0 && n_intervals > 0) {
     REQUIRE_PTR(schedule);
-    st = check_schedule_shape(d);
-    if (st != BEVPOOL_OK) return st;
     const size_t need = bevpool::schedule_layout(d, n_valid, n_intervals).total;
     if (schedule_bytes < need)
       return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",

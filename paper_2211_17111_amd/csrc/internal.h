@@ -50,96 +50,106 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
                           hipStream_t stream);
 
 // ---- schedule ----------------------------------------------------------------
-// The block schedule regroups the kept points of a plan for the scheduled
-// forward (and lists them pixel by pixel for the scheduled backward).
-// Terms, every count over kept points:
-//   strip  kSchedSW adjacent feature-map columns of one (sample, camera)
-//          image, all H rows; strips are numbered (b*N + n) * nsw + w / SW,
-//          nsw = ceil(W / SW); a pixel's column in its strip is w % SW
-//   pair   a maximal run of one pixel's kept points in one cell over
-//          consecutive depth bins (first bin d0, n points); pairs are ordered
-//          by (strip, cell, h * SW + column, d0)
-//   TC     (strip, cell) with pairs; within a strip TCs are ranked by (least
-//          d0, cell)
-//   piece  a run of consecutive TCs of one strip; a piece starts at a strip's
-//          first TC, at every tcmax-th TC of the strip (tcmax = kSchedK *
-//          min(4, kSchedEntries / (SW * K * H))) and where the strip's pair
-//          count before the TC crosses a multiple of kSchedPairs.  One piece
-//          is one workgroup of the scheduled forward.
-//   CC     (TC, column) with pairs; within a piece, ordered by (column, least
-//          d0, cell)
-//   block  kSchedK consecutive CCs of one column of a piece (fewer at the end
-//          of the column's run): the dense weight matrix of its CCs over the
-//          column's rows [hlo, hlo + nu), entries ebase + u * K + k of the
-//          piece's weight array
-//   slot   a float32 row of the forward's workspace: the partial sum of a TC
-//          whose cell is also reached from other strips; slots are numbered
-//          in (cell, strip) order
-// Device layout (int32 words, 256-byte aligned arrays; capacities from
-// n_valid, see schedule_layout):
-//   header[16]              counts, kSHdr*
-//   piece[n_pieces][16]     strip, plo, nh, dlo, nd, blk0, nblk, rec0, nrec,
-//                           tc0, ntc, cc0, ncc, nent, pix0, ncol (columns of
-//                           the strip inside the image)
-//   block[n_blocks][4]      column | ncells << 8, hlo, nu, ebase
-//   cc[n_ccs]               ebase + k | hlo << 16 (piece CC table)
-//   tc[n_tcs][2]            destination (BEV rank, or ~slot), and the partial
-//                           row (block-in-piece * K + k) of each column, one
-//                           byte each (0xff: no pair in that column)
-//   pixrec[n_pixrec]        per piece, per local pixel (h - plo) * SW +
-//                           column, its first record (relative to rec0), and
-//                           nrec after the last pixel
-//   rec[n_pairs]            per piece, pairs in (local pixel, d0) order:
-//                           d0 - dlo | (n - 1) << 11 | CC of the piece << 24
-//   comb_cell[n_comb], comb_slot0[n_comb + 1]   cells with several TCs
-//   empty[n_empty]          cells no kept point reaches, ascending
-//   bp_cell[n_pairs], bp_dn[n_pairs], pix_pair0[rows + 1]
-//                           the pairs in feature-row order (stable): BEV
-//                           rank, d0 | n << 16; first pair of every row
-constexpr int kSchedSW = 4;          // strip width in columns
-constexpr int kSchedK = 12;          // CCs per block
-constexpr int kSchedPairs = 3000;    // pairs per piece
-constexpr int kSchedEntries = 8192;  // most weight entries of a piece
-constexpr int kSchedMaxCC = 256;     // most CCs of a piece (8-bit index)
-constexpr int kSchedMaxD = 2048;     // depth bins a record can address
-constexpr int kPieceWords = 16;
-constexpr int kSHdrPairs = 0, kSHdrPieces = 1, kSHdrBlocks = 2, kSHdrValid = 3, kSHdrOcc = 4,
-              kSHdrOccFound = 5, kSHdrEmpty = 6, kSHdrSlots = 7, kSHdrComb = 8, kSHdrTCs = 9,
-              kSHdrCCs = 10, kSHdrMaxEnt = 11, kSHdrMaxBlk = 12, kSHdrMaxPix = 13,
-              kSHdrPixrec = 14, kSHdrMaxRec = 15;
-constexpr int kSchedHdrChecked = 16;  // header words a forward checks against its launch
-static_assert(kSHdrPairs == BEVPOOL_SCHEDULE_PAIRS && kSHdrPieces == BEVPOOL_SCHEDULE_PIECES &&
-                  kSHdrBlocks == BEVPOOL_SCHEDULE_BLOCKS && kSHdrValid == BEVPOOL_SCHEDULE_KEPT &&
-                  kSHdrOcc == BEVPOOL_SCHEDULE_CELLS &&
-                  kSHdrOccFound == BEVPOOL_SCHEDULE_CELLS_FOUND &&
-                  kSHdrEmpty == BEVPOOL_SCHEDULE_EMPTY && kSHdrSlots == BEVPOOL_SCHEDULE_SLOTS,
+// A schedule regroups the kept points of a plan by image strips, for the
+// scheduled forward and backward.  Definitions:
+//   strip    a block of bh x bw feature pixels of one (sample, camera) image;
+//            bh = min(H, R), bw = min(W, max(1, R / bh)) with R =
+//            strip_pixels(C) (strips of the last block row and column are cut
+//            at the image edge).  Strips are numbered (b, n, h / bh, w / bw)
+//            row-major; a pixel's local index in its strip is row-major over
+//            the strip's own width.  A column of pixels views one azimuth, so
+//            a strip's points fall into few BEV cells.
+//   pair     maximal run of kept points of one strip, one cell and one pixel
+//            over consecutive depth bins; pairs are ordered by (strip, BEV
+//            rank, local pixel, depth bin)
+//   share    pairs [c_w, c_(w+1)) of all P pairs, w < S: one share per
+//            workgroup of the scheduled forward (S = shares in the header), so
+//            that every workgroup sums about the same number of pairs;
+//            c_w = floor(P * w / S), moved to the start (end) of the strip it
+//            falls in when less than kMinPiece pairs from it
+//   item     a run of one strip's pairs inside one share: a strip is cut at
+//            the share boundaries inside it, and each piece of L pairs into
+//            K = ceil(L / kItemPairs) items, item j starting at pair
+//            floor(j * L / K) of the piece
+//   segment  maximal run of pairs of one cell inside one item
+//   slot     a float32 row of the forward workspace holding one segment's
+//            partial sum; only cells covered by several segments have slots,
+//            numbered by (cell, segment)
+// Device layout (int32 / uint32, 256-byte aligned arrays):
+//   header[16]                  counts, see kHdr*
+//   pair_rd0[n_valid]           depth rank of the pair's first point
+//   pair_ln[n_valid]            local pixel | segment head << 15 | points << 16
+//   pair_seg[n_valid] (uint16)  the pair's segment within its item
+//   item_strip[items_cap]       strip of each item
+//   item_pair0[items_cap + 1]   first pair of each item (+ end sentinel)
+//   item_seg0[items_cap + 1]    first segment of each item (+ end sentinel)
+//   seg_dest[n_valid]           BEV rank of a segment alone in its cell, or
+//                               ~slot (negative) for a cell with several
+//   comb_cell[n_occ + 1]        cells with several segments, ascending
+//   comb_slot0[n_occ + 1]       first slot of each (+ end sentinel: slots)
+//   empty[cells - n_occ + 1]    BEV rank of each empty cell, ascending
+//   bp_cell[n_valid]            pixel-major pairs (the pairs stably sorted by
+//   bp_dn[n_valid]                feature rank): BEV rank, d0 | points << 16
+//   pix_pair0[rows + 1]         first pixel-major pair of each feature row
+//   share_item0[kMaxShares + 1] first item of each share (+ end sentinel:
+//                               items), for the shares in the header
+constexpr int kItemPairs = 2048;          // most pairs of one forward item
+constexpr int kStripBytes = 32 * 1024;    // staged feature bytes of a strip (4-byte elements)
+constexpr uint32_t kPairHead = 1u << 15;  // pair_ln: first pair of a segment
+constexpr uint32_t kPairPixel = kPairHead - 1;
+constexpr int kHdrPairs = 0, kHdrItems = 1, kHdrSegs = 2, kHdrValid = 3, kHdrOcc = 4,
+              kHdrOccFound = 5, kHdrEmpty = 6, kHdrSlots = 7, kHdrComb = 8, kHdrStrips = 9,
+              kHdrShares = 10,     // S, the shares the items are cut at
+              kHdrSharesOk = 11;   // 1 if no share has more than kShareItems items
+constexpr int kMaxShares = 1024;   // most shares (workgroups of the scheduled forward)
+constexpr int kShareItems = 128;   // most items of a share the forward takes as one
+constexpr int kMinPiece = 512;     // share boundaries closer to a strip end move to it
+static_assert(kHdrPairs == BEVPOOL_SCHEDULE_PAIRS && kHdrItems == BEVPOOL_SCHEDULE_ITEMS &&
+                  kHdrSegs == BEVPOOL_SCHEDULE_SEGMENTS && kHdrValid == BEVPOOL_SCHEDULE_KEPT &&
+                  kHdrOcc == BEVPOOL_SCHEDULE_CELLS && kHdrOccFound == BEVPOOL_SCHEDULE_CELLS_FOUND &&
+                  kHdrEmpty == BEVPOOL_SCHEDULE_EMPTY && kHdrSlots == BEVPOOL_SCHEDULE_SLOTS,
               "header indices are part of the C interface");
 // gfx950 (MI355X) has 8 accelerator complex dies; workgroup i of a launch is
 // dispatched to die i % 8, each die with its own L2.
 constexpr int kXcds = 8;
 
-// Compute units of the current device (cached per device).
-int device_cus();
-// TCs per piece for a feature-map height H (0: H too large for a schedule).
-int64_t sched_tc_max(int64_t H);
+struct StripDims {
+  int64_t bh, bw;    // strip height and width in pixels
+  int64_t nhb, nwb;  // strips per image column and row
+  int64_t strips;    // B * N * nhb * nwb
+  int64_t pixels;    // bh * bw: most pixels of a strip
+};
+// Most pixels per strip: the staged feature rows of a 64-vector channel
+// chunk (at most 256 four-byte elements per row) fit kStripBytes.
+int64_t strip_pixels(int64_t C);
+StripDims strip_dims(const Dims& d);
 
 struct ScheduleLayout {
-  size_t header, piece, block, cc, tc, pixrec, rec, comb_cell, comb_slot0, empty, bp_cell, bp_dn,
-      pix_pair0, total;  // byte offsets of the schedule's arrays, and its size
-  size_t ws_total;       // bytes of build workspace
-  int64_t n_valid, n_occ, n_empty, piece_cap, pixrec_cap, nsw, strips;
+  size_t header, pair_rd0, pair_ln, pair_seg, item_strip, item_pair0, item_seg0, seg_dest, comb_cell,
+      comb_slot0, empty, bp_cell, bp_dn, pix_pair0, share_item0, total;
+  int64_t n_valid, n_occ, n_empty, items_cap;
+  StripDims sd;
+  // build workspace
+  size_t ws_ka, ws_va, ws_kb, ws_vb, ws_head, ws_pair_rb, ws_pair_row, ws_pair_dn, ws_flags,
+      ws_strip, ws_tiles, ws_hist, ws_sums, ws_total;
+  int64_t ntiles, nscan;
+  int row_bits, cell_bits, pixel_bits, strip_bits;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
+// Compute units of the current device (cached per device).
+int device_cus();
+// Workgroups of the scheduled forward on the current device: one per CU,
+// a whole number per die; the shares a schedule is cut at.
+int forward_workgroups();
 hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
                            int32_t n_intervals, void* schedule, void* workspace,
                            hipStream_t stream);
 // Float32 workspace rows of the scheduled forward: one per slot.
 size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots);
-// `hdr` is the host copy of the schedule's header.
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
-                                    const int32_t* hdr, void* out, void* workspace,
-                                    size_t workspace_bytes, hipStream_t stream);
+                                    int32_t n_valid, int32_t n_intervals, void* out,
+                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
 
 // ---- forward ---------------------------------------------------------------
 size_t forward_workspace_bytes(const Dims& d);

@@ -166,6 +166,15 @@ def test_schedule_validation(lib):
     assert call(sb=sb.value - 1) == EINVAL
     assert call(ws=None) == EWORKSPACE
     assert call(wb=wb.value - 1) == EWORKSPACE
+    f = lambda **k: lib.bevpool_forward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0), DUMMY, DUMMY,
+                                                  k.get("sc", DUMMY), k.get("sb", sb.value), 1000, 100,
+                                                  k.get("out", DUMMY), k.get("ws", DUMMY),
+                                                  k.get("wb", 1024), None)
+    assert f(i=0, o=1) == EDTYPE
+    assert f(sc=None) == EINVAL
+    assert f(sb=16) == EINVAL
+    assert f(out=None) == EINVAL
+    assert f(ws=None) == EWORKSPACE
     n = ctypes.c_size_t(0)
     assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), 10, ctypes.byref(n)) == OK
     assert n.value == 10 * s.C * 4
@@ -179,64 +188,3 @@ def test_schedule_validation(lib):
     assert b(sc=None) == EINVAL
     assert b(sb=16) == EINVAL
     assert b(gf=None) == EINVAL
-
-
-def _small_schedule():
-    """A schedule (numpy derivation) of a small random plan, and its shape."""
-    import numpy as np
-    import _blocks
-    import oracle
-    from workloads import random_coor
-    shape = dict(B=1, N=2, D=9, H=7, W=13, C=16, X=12, Y=10, Z=2)
-    coor = random_coor(np.random.default_rng(4), shape, p_out=0.3)
-    plan = oracle.prepare_ref(coor, shape)
-    sch = _blocks.derive(plan, shape)
-    return shape, plan, sch
-
-
-def test_forward_scheduled_validation(lib):
-    """The header copy sizes the launch: a short workspace is EWORKSPACE and an
-    inconsistent header EINVAL, both before any HIP call."""
-    import _blocks
-    shape, plan, sch = _small_schedule()
-    s = bp.make_shape(shape)
-    hdr = [int(v) for v in sch["header"]]
-    slots = hdr[_blocks.HDR["slots"]]
-    assert slots > 0
-    need = slots * shape["C"] * 4
-    sb = _blocks.layout(shape, plan["n_valid"], plan["n_intervals"])["total"]
-
-    def f(header=hdr, **k):
-        h = bp._header(header) if header is not None else None
-        return lib.bevpool_forward_scheduled(ctypes.byref(k.get("shape", s)), k.get("i", 0), k.get("o", 0),
-                                             DUMMY, DUMMY, k.get("sc", DUMMY), k.get("sb", sb), h,
-                                             k.get("out", DUMMY), k.get("ws", DUMMY), k.get("wb", need),
-                                             None)
-
-    assert f(i=0, o=1) == EDTYPE
-    assert f(out=None) == EINVAL
-    assert f(header=None) == EINVAL
-    assert f(sc=None) == EINVAL
-    assert f(sb=sb - 1) == EINVAL
-    assert f(ws=None) == EWORKSPACE
-    assert f(wb=need - 1) == EWORKSPACE and "workspace" in lib.bevpool_last_error().decode()
-    for key, value in (("occ_found", hdr[4] - 1), ("max_ent", 8193), ("pieces", 0),
-                       ("slots", hdr[9] + 1), ("empty", hdr[6] + 1), ("pairs", plan["n_valid"] + 1)):
-        bad = list(hdr)
-        bad[_blocks.HDR[key]] = value
-        assert f(header=bad) == EINVAL, key
-    tall = bp.make_shape(dict(shape, H=171))
-    assert f(shape=tall) == EINVAL
-    n = ctypes.c_size_t(0)
-    assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), slots, ctypes.byref(n)) == OK
-    assert n.value == need
-
-
-def test_schedule_shape_limits(lib):
-    sb, wb = ctypes.c_size_t(), ctypes.c_size_t()
-    for kw in (dict(D=2049), dict(H=171)):
-        s = _shape(**kw)
-        assert lib.bevpool_schedule_size(ctypes.byref(s), 1000, 100, ctypes.byref(sb),
-                                         ctypes.byref(wb)) == EINVAL, kw
-    s = _shape(D=2048, H=170)
-    assert lib.bevpool_schedule_size(ctypes.byref(s), 1000, 100, ctypes.byref(sb), ctypes.byref(wb)) == OK

@@ -12,7 +12,7 @@ import pytest
 import torch
 
 import _gpu
-import _blocks
+import _sched
 import oracle
 from paper_2211_17111_amd import bevpool as bp
 from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
@@ -233,42 +233,39 @@ def test_forward_with_oracle_plan():
 
 
 def _check_schedule(coor, shape, label):
-    """Every array of the GPU-built schedule equals the numpy derivation from
-    the oracle's plan, bit for bit."""
     plan = _gpu.run_prepare(coor, shape)
     sched = bp.schedule(plan)
     ref_plan = oracle.prepare_ref(coor, shape)
-    want = _blocks.derive(ref_plan, shape)
-    got = _blocks.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
-    assert list(got["header"]) == [int(v) for v in want["header"]], (label, got["header"], want["header"])
-    for k, g in got.items():
-        w = np.asarray(want[k]).reshape(np.shape(g)).astype(np.int64)
-        if k in ("rec", "bp_dn"):
-            w = w & 0xFFFFFFFF
-        if k == "tc" and w.size:
-            w[:, 1] &= 0xFFFFFFFF
-        np.testing.assert_array_equal(g, w, err_msg=f"{label}: {k}")
-    return want, sched
+    got = _sched.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
+    # items are cut at one share per workgroup of this device's forward
+    assert got["n"]["shares"] >= 1, label
+    want = _sched.derive(ref_plan, shape, shares=got["n"]["shares"])
+    assert got["n"] == want["n"], (label, got["n"], want["n"])
+    for k in want:
+        if k != "n":
+            np.testing.assert_array_equal(got[k], want[k], err_msg=f"{label}: {k}")
+    return want
 
 
 @pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
 def test_schedule_matches_numpy(name):
+    """Every array of the GPU-built schedule against a numpy derivation from
+    the oracle's plan (integer data: bit-exact)."""
     cfg = CONFIGS[name]
     _gpu.say(f"schedule vs numpy: {name}")
-    want, _ = _check_schedule(frustum_coor(cfg), cfg.shape(), name)
+    want = _check_schedule(frustum_coor(cfg), cfg.shape(), name)
     if name == "headline":
-        # blocks of 12 cells over one column's rows: far fewer blocks than pairs
-        assert want["header"][_blocks.HDR["blocks"]] < 0.01 * want["header"][_blocks.HDR["pairs"]]
+        # a strip's pairs fall into few cells: far fewer segments than pairs
+        assert want["n"]["segs"] < 0.05 * want["n"]["pairs"]
 
 
 def test_schedule_edge_shapes():
     rng = np.random.default_rng(11)
     shapes = [
-        dict(B=2, N=2, D=9, H=7, W=13, C=17, X=12, Y=10, Z=2),   # W not a multiple of 4
+        dict(B=2, N=2, D=9, H=7, W=13, C=17, X=12, Y=10, Z=2),   # C not a multiple of 8
         dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1),   # few cells, many pairs
         dict(B=1, N=2, D=3, H=30, W=40, C=80, X=64, Y=64, Z=1),  # many cells of few pairs
         dict(B=3, N=1, D=4, H=5, W=6, C=16, X=300, Y=7, Z=3),    # X, Y far apart
-        dict(B=1, N=1, D=40, H=150, W=9, C=8, X=16, Y=16, Z=2),  # tall image: 12 TCs per piece
     ]
     for i, shape in enumerate(shapes):
         _gpu.say(f"schedule edge shape {i}: {shape}")
@@ -276,33 +273,13 @@ def test_schedule_edge_shapes():
     shape = shapes[1]
     P = shape["B"] * shape["N"] * shape["D"] * shape["H"] * shape["W"]
     one = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
-    want, _ = _check_schedule(one, shape, "one cell")
-    assert want["header"][_blocks.HDR["comb"]] == 1
+    want = _check_schedule(one, shape, "one cell")
+    assert want["n"]["comb"] == 1 and want["n"]["slots"] == want["n"]["items"]
     shape = dict(B=1, N=1, D=40, H=20, W=8, C=8, X=8, Y=8, Z=1)
     two = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (40 * 20 * 8, 1))
     two.reshape(shape["D"], -1, 3)[1::2, :, 0] = 5   # every point its own pair
-    want, _ = _check_schedule(two, shape, "two cells")
-    assert want["header"][_blocks.HDR["pairs"]] == 40 * 20 * 8
-
-
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline"])
-def test_forward_with_numpy_schedule(name):
-    """The scheduled forward driven by a schedule packed on the host from the
-    numpy derivation (not the GPU build): the kernels alone against the
-    oracle."""
-    cfg = CONFIGS[name]
-    _gpu.say(f"forward with a host-built schedule: {name}")
-    coor = frustum_coor(cfg)
-    data = draw_inputs(cfg, with_grad=False)
-    plan = _gpu.run_prepare(coor, cfg.shape())
-    ref_plan = oracle.prepare_ref(coor, cfg.shape())
-    want = _blocks.derive(ref_plan, cfg.shape())
-    buf = _blocks.pack(want, plan.n_valid, plan.n_intervals)
-    sched = bp.Schedule(plan, _gpu.to_dev(buf), [int(v) for v in want["header"]])
-    out = bp.forward_scheduled(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), sched)
-    torch.cuda.synchronize()
-    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
-    _gpu.assert_within(out.cpu().numpy(), ref, mag, cfg.dtype, name, log=True)
+    want = _check_schedule(two, shape, "two cells")
+    assert want["n"]["items"] > want["n"]["strips"]   # strips cut into several items
 
 
 def test_scheduled_matches_ranges():
@@ -318,6 +295,30 @@ def test_scheduled_matches_ranges():
     assert torch.equal(b, c)
     # both within float32 rounding of each other relative to the output scale
     assert float((a - b).abs().max()) <= 1e-4 * float(a.abs().max())
+
+
+@pytest.mark.parametrize("name", ["bevdet", "headline"])
+def test_scheduled_without_shares(name):
+    """A schedule whose items were not cut for this launch's workgroups (here:
+    its header says a share is too long) is walked with an equal count of
+    each die's items instead; only the balance changes, so the result is the
+    same bit for bit."""
+    import copy
+    cfg = CONFIGS[name]
+    _gpu.say(f"forward without shares: {name}")
+    data = draw_inputs(cfg, with_grad=False)
+    plan = _gpu.run_prepare(frustum_coor(cfg), cfg.shape())
+    sched = bp.schedule(plan)
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    want = bp.forward_scheduled(d, f, sched)
+    other = copy.copy(sched)
+    other.buffer = sched.buffer.clone()
+    hdr = other.buffer[:64].view(torch.int32)
+    assert int(hdr[_sched.HDR["shares_ok"]]) == 1
+    hdr[_sched.HDR["shares_ok"]] = 0
+    got = bp.forward_scheduled(d, f, other)
+    torch.cuda.synchronize()
+    assert torch.equal(got, want)
 
 
 def test_scheduled_workspace_reuse():
@@ -343,23 +344,27 @@ def test_scheduled_workspace_reuse():
         assert torch.equal(fresh, reused), t
 
 
-def test_scheduled_header_mismatch_nan():
-    """A header copy that is consistent with the shape but belongs to another
-    schedule: the device header differs, and every element of out is NaN
-    (defined, visible) instead of a silent wrong result."""
+def test_scheduled_small_workspace_nan():
+    """A workspace one slot short: the cell holding the last slot comes out
+    NaN and every other cell as with a full workspace."""
     cfg = CONFIGS["bevdet"]
     shape = cfg.shape()
-    rng = np.random.default_rng(6)
     data = draw_inputs(cfg, with_grad=False)
-    p1 = _gpu.run_prepare(frustum_coor(cfg), shape)
-    p2 = _gpu.run_prepare(random_coor(rng, shape, p_out=0.3), shape)
-    s1, s2 = bp.schedule(p1), bp.schedule(p2)
-    assert s1.counts != s2.counts
-    # schedule 1's buffer sized for whichever needs more, with schedule 2's header
-    n_need = max(s1.buffer.numel(), s2.buffer.numel())
-    buf = torch.zeros(n_need, dtype=torch.uint8, device=_gpu.DEV)
-    buf[:s1.buffer.numel()] = s1.buffer
-    mixed = bp.Schedule(p2, buf, s2.counts)
-    out = bp.forward_scheduled(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), mixed)
+    plan = _gpu.run_prepare(frustum_coor(cfg), shape)
+    sched = bp.schedule(plan)
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    full = bp.forward_scheduled(d, f, sched)
+    n = bp.bevpool_forward_scheduled_workspace_size(shape, sched.n_slots)
+    small = torch.zeros(n - 4 * shape["C"], dtype=torch.uint8, device=_gpu.DEV)
+    out = bp.forward_scheduled(d, f, sched, workspace=small)
     torch.cuda.synchronize()
-    assert bool(torch.isnan(out).all())
+    sch = _sched.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
+    comb, c0 = sch["comb_cell"], sch["comb_slot0"]
+    assert comb.size > 0
+    short = comb[c0[1:] > sched.n_slots - 1]  # cells whose slots the workspace lacks
+    assert short.size == 1
+    got, want = out.reshape(-1, shape["C"]).cpu(), full.reshape(-1, shape["C"]).cpu()
+    mask = torch.zeros(got.shape[0], dtype=torch.bool)
+    mask[torch.from_numpy(short)] = True
+    assert bool(torch.isnan(got[mask]).all())
+    assert torch.equal(got[~mask], want[~mask])

@@ -1,127 +1,279 @@
-"""The block schedule's definitions, executed on the CPU (no GPU).
+"""The strip schedule's definitions, executed on the CPU (no GPU).
 
-tests/_blocks.py derives the block schedule from the oracle's plan with numpy
-and executes it the way the scheduled forward does: dense weights from the
-depth runs of each piece's records, per-block sums of weights times feature
-rows, per-cell sums of column partials, then the slots of cells reached from
-several strips.  The result must equal the oracle's forward (section 2.1) to
-float64 rounding.  This pins the schedule's semantics (a wrong entry, record,
-block row range, partial-row index or slot order fails here) before the GPU
-build is compared with it bit for bit.
+tests/_sched.py derives the schedule from the oracle's plan with numpy; here a
+plain interpreter walks that schedule the way the scheduled forward does
+(strip rows addressed from the strip number, pair weights from depth runs,
+segments cut by head bits, direct stores versus slots, then the slot
+combination and the empty-cell fill) and the result must equal the oracle's
+forward (section 2.1) to float64 rounding.  This pins the schedule's
+semantics (a wrong strip geometry, pair run, segment cut or slot order fails
+here) before any GPU compares its buffers against it bit for bit.
 """
 
 import numpy as np
 import pytest
 
-import _blocks
+import _sched
 import oracle
 from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
 
 
-def _check(coor, shape, data, label):
+def _execute(sch, depth, feat, shape):
+    """Forward from a derived schedule, in float64; also counts the stores of
+    every output row."""
+    B, N, D, H, W, C = (shape[k] for k in "BNDHWC")
+    cells = B * shape["Z"] * shape["Y"] * shape["X"]
+    hw = H * W
+    sd = _sched.strip_dims(shape)
+    dflat = depth.reshape(-1).astype(np.float64)
+    fflat = feat.reshape(-1, C).astype(np.float64)
+    out = np.full((cells, C), np.nan)
+    writes = np.zeros(cells, dtype=np.int64)
+    slots = np.full((sch["n"]["slots"], C), np.nan)
+    per = sd["nhb"] * sd["nwb"]
+    for i in range(sch["n"]["items"]):
+        s = int(sch["item_strip"][i])
+        bn, r = divmod(s, per)
+        hb, wb = divmod(r, sd["nwb"])
+        h0, w0 = hb * sd["bh"], wb * sd["bw"]
+        bws = min(sd["bw"], W - w0)
+        npix = min(sd["bh"], H - h0) * bws
+        rows = [(bn * H + h0 + lp // bws) * W + w0 + lp % bws for lp in range(npix)]
+        p0, p1 = sch["item_pair0"][i], sch["item_pair0"][i + 1]
+        g0, g1 = sch["item_seg0"][i], sch["item_seg0"][i + 1]
+        assert 1 <= p1 - p0 <= _sched.ITEM_PAIRS
+        seg = -1
+        acc = {}
+        for k in range(p0, p1):
+            ln = int(sch["pair_ln"][k])
+            if ln & _sched.PAIR_HEAD:
+                seg += 1
+            assert k > p0 or ln & _sched.PAIR_HEAD
+            assert sch["pair_seg"][k] == seg
+            lp, n = ln & (_sched.PAIR_HEAD - 1), ln >> 16
+            assert lp < npix and n >= 1
+            rd0 = int(sch["pair_rd0"][k])
+            w = sum(dflat[rd0 + j * hw] for j in range(n))
+            acc[seg] = acc.get(seg, 0.0) + w * fflat[rows[lp]]
+        assert seg + 1 == g1 - g0
+        for j, v in acc.items():
+            dest = int(sch["seg_dest"][g0 + j])
+            if dest >= 0:
+                out[dest] = v
+                writes[dest] += 1
+            else:
+                assert np.isnan(slots[~dest]).all()
+                slots[~dest] = v
+    for j, cell in enumerate(sch["comb_cell"]):
+        a, b = sch["comb_slot0"][j], sch["comb_slot0"][j + 1]
+        assert b - a >= 2
+        out[cell] = slots[a:b].sum(axis=0)
+        writes[cell] += 1
+    out[sch["empty"]] = 0.0
+    writes[sch["empty"]] += 1
+    return out, writes
+
+
+def _check(depth, feat, coor, shape, label, shares=1):
     plan = oracle.prepare_ref(coor, shape)
-    sch = _blocks.derive(plan, shape)
-    got = _blocks.execute(sch, data["depth"], data["feat"])
-    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
-    err = np.abs(got - ref)
-    assert np.all(err <= 1e-12 * mag + 1e-300), f"{label}: max err {err.max():.3e}"
-    return plan, sch
+    sch = _sched.derive(plan, shape, shares=shares)
+    out, writes = _execute(sch, depth, feat, shape)
+    assert (writes == 1).all(), f"{label}: rows written {np.bincount(writes)} times"
+    ref, mag = oracle.forward_ref(depth, feat, coor, shape)
+    ref = ref.reshape(out.shape)
+    mag = mag.reshape(out.shape)
+    assert np.all(np.abs(out - ref) <= 1e-12 * mag + 1e-300), label
+    return sch
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet"])
-def test_schedule_executes_to_oracle(name):
-    cfg = CONFIGS[name]
-    _check(frustum_coor(cfg), cfg.shape(), draw_inputs(cfg), name)
-
-
-@pytest.mark.parametrize("seed", range(4))
-def test_schedule_random_shapes(seed):
-    rng = np.random.default_rng(100 + seed)
-    shapes = [dict(B=2, N=2, D=9, H=7, W=13, C=5, X=12, Y=10, Z=2),
-              dict(B=1, N=3, D=17, H=5, W=9, C=3, X=6, Y=6, Z=1),
-              dict(B=3, N=1, D=4, H=5, W=6, C=4, X=300, Y=7, Z=3),
-              dict(B=1, N=1, D=40, H=20, W=8, C=2, X=8, Y=8, Z=1)]
-    shape = shapes[seed]
-    coor = random_coor(rng, shape, p_out=0.3)
-    _check(coor, shape, draw_small(rng, shape), f"shape {seed}")
-
-
-def test_schedule_edge_cases():
-    shape = dict(B=1, N=1, D=8, H=50, W=60, C=3, X=8, Y=8, Z=1)
-    P = 8 * 50 * 60
-    rng = np.random.default_rng(2)
-    data = draw_small(rng, shape)
-    one = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
-    plan, sch = _check(one, shape, data, "one cell")
-    # one TC per strip, one slot per strip, one combined cell
-    assert sch["header"][_blocks.HDR["comb"]] == 1
-    assert sch["header"][_blocks.HDR["slots"]] == sch["header"][_blocks.HDR["tcs"]] == 15
-    single = np.full((P, 3), -1, dtype=np.int32)
-    single[1234] = [3, 3, 0]
-    _check(single, shape, data, "single point")
-    two = one.copy()
-    two.reshape(8, -1, 3)[1::2, :, 0] = 5   # every point its own pair
-    _, sch = _check(two, shape, data, "alternating cells")
-    assert sch["header"][_blocks.HDR["pairs"]] == P
-
-
-def test_schedule_invariants():
-    """Structural facts the kernels rely on (headline rig, bevdet shape)."""
-    cfg = CONFIGS["bevdet"]
-    shape = cfg.shape()
-    plan = oracle.prepare_ref(frustum_coor(cfg), shape)
-    s = _blocks.derive(plan, shape)
-    h = s["header"]
-    K, SW = _blocks.K, _blocks.SW
-    npairs = int(h[_blocks.HDR["pairs"]])
-    # every kept point lies in exactly one pair
-    assert int(s["pair_n"].sum()) == plan["n_valid"]
-    # pieces partition blocks, TCs, CCs and records in order
-    pc = s["piece"]
-    for col, ncol in ((5, 6), (7, 8), (9, 10), (11, 12)):
-        assert pc[0, col] == 0 and np.all(pc[1:, col] == pc[:-1, col] + pc[:-1, ncol])
-    assert pc[-1, 7] + pc[-1, 8] == npairs
-    assert np.all(pc[:, 10] <= _blocks.tc_max(shape["H"]))
-    assert np.all(pc[:, 13] <= _blocks.ENT_BUDGET) and np.all(pc[:, 12] <= 256)
-    # records address entries inside their piece's weight array
-    for j in range(len(pc)):
-        strip, plo, nh, dlo, nd, blk0, nblk, rec0, nrec, tc0, ntc, cc0, ncc, nent, pix0, ncol = pc[j]
-        recs = s["rec"][rec0:rec0 + nrec]
-        assert np.all((recs & 0x7FF) + ((recs >> 11) & 0x1FFF) < nd)
-        assert np.all((recs >> 24) < ncc)
-        cct = s["cc"][cc0:cc0 + ncc]
-        assert np.all((cct & 0xFFFF) < nent)
-        blocks = s["block"][blk0:blk0 + nblk]
-        assert np.all(blocks[:, 3] + K * blocks[:, 2] <= nent)
-        assert np.all(((blocks[:, 0] >> 8) & 0xFF) <= K)
-        prs = s["tc"][tc0:tc0 + ntc, 1]
-        for c in range(SW):
-            pr = (prs >> (8 * c)) & 0xFF
-            assert np.all((pr == 0xFF) | (pr < nblk * K))
-    # slots: the comb table lists each shared cell's slots contiguously
-    slots = int(h[_blocks.HDR["slots"]])
-    assert s["comb_slot0"][0] == 0 and s["comb_slot0"][-1] == slots
-    assert np.all(np.diff(s["comb_slot0"]) >= 2)
-    dest = s["tc"][:, 0]
-    assert np.array_equal(np.sort(~dest[dest < 0]), np.arange(slots))
-
-
-def test_schedule_mutant_caught():
-    """A planted mistake in how entries are addressed (row stride K - 1)
-    makes the executed schedule disagree with the oracle."""
+@pytest.mark.parametrize("shares", [1, 256])
+def test_schedule_model_tiny(shares):
     cfg = CONFIGS["tiny"]
-    shape = cfg.shape()
-    coor = frustum_coor(cfg)
-    data = draw_inputs(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "tiny", shares)
+    assert sch["n"]["slots"] == 0 or sch["n"]["comb"] > 0
+
+
+@pytest.mark.parametrize("shares", [1, 256])
+def test_schedule_model_bevdet_geometry(shares):
+    cfg = CONFIGS["bevdet"]
+    data = draw_inputs(cfg, with_grad=False)
+    sch = _check(data["depth"], data["feat"], frustum_coor(cfg), cfg.shape(), "bevdet", shares)
+    # pixel columns see few cells: far fewer segments than pairs
+    assert sch["n"]["segs"] < 0.25 * sch["n"]["pairs"]
+
+
+@pytest.mark.parametrize("shape", [
+    dict(B=2, N=2, D=9, H=7, W=13, C=17, X=12, Y=10, Z=2),
+    dict(B=1, N=1, D=8, H=100, W=60, C=80, X=8, Y=8, Z=1),    # strips cut in height
+    dict(B=1, N=2, D=3, H=30, W=40, C=300, X=64, Y=64, Z=1),  # one-pixel-wide strips
+    dict(B=3, N=1, D=4, H=5, W=6, C=16, X=300, Y=7, Z=3),
+])
+@pytest.mark.parametrize("shares", [1, 8, 1000])
+def test_schedule_model_random(shape, shares):
+    rng = np.random.default_rng(shape["C"])
+    data = draw_small(rng, shape)
+    _check(data["depth"], data["feat"], random_coor(rng, shape, p_out=0.3), shape, str(shape), shares)
+
+
+@pytest.mark.parametrize("shares", [1, 3, 8, 64, 5000])
+def test_shares_cut_items(shares):
+    # every share boundary starts an item, so share w's items hold exactly its
+    # pairs [floor(P w / S), floor(P (w + 1) / S)); items stay inside one strip
+    # and hold at most ITEM_PAIRS pairs
+    cfg = CONFIGS["bevdet"]
+    plan = oracle.prepare_ref(frustum_coor(cfg), cfg.shape())
+    sch = _sched.derive(plan, cfg.shape(), shares=shares)
+    P = sch["n"]["pairs"]
+    ip0 = sch["item_pair0"]
+    si = sch["share_item0"]
+    assert si.size == shares + 1 and si[0] == 0 and si[-1] == sch["n"]["items"]
+    s_p0 = np.r_[ip0[:-1][np.r_[True, sch["item_strip"][1:] != sch["item_strip"][:-1]]], P]
+    def bound(w):  # floor(P w / S), moved to a strip end closer than MIN_PIECE
+        c = (P * w) // shares
+        if 0 < c < P:
+            j = np.searchsorted(s_p0, c, side="right") - 1
+            a, b = s_p0[j], s_p0[j + 1]
+            c = a if c - a < _sched.MIN_PIECE else (b if b - c < _sched.MIN_PIECE else c)
+        return c
+    for w in range(shares):
+        lo, hi = bound(w), bound(w + 1)
+        assert lo <= hi
+        if lo < hi:
+            assert ip0[si[w]] == lo and ip0[si[w + 1]] == hi
+        else:
+            assert si[w] == si[w + 1]
+        assert hi - lo <= P // shares + 1 + 2 * _sched.MIN_PIECE
+    # a share cut inside a strip leaves at least MIN_PIECE pairs on each side
+    for w in range(1, shares):
+        c = bound(w)
+        j = np.searchsorted(s_p0, c, side="right") - 1
+        assert c == s_p0[j] or min(c - s_p0[j], s_p0[j + 1] - c) >= _sched.MIN_PIECE
+    assert np.all(np.diff(ip0) >= 1) and np.all(np.diff(ip0) <= _sched.ITEM_PAIRS)
+    # every strip starts an item
+    strip_p0 = ip0[:-1][np.r_[True, sch["item_strip"][1:] != sch["item_strip"][:-1]]]
+    base = _sched.derive(plan, cfg.shape(), shares=1)
+    assert np.array_equal(strip_p0, base["item_pair0"][:-1][np.r_[True, base["item_strip"][1:] !=
+                                                                   base["item_strip"][:-1]]])
+    assert sch["n"]["shares_ok"] == int(np.diff(si).max() <= _sched.SHARE_ITEMS)
+
+
+def test_schedule_model_one_cell():
+    # every point in one cell: strips of many pairs are cut into several items,
+    # so the cell has one slot per item
+    shape = dict(B=1, N=1, D=40, H=20, W=8, C=8, X=8, Y=8, Z=1)
+    rng = np.random.default_rng(5)
+    data = draw_small(rng, shape)
+    P = shape["D"] * shape["H"] * shape["W"]
+    coor = np.tile(np.array([[4, 2, 0]], dtype=np.int32), (P, 1))
+    # alternate two cells along depth so that every point is its own pair
+    coor.reshape(shape["D"], -1, 3)[1::2, :, 0] = 5
+    sch = _check(data["depth"], data["feat"], coor, shape, "one cell")
+    assert sch["n"]["items"] > sch["n"]["strips"]
+    assert sch["n"]["comb"] == 2
+
+
+def test_strip_dims_budget():
+    # a strip's rows of one 64-vector channel chunk fit the LDS budget
+    for C in (1, 16, 64, 80, 256, 300, 4096):
+        sd = _sched.strip_dims(dict(B=1, N=1, H=40, W=100, C=C))
+        assert sd["pixels"] * 4 * min(C, 256) <= _sched.STRIP_BYTES or sd["pixels"] == 1
+    sd = _sched.strip_dims(dict(B=1, N=6, H=40, W=100, C=80))
+    assert (sd["bh"], sd["bw"], sd["strips"]) == (40, 2, 300)
+
+
+def _walk_partition(sch, depth, feat, shape, G):
+    """The scheduled forward's in-item work split, executed on the CPU: an
+    item's pairs are cut into G equal ranges; a range sums its segments,
+    stores the ones it holds whole, keeps the part of a segment it starts
+    inside (handed to the range holding that segment's start) and of one it
+    ends inside (which then adds the following ranges' parts in order)."""
+    B, N, D, H, W, C = (shape[k] for k in "BNDHWC")
+    hw = H * W
+    cells = B * shape["Z"] * shape["Y"] * shape["X"]
+    sd = _sched.strip_dims(shape)
+    dflat = depth.reshape(-1).astype(np.float64)
+    fflat = feat.reshape(-1, C).astype(np.float64)
+    out = np.full((cells, C), np.nan)
+    slots = np.full((sch["n"]["slots"], C), np.nan)
+    per = sd["nhb"] * sd["nwb"]
+
+    def store(dest, v):
+        target = out[dest] if dest >= 0 else slots[~dest]
+        assert np.isnan(target).all()
+        target[:] = v
+
+    for i in range(sch["n"]["items"]):
+        s = int(sch["item_strip"][i])
+        bn, r = divmod(s, per)
+        hb, wb = divmod(r, sd["nwb"])
+        h0, w0 = hb * sd["bh"], wb * sd["bw"]
+        bws = min(sd["bw"], W - w0)
+        p0, p1 = sch["item_pair0"][i], sch["item_pair0"][i + 1]
+        np_ = p1 - p0
+        g0 = sch["item_seg0"][i]
+        ln = sch["pair_ln"][p0:p1]
+        head = (ln & _sched.PAIR_HEAD) != 0
+        seg = sch["pair_seg"][p0:p1]
+        lp = ln & (_sched.PAIR_HEAD - 1)
+        n = ln >> 16
+        rd0 = sch["pair_rd0"][p0:p1]
+        rows = (bn * H + h0 + lp // bws) * W + w0 + lp % bws
+        wts = np.array([sum(dflat[rd0[k] + j * hw] for j in range(n[k])) for k in range(np_)])
+        dest = sch["seg_dest"][g0:]
+        rb = lambda g: (g * np_) // G
+        first, last = {}, {}
+        for g in range(G):
+            kb, ke = rb(g), rb(g + 1)
+            if kb >= ke:
+                continue
+            prev_cont = not head[kb]
+            next_cont = ke < np_ and not head[ke]
+            cur, pend, acc = seg[kb], prev_cont, np.zeros(C)
+            for k in range(kb, ke):
+                if head[k] and k != kb:
+                    if pend:
+                        first[g], pend = acc, False
+                    else:
+                        store(dest[cur], acc)
+                    acc, cur = np.zeros(C), cur + 1
+                acc = acc + wts[k] * fflat[rows[k]]
+            if pend:
+                first[g] = acc
+            elif next_cont:
+                last[g] = (acc, seg[ke - 1])
+            else:
+                store(dest[cur], acc)
+        for g, (v, sg) in last.items():
+            total = v.copy()
+            for g2 in range(g + 1, G):
+                b2, e2 = rb(g2), rb(g2 + 1)
+                if b2 >= e2:
+                    continue
+                if head[b2]:
+                    break
+                total += first[g2]
+                if not (seg[e2 - 1] == sg and e2 < np_ and not head[e2]):
+                    break
+            store(dest[sg], total)
+    for j, c in enumerate(sch["comb_cell"]):
+        out[c] = slots[sch["comb_slot0"][j]:sch["comb_slot0"][j + 1]].sum(axis=0)
+    out[sch["empty"]] = 0.0
+    return out
+
+
+@pytest.mark.parametrize("G", [1, 7, 36, 64, 5000])
+def test_walk_partition_model(G):
+    # every output row written once and equal to the oracle, whatever the
+    # number of ranges (more ranges than pairs included)
+    shape = dict(B=1, N=2, D=12, H=6, W=5, C=8, X=6, Y=6, Z=1)
+    rng = np.random.default_rng(G)
+    data = draw_small(rng, shape)
+    coor = random_coor(rng, shape, p_out=0.2)
+    coor[::3, 0] = coor[0, 0]  # long segments across ranges
     plan = oracle.prepare_ref(coor, shape)
-    sch = _blocks.derive(plan, shape)
-    saved = _blocks.K
-    try:
-        _blocks.K = saved - 1
-        got = _blocks.execute(sch, data["depth"], data["feat"])
-    except (IndexError, ValueError):
-        return  # an out-of-range entry is caught too
-    finally:
-        _blocks.K = saved
-    ref, _ = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
-    assert not np.allclose(got, ref)
+    sch = _sched.derive(plan, shape)
+    out = _walk_partition(sch, data["depth"], data["feat"], shape, G)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
+    ref = ref.reshape(out.shape)
+    assert np.all(np.abs(out - ref) <= 1e-12 * mag.reshape(out.shape) + 1e-300)
