@@ -198,7 +198,7 @@ def main():
 
     def forward_strips(s):
         bp.bevpool_forward_scheduled(shape, code, ocode, s.depth, s.feat, s.sched, sched_bytes, nv, ni,
-                                     s.out, ws_fs, ws_fs_bytes, stream)
+                                     n_slots, s.out, ws_fs, ws_fs_bytes, stream)
 
     def forward_interval(s):
         bp.bevpool_forward(shape, code, ocode, s.depth, s.feat, s.rd, s.rf, s.rb, s.st, s.ln, nv, ni,

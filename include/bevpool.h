@@ -183,16 +183,18 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype,
  *
  * bevpool_forward_scheduled computes exactly what bevpool_forward computes
  * (same layouts, dtypes and zero-filled empty cells, every element of `out`
- * written once, no atomics, bitwise reproducible) from the schedule alone;
- * n_valid and n_intervals must be the values the schedule was built with.
- * Its workspace holds the slots: bevpool_forward_scheduled_workspace_size
- * bytes for the header's BEVPOOL_SCHEDULE_SLOTS count (float32 rows of C;
- * may be 0 bytes and NULL when that count is 0).  The workspace contents are
- * scratch: one forward at a time per workspace; the schedule is only read, so
- * concurrent forwards may share it.  The size cannot be checked without
- * reading the schedule: cells whose slots lie beyond a too small workspace
- * are written as NaN (nothing is written outside the workspace).  A schedule
- * whose cell count does not match n_intervals leaves `out` unwritten.
+ * written once, no atomics, bitwise reproducible) from the schedule alone.
+ * n_valid and n_intervals are the values the schedule was built with, and
+ * n_slots is its header's BEVPOOL_SCHEDULE_SLOTS count (read back once by
+ * the caller).  Its workspace holds the slots: at least
+ * bevpool_forward_scheduled_workspace_size(shape, n_slots) bytes (float32
+ * rows of C; may be 0 bytes and NULL when n_slots is 0), else
+ * BEVPOOL_EWORKSPACE before anything is enqueued.  The workspace contents
+ * are scratch: one forward at a time per workspace; the schedule is only
+ * read, so concurrent forwards may share it.  If the schedule's header does
+ * not hold these three counts (a schedule of another plan, or one not yet
+ * built), every element of `out` is written as NaN; nothing is read or
+ * written outside the schedule, the inputs, `out` and the workspace.
  */
 #define BEVPOOL_SCHEDULE_HEADER 16
 enum bevpool_schedule_count {
@@ -217,8 +219,8 @@ int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
                               size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
-                              void* out, void* workspace, size_t workspace_bytes,
-                              void* stream);
+                              int32_t n_slots, void* out, void* workspace,
+                              size_t workspace_bytes, void* stream);
 
 /*
  * Gradients of bevpool_forward (not in the paper; chain rule):

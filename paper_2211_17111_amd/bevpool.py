@@ -24,6 +24,9 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "bevpool.h")
 
 BEVPOOL_F32 = 0
 BEVPOOL_F16 = 1
+# status codes (enum bevpool_status)
+BEVPOOL_OK, BEVPOOL_EINVAL, BEVPOOL_EOVERFLOW, BEVPOOL_EDTYPE, BEVPOOL_EWORKSPACE, BEVPOOL_ELAUNCH = \
+    0, -1, -2, -3, -4, -5
 
 _DTYPE_CODE = {torch.float32: BEVPOOL_F32, torch.float16: BEVPOOL_F16}
 _CODE_DTYPE = {BEVPOOL_F32: torch.float32, BEVPOOL_F16: torch.float16}
@@ -76,7 +79,7 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_scheduled_workspace_size.restype = ctypes.c_int
     lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
-                                              vp, vp, sz, vp]
+                                              i32, vp, vp, sz, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -210,13 +213,13 @@ def bevpool_forward_scheduled_workspace_size(shape, n_slots) -> int:
 
 
 def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
-                              n_valid, n_intervals, out, workspace, workspace_bytes,
+                              n_valid, n_intervals, n_slots, out, workspace, workspace_bytes,
                               stream=None) -> None:
     lib = load_library()
     s = make_shape(shape)
     _check(lib, lib.bevpool_forward_scheduled(ctypes.byref(s), int(in_dtype), int(out_dtype), _ptr(depth),
                                               _ptr(feat), _ptr(schedule), int(schedule_bytes),
-                                              int(n_valid), int(n_intervals), _ptr(out),
+                                              int(n_valid), int(n_intervals), int(n_slots), _ptr(out),
                                               _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
 
@@ -387,8 +390,8 @@ def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, 
     if workspace is None:
         workspace = forward_scheduled_workspace(sched)
     bevpool_forward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, sched.buffer,
-                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, out, workspace,
-                              workspace.numel() * workspace.element_size(), stream)
+                              sched.buffer.numel(), plan.n_valid, plan.n_intervals, sched.n_slots, out,
+                              workspace, workspace.numel() * workspace.element_size(), stream)
     return out
 
 

@@ -258,7 +258,8 @@ int bevpool_forward_scheduled_workspace_size(const bevpool_shape* shape, int32_t
 int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
                               const void* depth, const void* feat, const void* schedule,
                               size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
-                              void* out, void* workspace, size_t workspace_bytes, void* stream) {
+                              int32_t n_slots, void* out, void* workspace, size_t workspace_bytes,
+                              void* stream) {
   bevpool::Dims d;
   int st = check_shape(shape, &d);
   if (st != BEVPOOL_OK) return st;
@@ -275,11 +276,16 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
     if (schedule_bytes < need)
       return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
                   schedule_bytes, need);
-    if (workspace == nullptr && workspace_bytes > 0)
-      return fail(BEVPOOL_EWORKSPACE, "workspace of %zu bytes at NULL", workspace_bytes);
+    // (each slot holds part of a cell's pairs, so there are at most n_valid)
+    if (n_slots < 0 || n_slots > n_valid)
+      return fail(BEVPOOL_EINVAL, "n_slots = %d outside [0, n_valid = %d]", n_slots, n_valid);
+    const size_t ws_need = bevpool::forward_scheduled_workspace_bytes(d, n_slots);
+    if (ws_need > 0 && (workspace == nullptr || workspace_bytes < ws_need))
+      return fail(BEVPOOL_EWORKSPACE, "%d slots need %zu workspace bytes, got %zu at %p", n_slots,
+                  ws_need, workspace_bytes, workspace);
   }
   return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, depth, feat, schedule,
-                                                    n_valid, n_intervals, out, workspace,
+                                                    n_valid, n_intervals, n_slots, out, workspace,
                                                     workspace_bytes,
                                                     static_cast<hipStream_t>(stream)),
                   "bevpool_forward_scheduled");

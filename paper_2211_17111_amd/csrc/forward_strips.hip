@@ -79,11 +79,18 @@ struct StripArgs {
   const int32_t* share_item0;
   float* slots;
   int64_t slot_cap;  // slots the workspace holds
-  int32_t n_valid, n_occ, items_cap;
+  int32_t n_valid, n_occ, n_slots, items_cap;  // counts the launch was sized from
   int32_t C, H, W, bh, bw, nhb, nwb, strips;
   int32_t hw32;    // H * W
   int64_t P, cells, n_empty;
 };
+
+// The schedule's header must hold the counts the launch was sized from.
+__device__ __forceinline__ bool header_ok(const StripArgs& a) {
+  const int32_t* hdr = a.hdr;
+  return hdr[kHdrOcc] == a.n_occ && hdr[kHdrOccFound] == a.n_occ && hdr[kHdrValid] == a.n_valid &&
+         hdr[kHdrSlots] == a.n_slots;
+}
 
 struct PairRec {
   float w;      // summed depth score
@@ -201,7 +208,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // (the share bounds are read with the counts; used only if they apply)
   const int32_t sh_lo = a.share_item0[min(w_idx, kMaxShares)];
   const int32_t sh_hi = a.share_item0[min(w_idx + 1, kMaxShares)];
-  if (hdr[kHdrOccFound] != a.n_occ || hdr[kHdrOcc] != a.n_occ) return;  // uniform
+  if (!header_ok(a)) return;  // (uniform; k_fwd_combine writes NaN everywhere)
   const int32_t n_items = min(hdr[kHdrItems], a.items_cap);
   const int32_t n_pairs = min(hdr[kHdrPairs], a.n_valid);
   const int32_t n_segs = min(hdr[kHdrSegs], a.n_valid);
@@ -684,7 +691,7 @@ template <typename TOut, int VEC>
 __global__ __launch_bounds__(kCombThreads) void k_fwd_combine(TOut* __restrict__ out,
                                                               StripArgs a) {
   const int32_t* hdr = a.hdr;
-  if (hdr[kHdrOccFound] != a.n_occ || hdr[kHdrOcc] != a.n_occ) return;
+  const bool ok = header_ok(a);
   const int lane = lane_id();
   const int C = a.C;
   const int CV = C / VEC;
@@ -695,6 +702,17 @@ __global__ __launch_bounds__(kCombThreads) void k_fwd_combine(TOut* __restrict__
   const int vi = lane - lg * cvc;
   if (lg >= gpw) return;
   const int64_t j = ((int64_t)blockIdx.x * (kCombThreads / kWave) + threadIdx.x / kWave) * gpw + lg;
+  if (!ok) {
+    // a schedule that does not hold the launch's counts: every cell is NaN
+    // (the grid has a lane group per cell and channel chunk)
+    if (j < a.cells) {
+      float nan[VEC];
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) nan[e] = __builtin_nanf("");
+      Vec<TOut, VEC>::store(out + j * C + (int64_t)(cbase + vi) * VEC, nan);
+    }
+    return;
+  }
   const int64_t n_comb = min(hdr[kHdrComb], a.n_occ);
   const int64_t n_empty = min<int64_t>(hdr[kHdrEmpty], a.n_empty);
   const int64_t col = (int64_t)(cbase + vi) * VEC;
@@ -814,8 +832,9 @@ size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots) {
 
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
-                                    int32_t n_valid, int32_t n_intervals, void* out,
-                                    void* workspace, size_t workspace_bytes, hipStream_t stream) {
+                                    int32_t n_valid, int32_t n_intervals, int32_t n_slots,
+                                    void* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream) {
   const bool al = aligned16(feat) && aligned16(out) && aligned16(workspace);
   const bool half_in = in_dtype == BEVPOOL_F16;
   const bool half_out = out_dtype == BEVPOOL_F16;
@@ -846,6 +865,7 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.slot_cap = workspace == nullptr ? 0 : (int64_t)(workspace_bytes / ((size_t)d.C * sizeof(float)));
   a.n_valid = n_valid;
   a.n_occ = n_intervals;
+  a.n_slots = n_slots;
   a.items_cap = (int32_t)L.items_cap;
   a.C = (int32_t)d.C;
   a.H = (int32_t)d.H;

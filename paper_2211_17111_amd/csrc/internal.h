@@ -148,8 +148,9 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
 size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots);
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
-                                    int32_t n_valid, int32_t n_intervals, void* out,
-                                    void* workspace, size_t workspace_bytes, hipStream_t stream);
+                                    int32_t n_valid, int32_t n_intervals, int32_t n_slots,
+                                    void* out, void* workspace, size_t workspace_bytes,
+                                    hipStream_t stream);
 
 // ---- forward ---------------------------------------------------------------
 size_t forward_workspace_bytes(const Dims& d);

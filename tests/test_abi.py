@@ -11,6 +11,16 @@ import pytest
 from paper_2211_17111_amd import bevpool as bp
 
 OK, EINVAL, EOVERFLOW, EDTYPE, EWORKSPACE, ELAUNCH = 0, -1, -2, -3, -4, -5
+
+
+def test_status_constants_match_header():
+    """The binding's status constants are the header's enum values."""
+    import re
+    src = open(bp.HEADER_PATH).read()
+    enum = dict((m.group(1), int(m.group(2))) for m in re.finditer(r"(BEVPOOL_E?[A-Z]+) = (-?\d+)", src))
+    for name in ("BEVPOOL_OK", "BEVPOOL_EINVAL", "BEVPOOL_EOVERFLOW", "BEVPOOL_EDTYPE", "BEVPOOL_EWORKSPACE",
+                 "BEVPOOL_ELAUNCH"):
+        assert getattr(bp, name) == enum[name], name
 DUMMY = 0x1000  # non-NULL, never dereferenced: every call below fails validation first
 
 SHAPE = dict(B=1, N=6, D=118, H=40, W=100, C=80, X=128, Y=128, Z=1)
@@ -166,15 +176,21 @@ def test_schedule_validation(lib):
     assert call(sb=sb.value - 1) == EINVAL
     assert call(ws=None) == EWORKSPACE
     assert call(wb=wb.value - 1) == EWORKSPACE
+    need = 10 * s.C * 4  # ten slots
     f = lambda **k: lib.bevpool_forward_scheduled(ctypes.byref(s), k.get("i", 0), k.get("o", 0), DUMMY, DUMMY,
                                                   k.get("sc", DUMMY), k.get("sb", sb.value), 1000, 100,
-                                                  k.get("out", DUMMY), k.get("ws", DUMMY),
-                                                  k.get("wb", 1024), None)
+                                                  k.get("ns", 10), k.get("out", DUMMY), k.get("ws", DUMMY),
+                                                  k.get("wb", need), None)
     assert f(i=0, o=1) == EDTYPE
     assert f(sc=None) == EINVAL
     assert f(sb=16) == EINVAL
     assert f(out=None) == EINVAL
+    # the slot count the caller read from the header sizes the workspace
+    assert f(ns=-1) == EINVAL
+    assert f(ns=1001) == EINVAL  # (more slots than kept points)
     assert f(ws=None) == EWORKSPACE
+    assert f(wb=need - 1) == EWORKSPACE
+    assert f(ns=11) == EWORKSPACE
     n = ctypes.c_size_t(0)
     assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), 10, ctypes.byref(n)) == OK
     assert n.value == 10 * s.C * 4

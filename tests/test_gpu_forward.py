@@ -344,27 +344,51 @@ def test_scheduled_workspace_reuse():
         assert torch.equal(fresh, reused), t
 
 
-def test_scheduled_small_workspace_nan():
-    """A workspace one slot short: the cell holding the last slot comes out
-    NaN and every other cell as with a full workspace."""
+def test_scheduled_workspace_checked():
+    """A workspace smaller than the schedule's slot count needs is refused
+    with BEVPOOL_EWORKSPACE before anything is enqueued: `out` keeps its
+    contents."""
     cfg = CONFIGS["bevdet"]
     shape = cfg.shape()
     data = draw_inputs(cfg, with_grad=False)
     plan = _gpu.run_prepare(frustum_coor(cfg), shape)
     sched = bp.schedule(plan)
     d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
-    full = bp.forward_scheduled(d, f, sched)
     n = bp.bevpool_forward_scheduled_workspace_size(shape, sched.n_slots)
-    small = torch.zeros(n - 4 * shape["C"], dtype=torch.uint8, device=_gpu.DEV)
-    out = bp.forward_scheduled(d, f, sched, workspace=small)
+    assert n > 0
+    small = torch.zeros(n - 4, dtype=torch.uint8, device=_gpu.DEV)
+    out = torch.full((cfg.B, cfg.Z, cfg.Y, cfg.X, cfg.C), 7.0, device=_gpu.DEV)
+    with pytest.raises(bp.BevpoolError) as err:
+        bp.forward_scheduled(d, f, sched, out=out, workspace=small)
+    assert err.value.status == bp.BEVPOOL_EWORKSPACE
     torch.cuda.synchronize()
-    sch = _sched.decode(sched.buffer.cpu().numpy(), shape, plan.n_valid, plan.n_intervals)
-    comb, c0 = sch["comb_cell"], sch["comb_slot0"]
-    assert comb.size > 0
-    short = comb[c0[1:] > sched.n_slots - 1]  # cells whose slots the workspace lacks
-    assert short.size == 1
-    got, want = out.reshape(-1, shape["C"]).cpu(), full.reshape(-1, shape["C"]).cpu()
-    mask = torch.zeros(got.shape[0], dtype=torch.bool)
-    mask[torch.from_numpy(short)] = True
-    assert bool(torch.isnan(got[mask]).all())
-    assert torch.equal(got[~mask], want[~mask])
+    assert bool((out == 7.0).all())
+
+
+@pytest.mark.parametrize("case", ["slots", "unbuilt"])
+def test_scheduled_header_mismatch_nan(case):
+    """A schedule whose header does not hold the counts of the call (another
+    slot count, or a buffer no build has written) gives NaN in every element
+    of `out`, never a partial or stale result."""
+    cfg = CONFIGS["bevdet"]
+    shape = cfg.shape()
+    data = draw_inputs(cfg, with_grad=False)
+    plan = _gpu.run_prepare(frustum_coor(cfg), shape)
+    sched = bp.schedule(plan)
+    d, f = _gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"])
+    n_slots = sched.n_slots
+    buf = sched.buffer
+    if case == "slots":
+        n_slots += 1
+    else:
+        buf = torch.zeros_like(sched.buffer)
+    ws = torch.empty(bp.bevpool_forward_scheduled_workspace_size(shape, n_slots) + 16, dtype=torch.uint8,
+                     device=_gpu.DEV)
+    out = torch.zeros((cfg.B, cfg.Z, cfg.Y, cfg.X, cfg.C), device=_gpu.DEV)
+    code = bp.BEVPOOL_F32
+    bp.bevpool_forward_scheduled(shape, code, code, d, f, buf, buf.numel(), plan.n_valid, plan.n_intervals,
+                                 n_slots, out, ws, ws.numel())
+    torch.cuda.synchronize()
+    assert bool(torch.isnan(out).all())
+
+

@@ -38,7 +38,7 @@ def test_graph_replays_match_eager():
     sb, wb = bp.bevpool_schedule_size(shape, nv, ni)
     sched = torch.empty(sb, dtype=torch.uint8, device=dev)
     ws_s = torch.empty(wb, dtype=torch.uint8, device=dev)
-    n_slots = bp.schedule(plan).n_slots
+    n_slots = bp.schedule(plan).n_slots  # (the header, read back once before capture)
     fb = bp.bevpool_forward_scheduled_workspace_size(shape, n_slots)
     ws_f = torch.empty(max(fb, 16), dtype=torch.uint8, device=dev)
     out = torch.empty((cfg.B, cfg.Z, cfg.Y, cfg.X, cfg.C), dtype=torch.float32, device=dev)
@@ -48,7 +48,8 @@ def test_graph_replays_match_eager():
     def run():  # everything on the current stream
         bp.bevpool_prepare(shape, coor, rd, rf, rb, st, ln, cnt, ws_p, ws_p.numel())
         bp.bevpool_schedule(shape, rd, rb, nv, ni, sched, sb, ws_s, ws_s.numel())
-        bp.bevpool_forward_scheduled(shape, code, code, depth, feat, sched, sb, nv, ni, out, ws_f, fb)
+        bp.bevpool_forward_scheduled(shape, code, code, depth, feat, sched, sb, nv, ni, n_slots, out,
+                                     ws_f, fb)
         bp.bevpool_backward_scheduled(shape, code, code, grad_out, depth, feat, sched, sb, nv, ni, gd, gf)
 
     # (the plan and schedule arrays are written only up to their counts: every
