@@ -223,6 +223,27 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                               size_t workspace_bytes, void* stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc):
+ * bevpool_forward_scheduled without a workspace.  The slots live in a
+ * static device array of BEVPOOL_NOALLOC_SCRATCH_BYTES bytes that the
+ * library holds on each device it runs on from the first call there until
+ * the process ends; nothing is allocated or freed by the call (the first
+ * call on a device looks the array's address up).  Arguments, results and
+ * errors as bevpool_forward_scheduled, except that a schedule whose n_slots
+ * float32 rows of C exceed BEVPOOL_NOALLOC_SCRATCH_BYTES is refused with
+ * BEVPOOL_EWORKSPACE.  Every call on a device uses the same array: calls
+ * that may overlap on one device (on different streams, or from different
+ * threads without ordering) race and give undefined results.
+ */
+#define BEVPOOL_NOALLOC_SCRATCH_BYTES (32u << 20)
+int bevpool_forward_scheduled_noalloc(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                                      const void* depth, const void* feat, const void* schedule,
+                                      size_t schedule_bytes, int32_t n_valid,
+                                      int32_t n_intervals, int32_t n_slots, void* out,
+                                      void* stream);
+
+/*
  * Gradients of bevpool_forward (not in the paper; chain rule):
  *   grad_depth[p]  = sum_c grad_out[rank_bev(p), c] * feat[rank_feat(p), c]
  *                    for a kept point p, and +0.0 for a dropped point;

@@ -24,6 +24,7 @@ HEADER_PATH = os.path.join(os.path.dirname(_PKG), "include", "bevpool.h")
 
 BEVPOOL_F32 = 0
 BEVPOOL_F16 = 1
+NOALLOC_SCRATCH_BYTES = 32 << 20  # BEVPOOL_NOALLOC_SCRATCH_BYTES
 # status codes (enum bevpool_status)
 BEVPOOL_OK, BEVPOOL_EINVAL, BEVPOOL_EOVERFLOW, BEVPOOL_EDTYPE, BEVPOOL_EWORKSPACE, BEVPOOL_ELAUNCH = \
     0, -1, -2, -3, -4, -5
@@ -80,6 +81,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
                                               i32, vp, vp, sz, vp]
+    lib.bevpool_forward_scheduled_noalloc.restype = ctypes.c_int
+    lib.bevpool_forward_scheduled_noalloc.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32,
+                                                      i32, i32, vp, vp]
     lib.bevpool_backward_workspace_size.restype = ctypes.c_int
     lib.bevpool_backward_workspace_size.argtypes = [shp, ctypes.POINTER(sz)]
     lib.bevpool_backward.restype = ctypes.c_int
@@ -222,6 +226,17 @@ def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule,
                                               int(n_valid), int(n_intervals), int(n_slots), _ptr(out),
                                               _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
+
+
+def bevpool_forward_scheduled_noalloc(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
+                                      n_valid, n_intervals, n_slots, out, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_forward_scheduled_noalloc(ctypes.byref(s), int(in_dtype), int(out_dtype),
+                                                      _ptr(depth), _ptr(feat), _ptr(schedule),
+                                                      int(schedule_bytes), int(n_valid), int(n_intervals),
+                                                      int(n_slots), _ptr(out), _stream(stream)),
+           "bevpool_forward_scheduled_noalloc")
 
 
 def bevpool_backward_workspace_size(shape) -> int:

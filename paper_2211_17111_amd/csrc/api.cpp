@@ -91,6 +91,44 @@ int from_hip(hipError_t e, const char* what) {
   return fail(BEVPOOL_ELAUNCH, "%s: %s (%s)", what, hipGetErrorName(e), hipGetErrorString(e));
 }
 
+int check_counts(const bevpool::Dims& d, int32_t n_valid, int32_t n_intervals) {
+  if (n_valid < 0 || n_valid > d.P)
+    return fail(BEVPOOL_EINVAL, "n_valid = %d outside [0, %lld]", n_valid, (long long)d.P);
+  const int64_t cap = d.P < d.cells ? d.P : d.cells;
+  if (n_intervals < 0 || n_intervals > cap || n_intervals > n_valid ||
+      (n_valid > 0 && n_intervals == 0))
+    return fail(BEVPOOL_EINVAL, "n_intervals = %d inconsistent with n_valid = %d (cells %lld)",
+                n_intervals, n_valid, (long long)d.cells);
+  return BEVPOOL_OK;
+}
+
+// Checks shared by the two scheduled forwards (everything but the workspace).
+int check_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                            const void* depth, const void* feat, const void* schedule,
+                            size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                            int32_t n_slots, void* out, bevpool::Dims* d) {
+  int st = check_shape(shape, d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_dtypes(in_dtype, out_dtype);
+  if (st != BEVPOOL_OK) return st;
+  st = check_counts(*d, n_valid, n_intervals);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(out);
+  if (n_intervals > 0) {
+    REQUIRE_PTR(depth);
+    REQUIRE_PTR(feat);
+    REQUIRE_PTR(schedule);
+    const size_t need = bevpool::schedule_layout(*d, n_valid, n_intervals).total;
+    if (schedule_bytes < need)
+      return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
+                  schedule_bytes, need);
+    // (each slot holds part of a cell's pairs, so there are at most n_valid)
+    if (n_slots < 0 || n_slots > n_valid)
+      return fail(BEVPOOL_EINVAL, "n_slots = %d outside [0, n_valid = %d]", n_slots, n_valid);
+  }
+  return BEVPOOL_OK;
+}
+
 }  // namespace
 
 extern "C" {
@@ -190,17 +228,6 @@ int bevpool_forward(const bevpool_shape* shape, int in_dtype, int out_dtype, con
                   "bevpool_forward");
 }
 
-static int check_counts(const bevpool::Dims& d, int32_t n_valid, int32_t n_intervals) {
-  if (n_valid < 0 || n_valid > d.P)
-    return fail(BEVPOOL_EINVAL, "n_valid = %d outside [0, %lld]", n_valid, (long long)d.P);
-  const int64_t cap = d.P < d.cells ? d.P : d.cells;
-  if (n_intervals < 0 || n_intervals > cap || n_intervals > n_valid ||
-      (n_valid > 0 && n_intervals == 0))
-    return fail(BEVPOOL_EINVAL, "n_intervals = %d inconsistent with n_valid = %d (cells %lld)",
-                n_intervals, n_valid, (long long)d.cells);
-  return BEVPOOL_OK;
-}
-
 int bevpool_schedule_size(const bevpool_shape* shape, int32_t n_valid, int32_t n_intervals,
                           size_t* schedule_bytes, size_t* workspace_bytes) {
   bevpool::Dims d;
@@ -261,24 +288,10 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                               int32_t n_slots, void* out, void* workspace, size_t workspace_bytes,
                               void* stream) {
   bevpool::Dims d;
-  int st = check_shape(shape, &d);
+  int st = check_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule,
+                                   schedule_bytes, n_valid, n_intervals, n_slots, out, &d);
   if (st != BEVPOOL_OK) return st;
-  st = check_dtypes(in_dtype, out_dtype);
-  if (st != BEVPOOL_OK) return st;
-  st = check_counts(d, n_valid, n_intervals);
-  if (st != BEVPOOL_OK) return st;
-  REQUIRE_PTR(out);
   if (n_intervals > 0) {
-    REQUIRE_PTR(depth);
-    REQUIRE_PTR(feat);
-    REQUIRE_PTR(schedule);
-    const size_t need = bevpool::schedule_layout(d, n_valid, n_intervals).total;
-    if (schedule_bytes < need)
-      return fail(BEVPOOL_EINVAL, "schedule of %zu bytes is smaller than the %zu this plan needs",
-                  schedule_bytes, need);
-    // (each slot holds part of a cell's pairs, so there are at most n_valid)
-    if (n_slots < 0 || n_slots > n_valid)
-      return fail(BEVPOOL_EINVAL, "n_slots = %d outside [0, n_valid = %d]", n_slots, n_valid);
     const size_t ws_need = bevpool::forward_scheduled_workspace_bytes(d, n_slots);
     if (ws_need > 0 && (workspace == nullptr || workspace_bytes < ws_need))
       return fail(BEVPOOL_EWORKSPACE, "%d slots need %zu workspace bytes, got %zu at %p", n_slots,
@@ -289,6 +302,31 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                                                     workspace_bytes,
                                                     static_cast<hipStream_t>(stream)),
                   "bevpool_forward_scheduled");
+}
+
+int bevpool_forward_scheduled_noalloc(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                                      const void* depth, const void* feat, const void* schedule,
+                                      size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,
+                                      int32_t n_slots, void* out, void* stream) {
+  bevpool::Dims d;
+  int st = check_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule,
+                                   schedule_bytes, n_valid, n_intervals, n_slots, out, &d);
+  if (st != BEVPOOL_OK) return st;
+  const size_t ws_need =
+      n_intervals > 0 ? bevpool::forward_scheduled_workspace_bytes(d, n_slots) : 0;
+  if (ws_need > bevpool::kNoAllocScratchBytes)
+    return fail(BEVPOOL_EWORKSPACE,
+                "%d slots need %zu bytes; the allocation-free forward holds at most %zu "
+                "(use bevpool_forward_scheduled with a workspace)",
+                n_slots, ws_need, bevpool::kNoAllocScratchBytes);
+  void* scratch = nullptr;
+  st = from_hip(bevpool::forward_noalloc_scratch(&scratch), "bevpool_forward_scheduled_noalloc");
+  if (st != BEVPOOL_OK) return st;
+  return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, depth, feat, schedule,
+                                                    n_valid, n_intervals, n_slots, out, scratch,
+                                                    bevpool::kNoAllocScratchBytes,
+                                                    static_cast<hipStream_t>(stream)),
+                  "bevpool_forward_scheduled_noalloc");
 }
 
 int bevpool_backward_workspace_size(const bevpool_shape* shape, size_t* bytes) {

@@ -39,6 +39,8 @@
 #include "vec.h"
 
 #include <algorithm>
+#include <atomic>
+#include <mutex>
 #include <type_traits>
 
 namespace bevpool {
@@ -889,6 +891,42 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   }
   if (vec == 8) return run<half_t, float, 8>(d, L.sd, depth, feat, a, out, stream);
   return run<half_t, float, 1>(d, L.sd, depth, feat, a, out, stream);
+}
+
+// ---- allocation-free forward: the slots live in a file-scope device array.
+// Each device holds its own copy from the first call on it until the
+// process ends; every call on a device shares it.
+namespace {
+
+static __device__ __align__(256) float scratch[kNoAllocScratchBytes / sizeof(float)];
+
+constexpr int kMaxDevices = 64;
+std::atomic<void*> g_scratch_addr[kMaxDevices];
+std::mutex g_scratch_mu;
+
+}  // namespace
+
+hipError_t forward_noalloc_scratch(void** addr) {
+  *addr = nullptr;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  void* p = g_scratch_addr[dev].load(std::memory_order_acquire);
+  if (p == nullptr) {
+    // (once per device, with that device current: the array's device
+    // address; in host code `scratch` itself is only a stand-in)
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    p = g_scratch_addr[dev].load(std::memory_order_acquire);
+    if (p == nullptr) {
+      e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+      if (e != hipSuccess) return e;
+      if (p == nullptr) return hipErrorInvalidSymbol;
+      g_scratch_addr[dev].store(p, std::memory_order_release);
+    }
+  }
+  *addr = p;
+  return hipSuccess;
 }
 
 }  // namespace bevpool

@@ -146,6 +146,11 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
                            hipStream_t stream);
 // Float32 workspace rows of the scheduled forward: one per slot.
 size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots);
+// bevpool_forward_scheduled_noalloc: the slots in a static device array of
+// this many bytes; its device address on the current device (looked up on
+// the first call per device)
+constexpr size_t kNoAllocScratchBytes = BEVPOOL_NOALLOC_SCRATCH_BYTES;
+hipError_t forward_noalloc_scratch(void** addr);
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
                                     int32_t n_valid, int32_t n_intervals, int32_t n_slots,

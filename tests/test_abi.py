@@ -42,6 +42,7 @@ def test_exports_every_declared_symbol(lib):
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
         "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
         "bevpool_forward_scheduled", "bevpool_forward_scheduled_workspace_size",
+        "bevpool_forward_scheduled_noalloc",
         "bevpool_backward_workspace_size", "bevpool_backward", "bevpool_backward_scheduled",
     }
     for n in names:
@@ -191,6 +192,17 @@ def test_schedule_validation(lib):
     assert f(ws=None) == EWORKSPACE
     assert f(wb=need - 1) == EWORKSPACE
     assert f(ns=11) == EWORKSPACE
+    # the allocation-free forward: the same checks, and a bound on the slots
+    g = lambda **k: lib.bevpool_forward_scheduled_noalloc(ctypes.byref(s), k.get("i", 0), k.get("o", 0), DUMMY,
+                                                          DUMMY, k.get("sc", DUMMY), k.get("sb", sb.value),
+                                                          1000, 100, k.get("ns", 10), k.get("out", DUMMY),
+                                                          None)
+    assert g(i=0, o=1) == EDTYPE
+    assert g(sc=None) == EINVAL
+    assert g(sb=16) == EINVAL
+    assert g(out=None) == EINVAL
+    assert g(ns=-1) == EINVAL
+    assert g(ns=1001) == EINVAL
     n = ctypes.c_size_t(0)
     assert lib.bevpool_forward_scheduled_workspace_size(ctypes.byref(s), 10, ctypes.byref(n)) == OK
     assert n.value == 10 * s.C * 4
@@ -204,3 +216,20 @@ def test_schedule_validation(lib):
     assert b(sc=None) == EINVAL
     assert b(sb=16) == EINVAL
     assert b(gf=None) == EINVAL
+
+
+def test_noalloc_scratch_bound():
+    """The allocation-free forward refuses, before any HIP call, a schedule
+    whose slots exceed its static array, and the binding's constant is the
+    header's."""
+    import re
+    src = open(bp.HEADER_PATH).read()
+    m = re.search(r"#define BEVPOOL_NOALLOC_SCRATCH_BYTES \((\d+)u << (\d+)\)", src)
+    assert m and bp.NOALLOC_SCRATCH_BYTES == int(m.group(1)) << int(m.group(2))
+    lib = bp.load_library()
+    s = bp.make_shape(dict(B=1, N=1, D=64, H=16, W=16, C=1024, X=64, Y=64, Z=1))
+    n_slots = bp.NOALLOC_SCRATCH_BYTES // (1024 * 4) + 1  # one slot more than fits
+    st = lib.bevpool_forward_scheduled_noalloc(ctypes.byref(s), 0, 0, DUMMY, DUMMY, DUMMY, 1 << 40, 16384, 4096,
+                                               n_slots, DUMMY, None)
+    assert st == EWORKSPACE
+    assert "allocation-free" in bp.bevpool_last_error()
