@@ -51,7 +51,9 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     global _lib
     if _lib is not None and path is None:
         return _lib
-    p = path or LIB_PATH
+    # (BEVPOOL_LIBRARY names another build of the same ABI, e.g. the
+    # host-sanitizer build the ABI tests run against)
+    p = path or os.environ.get("BEVPOOL_LIBRARY") or LIB_PATH
     if not os.path.exists(p):
         raise RuntimeError(f"{p} not found: build it with paper_2211_17111_amd.build.build()")
     lib = ctypes.CDLL(p)

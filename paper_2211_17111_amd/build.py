@@ -48,8 +48,25 @@ def _run(cmd, verbose):
         print(out, flush=True)
 
 
+def remove_stale_objects() -> list[str]:
+    """Delete objects in the build folder that no source in SOURCES produces
+    (left by renamed or deleted sources), so the folder holds only what the
+    library links."""
+    keep = {os.path.splitext(src)[0] + ".o" for src in SOURCES}
+    removed = []
+    if os.path.isdir(BUILD):
+        for name in sorted(os.listdir(BUILD)):
+            if name.endswith(".o") and name not in keep:
+                os.remove(os.path.join(BUILD, name))
+                removed.append(name)
+    return removed
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
+    for name in remove_stale_objects():
+        if verbose:
+            print(f"removed stale {name}", flush=True)
     cc = hipcc()
 
     def compile_one(src):
@@ -64,6 +81,54 @@ def build(verbose: bool = False) -> str:
     _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
     return LIB_PATH
+
+
+SAN_DIR = os.path.join(BUILD, "asan")
+SAN_LIB = os.path.join(SAN_DIR, "libbevpool_asan.so")
+# AddressSanitizer and UndefinedBehaviorSanitizer on the host code only (the
+# device code is compiled as usual)
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-fno-omit-frame-pointer", "-g"]
+
+
+def sanitizer_runtime() -> str:
+    """The compiler's AddressSanitizer runtime, preloaded into a process that
+    loads the sanitized library."""
+    rocm = os.environ.get("ROCM_PATH", "/opt/rocm")
+    res = subprocess.run([os.path.join(rocm, "llvm", "bin", "clang"),
+                          "-print-file-name=libclang_rt.asan-x86_64.so"],
+                         stdout=subprocess.PIPE, text=True)
+    path = res.stdout.strip()
+    if not os.path.isabs(path):  # (newer layouts name it per target)
+        res = subprocess.run([os.path.join(rocm, "llvm", "bin", "clang"), "-print-runtime-dir"],
+                             stdout=subprocess.PIPE, text=True)
+        path = os.path.join(res.stdout.strip(), "libclang_rt.asan.so")
+    return path
+
+
+def build_sanitized(verbose: bool = False) -> str:
+    """The same library with host-side ASan/UBSan instrumentation, for the
+    ABI tests' argument-validation paths (no GPU needed).  Rebuilt only when
+    a source or header is newer than it."""
+    os.makedirs(SAN_DIR, exist_ok=True)
+    inputs = [os.path.join(CSRC, f) for f in os.listdir(CSRC)] + [os.path.join(INCLUDE, "bevpool.h")]
+    if os.path.exists(SAN_LIB) and os.path.getmtime(SAN_LIB) >= max(map(os.path.getmtime, inputs)):
+        return SAN_LIB
+    cc = hipcc()
+    flags = [f if f != "-O3" else "-O1" for f in COMMON] + SAN_FLAGS
+
+    def compile_one(src):
+        obj = os.path.join(SAN_DIR, os.path.splitext(src)[0] + ".o")
+        lang = ["-x", "hip"] if src.endswith(".hip") else []
+        _run([cc, *flags, *lang, "-c", os.path.join(CSRC, src), "-o", obj], verbose)
+        return obj
+
+    with ThreadPoolExecutor(max_workers=min(4, len(SOURCES))) as ex:
+        objs = list(ex.map(compile_one, SOURCES))
+    tmp = SAN_LIB + ".tmp"
+    _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *SAN_FLAGS, *objs, "-o", tmp], verbose)
+    os.replace(tmp, SAN_LIB)
+    return SAN_LIB
 
 
 if __name__ == "__main__":
