@@ -16,8 +16,11 @@ launches (mean and percentiles are reported beside it).  The achieved
 bandwidth divides the algorithmic bytes of one forward by that latency.
 --forward picks the entry point timed as the metric (interval-table or
 strip-schedule forward); the other one is timed the same way and reported
-beside it.  So is a plain device copy that reads and writes the same number
-of bytes: the bandwidth one launch of this size reaches at best.
+beside it.  So is a hand-written streaming kernel (stream_probe.hip, a
+library of its own) that reads the forward's algorithmic read bytes and
+writes its output bytes: the bandwidth one launch of this size and mix
+reaches.  The other four workloads' cold forward and backward medians are
+reported in `detail` (--other-workloads).
 
 The CPU baseline is the float64 oracle timed on the host: whole forwards of
 the same workload, repeated until a minimum CPU time is spent, reported as the
@@ -58,14 +61,42 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
-def forward_min_bytes(cfg, n_valid, n_intervals) -> int:
-    """Algorithmic HBM bytes of one forward: depth of kept points, the whole
-    feature once, two ranks per kept point, start/length/cell per interval,
-    and every output element once."""
+def forward_read_bytes(cfg, n_valid, n_intervals) -> int:
+    """Algorithmic HBM bytes one forward reads: depth of kept points, the
+    whole feature once, two ranks per kept point, start/length/cell per
+    interval."""
     s_in = 4 if cfg.dtype == "f32" else 2
-    s_out = 4 if cfg.out_dtype == "f32" else 2
     feat = cfg.B * cfg.N * cfg.H * cfg.W * cfg.C
-    return s_in * n_valid + s_in * feat + 8 * n_valid + 12 * n_intervals + s_out * cfg.cells * cfg.C
+    return s_in * n_valid + s_in * feat + 8 * n_valid + 12 * n_intervals
+
+
+def forward_write_bytes(cfg) -> int:
+    """Algorithmic HBM bytes one forward writes: every output element once."""
+    s_out = 4 if cfg.out_dtype == "f32" else 2
+    return s_out * cfg.cells * cfg.C
+
+
+def forward_min_bytes(cfg, n_valid, n_intervals) -> int:
+    """Algorithmic HBM bytes of one forward (reads and writes)."""
+    return forward_read_bytes(cfg, n_valid, n_intervals) + forward_write_bytes(cfg)
+
+
+def schedule_min_bytes(n_valid, schedule_bytes) -> int:
+    """Algorithmic HBM bytes of one schedule build: the plan's depth and BEV
+    ranks of the kept points read once, the schedule written once."""
+    return 8 * n_valid + schedule_bytes
+
+
+def cpu_model() -> str:
+    """The host CPU's model name (/proc/cpuinfo), else what platform knows."""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return platform.processor() or platform.machine()
 
 
 def prepare_min_bytes(cfg, n_valid, n_intervals) -> int:
@@ -119,6 +150,75 @@ class BufferSet:
         return sum(t.numel() * t.element_size() for t in vars(self).values() if isinstance(t, torch.Tensor))
 
 
+def _cold(n, pick, fn, stream):
+    """Per-launch HIP event pairs on `stream` over n launches (after a short
+    warm-up), and the back-to-back region per launch."""
+    for i in range(min(n, 8)):
+        fn(pick(i))
+    torch.cuda.synchronize()
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
+    for i in range(n):
+        ev[i][0].record(stream)
+        fn(pick(i))
+        ev[i][1].record(stream)
+    torch.cuda.synchronize()
+    per = np.array([a.elapsed_time(b) for a, b in ev])
+    r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    r0.record(stream)
+    for i in range(n):
+        fn(pick(i))
+    r1.record(stream)
+    torch.cuda.synchronize()
+    return per, r0.elapsed_time(r1) / n
+
+
+def measure_workload(name, dev, stream, launches=48, nsets=6) -> dict:
+    """Cold forward and backward (scheduled entry points) of another workload:
+    the median per-launch latency over `launches` launches cycling `nsets`
+    independent input/output sets, and the back-to-back region."""
+    cfg = CONFIGS[name]
+    shape = cfg.shape()
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg)
+    plan = bp.prepare(torch.from_numpy(coor).to(dev), shape)
+    sched = bp.schedule(plan)
+    ws = bp.forward_scheduled_workspace(sched)
+    code = bp.BEVPOOL_F32 if cfg.dtype == "f32" else bp.BEVPOOL_F16
+    ocode = bp.BEVPOOL_F32 if cfg.out_dtype == "f32" else bp.BEVPOOL_F16
+    odt = torch.float32 if cfg.out_dtype == "f32" else torch.float16
+    sets = []
+    for _ in range(nsets):
+        depth = torch.from_numpy(data["depth"]).to(dev)
+        feat = torch.from_numpy(data["feat"]).to(dev)
+        sets.append(dict(depth=depth, feat=feat, grad_out=torch.from_numpy(data["grad_out"]).to(dev),
+                         out=torch.empty((cfg.B, cfg.Z, cfg.Y, cfg.X, cfg.C), dtype=odt, device=dev),
+                         gd=torch.empty_like(depth), gf=torch.empty_like(feat)))
+    nv, ni = plan.n_valid, plan.n_intervals
+    sb = sched.buffer.numel()
+
+    def fwd(t):
+        bp.bevpool_forward_scheduled(shape, code, ocode, t["depth"], t["feat"], sched.buffer, sb, nv, ni,
+                                     sched.n_slots, t["out"], ws, ws.numel(), stream)
+
+    def bwd(t):
+        bp.bevpool_backward_scheduled(shape, code, ocode, t["grad_out"], t["depth"], t["feat"], sched.buffer,
+                                      sb, nv, ni, t["gd"], t["gf"], stream)
+
+    pf, rf = _cold(launches, lambda i: sets[i % nsets], fwd, stream)
+    pb, rb = _cold(launches, lambda i: sets[i % nsets], bwd, stream)
+    fb, bb = forward_min_bytes(cfg, nv, ni), backward_min_bytes(cfg, nv, ni)
+    fms, bms = float(np.median(pf)), float(np.median(pb))
+    return {"config": f"B={cfg.B} N={cfg.N} H={cfg.H} W={cfg.W} D={cfg.D} C={cfg.C} "
+                      f"BEV {cfg.X}x{cfg.Y}x{cfg.Z} {cfg.dtype}->{cfg.out_dtype}",
+            "n_valid": nv, "n_intervals": ni,
+            "forward_ms": fms, "forward_region_ms_per_launch": rf, "forward_bytes": fb,
+            "forward_gbs": round(fb / (fms * 1e-3) / 1e9, 1),
+            "backward_ms": bms, "backward_region_ms_per_launch": rb, "backward_bytes": bb,
+            "backward_gbs": round(bb / (bms * 1e-3) / 1e9, 1),
+            "launches": launches, "rotating_sets": nsets,
+            "time": "median of per-launch HIP events, cold (rotating sets)"}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -137,6 +237,9 @@ def main():
                          "bevpool_backward_scheduled")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also launch one plain 256 MiB device copy (hardware-counter calibration)")
+    ap.add_argument("--other-workloads", default="tiny,bevdet,large,train",
+                    help="workloads whose cold forward and backward medians are reported in detail "
+                         "('' for none)")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -255,6 +358,8 @@ def main():
     plan_gbs = plan_bytes / (plan_ms * 1e-3) / 1e9
     log(f"prepare {plan_ms * 1e3:.1f} us ({plan_bytes / 1e6:.2f} MB -> {plan_gbs:.0f} GB/s), "
         f"schedule build {sched_ms * 1e3:.1f} us")
+    sched_min = schedule_min_bytes(nv, sched_bytes)
+    sched_gbs = sched_min / (sched_ms * 1e-3) / 1e9
     bwd_bytes = backward_min_bytes(cfg, nv, ni)
     bwd_gbs = bwd_bytes / (bwd_ms * 1e-3) / 1e9
     step_ms = float(np.mean([e[0].elapsed_time(e[3]) for e in evs]))
@@ -306,20 +411,43 @@ def main():
         f"{cold.mean() * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
         f"{warm.mean() * 1e3:.2f} us; {min_bytes / 1e6:.2f} MB -> {achieved:.0f} GB/s")
 
-    # ---- the achievable ceiling at this size: a plain device copy (torch's
-    # copy kernel) that reads and writes the forward's algorithmic bytes, timed
-    # the same way (cold: as many buffer pairs as sets, cycled)
-    half = (min_bytes // 2 + 255) // 256 * 256
-    pairs = [(torch.empty(half, dtype=torch.uint8, device=dev), torch.empty(half, dtype=torch.uint8, device=dev))
-             for _ in range(len(sets))]
-    copy_cold, _ = timed_forwards(args.fwd_launches, lambda i: pairs[i % len(pairs)],
-                                  lambda pr: pr[1].copy_(pr[0]))
-    host_us.pop()  # (the copy's enqueue time is not the forward's)
+    # ---- the achievable ceiling at this size and mix: a hand-written
+    # streaming kernel (a library of its own, not the product) that reads the
+    # forward's algorithmic read bytes and writes its output bytes, timed the
+    # same way (cold: as many buffer pairs as sets, cycled)
+    import ctypes
+    from paper_2211_17111_amd import build as pbuild
+    probe = ctypes.CDLL(pbuild.PROBE_LIB)
+    probe.bevpool_probe_stream.restype = ctypes.c_int
+    probe.bevpool_probe_stream.argtypes = [ctypes.c_void_p, ctypes.c_size_t, ctypes.c_void_p,
+                                           ctypes.c_size_t, ctypes.c_void_p]
+    rd_bytes = (forward_read_bytes(cfg, nv, ni) + 15) // 16 * 16
+    wr_bytes = (forward_write_bytes(cfg) + 15) // 16 * 16
+    pairs = [(torch.ones(rd_bytes // 4, dtype=torch.float32, device=dev),
+              torch.empty(wr_bytes // 4, dtype=torch.float32, device=dev)) for _ in range(len(sets))]
+
+    def stream_mix(pr):
+        st = probe.bevpool_probe_stream(pr[0].data_ptr(), rd_bytes, pr[1].data_ptr(), wr_bytes,
+                                        stream.cuda_stream)
+        if st != 0:
+            raise RuntimeError(f"bevpool_probe_stream failed ({st})")
+
+    copy_cold, copy_region = timed_forwards(args.fwd_launches, lambda i: pairs[i % len(pairs)], stream_mix)
+    host_us.pop()  # (the probe's enqueue time is not the forward's)
     copy_ms = float(np.median(copy_cold))
-    copy_gbs = 2 * half / (copy_ms * 1e-3) / 1e9
+    copy_gbs = (rd_bytes + wr_bytes) / (copy_ms * 1e-3) / 1e9
+    copy_region_gbs = (rd_bytes + wr_bytes) / (copy_region * 1e-3) / 1e9
     del pairs
-    log(f"copy of the same bytes ({2 * half / 1e6:.2f} MB read + written), cold median "
-        f"{copy_ms * 1e3:.2f} us -> {copy_gbs:.0f} GB/s ({copy_gbs / HBM_PEAK_GBS * 100:.1f}% of peak)")
+    log(f"stream probe with the forward's mix ({rd_bytes / 1e6:.2f} MB read, {wr_bytes / 1e6:.2f} MB "
+        f"written), cold median {copy_ms * 1e3:.2f} us -> {copy_gbs:.0f} GB/s "
+        f"({copy_gbs / HBM_PEAK_GBS * 100:.1f}% of peak); back-to-back {copy_region * 1e3:.2f} us/launch")
+
+    others = {}
+    for name in [w for w in args.other_workloads.split(",") if w and w != cfg.name]:
+        others[name] = measure_workload(name, dev, stream)
+        o = others[name]
+        log(f"{name}: forward cold median {o['forward_ms'] * 1e3:.2f} us ({o['forward_gbs']:.0f} GB/s), "
+            f"backward cold median {o['backward_ms'] * 1e3:.2f} us ({o['backward_gbs']:.0f} GB/s)")
 
     traffic = None
     if os.path.exists(PMC_FILE):
@@ -349,7 +477,7 @@ def main():
                "sample": f"{reps} full forwards of this workload by oracle.forward_ref (float64, "
                          f"materialised frustum + np.add.at, single-threaded numpy), {spent:.1f} s "
                          f"in total; value is the mean per forward",
-               "host_cpu_count": os.cpu_count(), "host_cpu": platform.processor() or platform.machine()}
+               "host_cpu_count": os.cpu_count(), "host_cpu": cpu_model()}
         log(f"cpu oracle: {reps} forwards in {spent:.1f} s -> {cpu['value']} ms per forward")
 
     if args.copy_calibration:
@@ -388,8 +516,11 @@ def main():
                                 "launches": int(cold.size), "rotating_sets": len(sets),
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
             "forward_cold_region_ms_per_launch": cold_region,
-            "copy_same_bytes_cold": {"p50_ms": copy_ms, "gbs": round(copy_gbs, 1), "bytes": 2 * half,
-                                     "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4)},
+            "stream_probe_same_mix_cold": {
+                "p50_ms": copy_ms, "gbs": round(copy_gbs, 1), "read_bytes": rd_bytes,
+                "write_bytes": wr_bytes, "frac_of_peak": round(copy_gbs / HBM_PEAK_GBS, 4),
+                "region_ms_per_launch": copy_region, "region_gbs": round(copy_region_gbs, 1),
+                "kernel": "k_stream_mix (stream_probe.hip, libbevpool_probe.so)"},
             "forward_warm_ms": float(warm.mean()),
             "forward_host_enqueue_us": host_us,
             "forward_warm_region_ms_per_launch": warm_region,
@@ -400,6 +531,11 @@ def main():
             f"forward_{other_name}_cold_region_ms_per_launch": cold_oth_region,
             "prepare_ms": prep_ms, "forward_in_step_ms": fwd_in_step_ms, "backward_ms": bwd_ms,
             "prepare_only_ms": plan_ms, "schedule_build_ms": sched_ms,
+            "schedule_roofline": {"algorithmic_bytes": sched_min, "achieved_gbs": round(sched_gbs, 1),
+                                  "peak_gbs": HBM_PEAK_GBS, "frac": round(sched_gbs / HBM_PEAK_GBS, 4),
+                                  "schedule_bytes": sched_bytes,
+                                  "time": "mean over the steps of the step's schedule build (HIP events)"},
+            "other_workloads": others,
             "prepare_roofline": {"algorithmic_bytes": plan_bytes, "achieved_gbs": round(plan_gbs, 1),
                                  "peak_gbs": HBM_PEAK_GBS, "frac": round(plan_gbs / HBM_PEAK_GBS, 4),
                                  "time": "mean over the steps of the step's prepare (HIP events)"},

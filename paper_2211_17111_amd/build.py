@@ -22,6 +22,9 @@ LIB_PATH = os.path.join(PKG, LIB_NAME)
 
 ARCH = "gfx950"
 SOURCES = ["prepare.hip", "forward.hip", "forward_strips.hip", "backward.hip", "api.cpp"]
+# measurement probe for bench.py, built into a library of its own
+PROBE_SOURCE = "stream_probe.hip"
+PROBE_LIB = os.path.join(PKG, "libbevpool_probe.so")
 
 # No fast-math and no flush-to-zero on the GPU path; packed fp32 ops off.
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -52,7 +55,7 @@ def remove_stale_objects() -> list[str]:
     """Delete objects in the build folder that no source in SOURCES produces
     (left by renamed or deleted sources), so the folder holds only what the
     library links."""
-    keep = {os.path.splitext(src)[0] + ".o" for src in SOURCES}
+    keep = {os.path.splitext(src)[0] + ".o" for src in SOURCES + [PROBE_SOURCE]}
     removed = []
     if os.path.isdir(BUILD):
         for name in sorted(os.listdir(BUILD)):
@@ -80,6 +83,11 @@ def build(verbose: bool = False) -> str:
     tmp = LIB_PATH + ".tmp"
     _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp], verbose)
     os.replace(tmp, LIB_PATH)
+    # the measurement probe, a library of its own (bench.py loads it)
+    pobj = os.path.join(BUILD, "stream_probe.o")
+    _run([cc, *COMMON, "-x", "hip", "-c", os.path.join(CSRC, PROBE_SOURCE), "-o", pobj], verbose)
+    _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", pobj, "-o", PROBE_LIB + ".tmp"], verbose)
+    os.replace(PROBE_LIB + ".tmp", PROBE_LIB)
     return LIB_PATH
 
 
