@@ -237,7 +237,7 @@ def main():
                          "bevpool_backward_scheduled")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="also launch one plain 256 MiB device copy (hardware-counter calibration)")
-    ap.add_argument("--other-workloads", default="tiny,bevdet,large,train",
+    ap.add_argument("--other-workloads", default="tiny,bevdet,large,train,voxel3d",
                     help="workloads whose cold forward and backward medians are reported in detail "
                          "('' for none)")
     args = ap.parse_args()

@@ -247,7 +247,7 @@ def _check_schedule(coor, shape, label):
     return want
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train", "voxel3d"])
 def test_schedule_matches_numpy(name):
     """Every array of the GPU-built schedule against a numpy derivation from
     the oracle's plan (integer data: bit-exact)."""

@@ -1,8 +1,9 @@
-"""Every output element at the three largest workloads against the oracle.
+"""Every output element at the four largest workloads against the oracle.
 
 The headline (6 views, 40x100, D=118, C=80, fp32), large (4 samples,
-40x110, D=118, fp16 in and out, 256x256 grid) and train (8 samples, 16x44,
-D=118, fp32) workloads are compared over the whole output: the forward of
+40x110, D=118, fp16 in and out, 256x256 grid), train (8 samples, 16x44,
+D=118, fp32) and voxel3d (the headline rig into a 128x128x16 voxel grid)
+workloads are compared over the whole output: the forward of
 both the interval-table path and the scheduled path, and grad_depth and
 grad_feat of both backward paths, each element within
 tol * sum|terms| + 1e-6 of the float64 oracle (section 2.1: the
@@ -23,7 +24,7 @@ from workloads import CONFIGS, draw_inputs, frustum_coor
 
 pytestmark = pytest.mark.gpu
 
-NAMES = ["headline", "large", "train"]
+NAMES = ["headline", "large", "train", "voxel3d"]
 _CACHE: dict = {}
 
 

@@ -10,7 +10,7 @@ from workloads import CONFIGS, frustum_coor, random_coor
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train", "voxel3d"])
 def test_prepare_configs(name):
     cfg = CONFIGS[name]
     _gpu.say(f"prepare parity: {name} P={cfg.P}")

@@ -16,6 +16,29 @@ def test_config_sizes():
     assert CONFIGS["large"].X == 256 and CONFIGS["large"].P == 12_460_800
     assert CONFIGS["train"].P == 3_987_456
     assert CONFIGS["bevdet"].P == 249_216
+    v = CONFIGS["voxel3d"]
+    assert (v.X, v.Y, v.Z, v.P, v.cells) == (128, 128, 16, 2_832_000, 262_144)
+
+
+def test_voxel3d_height_slices():
+    """Camera 0, feature row h = 19 (centre v = 312 px, 8 px above the
+    principal point at 320): a ray at elevation atan(8 / f) climbs from
+    1.5 m by 8/f per metre of depth, f = 800 / tan(35 deg) = 1142.5 px; over
+    1..59.5 m that stays in [1.5, 1.92] m, inside the slice [1.5, 2.0) m,
+    index floor((z + 5) / 0.5) = 13.  Row h = 20 (8 px below) descends from
+    1.5 m into [1.08, 1.5) m, index 12."""
+    cfg = CONFIGS["voxel3d"]
+    per_view = cfg.D * cfg.H * cfg.W
+    c = frustum_coor(cfg)[:per_view].reshape(cfg.D, cfg.H, cfg.W, 3)
+    ext = np.array([cfg.X, cfg.Y, cfg.Z])
+    inside = np.all((c >= 0) & (c < ext), axis=-1)
+    for h, iz in ((19, 13), (20, 12)):
+        kept = inside[:, h, :]
+        assert kept.any()
+        assert np.all(c[:, h, :, 2][kept] == iz), (h, np.unique(c[:, h, :, 2][kept]))
+    # points inside the grid fill all 16 slices
+    zs = c[..., 2][inside]
+    assert np.array_equal(np.unique(zs), np.arange(16))
 
 
 def test_hand_evaluated_point_tiny():

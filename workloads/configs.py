@@ -104,6 +104,12 @@ CONFIGS: dict[str, Config] = {
                     D=118, depth_start=1.0, depth_step=0.5, C=80,
                     dtype="f16", out_dtype="f16",
                     xy_lo=-51.2, xy_hi=51.2, xy_res=0.4, seed=3),
+    # The headline rig into a 3-D voxel grid: z over [-5, 3) m in 0.5 m
+    # slices, so 128x128x16 cells.
+    "voxel3d": Config(name="voxel3d", B=1, N=6, img_h=640, img_w=1600, stride=16,
+                      D=118, depth_start=1.0, depth_step=0.5, C=80,
+                      dtype="f32", out_dtype="f32",
+                      xy_lo=-51.2, xy_hi=51.2, xy_res=0.8, z_res=0.5, seed=5),
     # Training batch: eight samples at 256x704, D=118, C=80.
     "train": Config(name="train", B=8, N=6, img_h=256, img_w=704, stride=16,
                     D=118, depth_start=1.0, depth_step=0.5, C=80,
