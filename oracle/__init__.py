@@ -19,6 +19,9 @@ from .bevpool_ref import (
     forward_cells_ref,
     grad_depth_points_ref,
     grad_feat_pixels_ref,
+    depth_lse_ref,
+    depth_softmax_ref,
+    forward_softmax_ref,
 )
 
 __all__ = [
@@ -31,4 +34,7 @@ __all__ = [
     "forward_cells_ref",
     "grad_depth_points_ref",
     "grad_feat_pixels_ref",
+    "depth_lse_ref",
+    "depth_softmax_ref",
+    "forward_softmax_ref",
 ]

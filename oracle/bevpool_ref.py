@@ -236,3 +236,35 @@ def grad_feat_pixels_ref(grad_out: np.ndarray, depth: np.ndarray, coor: np.ndarr
         val[i] = t.sum(axis=0)
         mag[i] = np.abs(t).sum(axis=0)
     return val, mag
+
+
+# ---- depth scores from logits (the fused depth-softmax forward) -----------
+#
+# Section 2.1, paragraph 1 takes the depth score (N, D, H, W) as each pixel's
+# distribution over its D depth classes.  When a network gives logits, the
+# distribution is their softmax over the depth axis.  The reading here: the
+# softmax is taken per (b, n, h, w) over d, in float64 from the given
+# (possibly rounded) logits, and the forward is then exactly forward_ref on
+# those scores.
+
+
+def depth_lse_ref(logits: np.ndarray) -> np.ndarray:
+    """Log-sum-exp over the depth axis of logits (B, N, D, H, W): (B, N, H, W).
+
+    Computed as m + log(sum exp(logit - m)) with m the largest logit of the
+    pixel, so no term overflows."""
+    x = np.asarray(logits, dtype=_F64)
+    m = x.max(axis=2, keepdims=True)
+    return (m + np.log(np.exp(x - m).sum(axis=2, keepdims=True)))[:, :, 0]
+
+
+def depth_softmax_ref(logits: np.ndarray) -> np.ndarray:
+    """Depth scores exp(logit - lse) (B, N, D, H, W): per pixel, a
+    distribution over the depth bins."""
+    x = np.asarray(logits, dtype=_F64)
+    return np.exp(x - depth_lse_ref(x)[:, :, None])
+
+
+def forward_softmax_ref(logits: np.ndarray, feat: np.ndarray, coor: np.ndarray, shape: dict):
+    """forward_ref with the depth scores of depth_softmax_ref(logits)."""
+    return forward_ref(depth_softmax_ref(logits), feat, coor, shape)

@@ -31,8 +31,11 @@ def _softmax_depth(logits: np.ndarray) -> np.ndarray:
     return e / e.sum(axis=1, keepdims=True)
 
 
-def draw_inputs(cfg: Config, seed: int | None = None, with_grad: bool = True) -> dict:
-    """Depth (B,N,D,H,W), feat (B,N,H,W,C) and grad_out (B,Z,Y,X,C)."""
+def draw_inputs(cfg: Config, seed: int | None = None, with_grad: bool = True,
+                with_logits: bool = False) -> dict:
+    """Depth (B,N,D,H,W), feat (B,N,H,W,C) and grad_out (B,Z,Y,X,C); with
+    with_logits also the depth logits (B,N,D,H,W) the scores were drawn
+    from, rounded to the working precision."""
     rng = np.random.default_rng(cfg.seed if seed is None else seed)
     dt = _NP_DTYPE[cfg.dtype]
     odt = _NP_DTYPE[cfg.out_dtype]
@@ -41,13 +44,19 @@ def draw_inputs(cfg: Config, seed: int | None = None, with_grad: bool = True) ->
     depth = np.empty((B, N, D, H, W), dtype=dt)
     feat = np.empty((B, N, H, W, C), dtype=dt)
     grad = np.empty((B, Z, Y, X, C), dtype=odt) if with_grad else None
+    lg = np.empty((B, N, D, H, W), dtype=dt) if with_logits else None
     for b in range(B):
         logits = 3.0 * rng.standard_normal((N, D, H, W))
         depth[b] = _softmax_depth(logits).astype(dt)
+        if with_logits:
+            lg[b] = logits.astype(dt)
         feat[b] = rng.standard_normal((N, H, W, C)).astype(dt)
         if with_grad:
             grad[b] = rng.standard_normal((Z, Y, X, C)).astype(odt)
-    return {"depth": depth, "feat": feat, "grad_out": grad}
+    out = {"depth": depth, "feat": feat, "grad_out": grad}
+    if with_logits:
+        out["logits"] = lg
+    return out
 
 
 def draw_small(rng: np.random.Generator, shape: dict, dtype: str = "f32",
