@@ -442,6 +442,40 @@ def main():
         f"written), cold median {copy_ms * 1e3:.2f} us -> {copy_gbs:.0f} GB/s "
         f"({copy_gbs / HBM_PEAK_GBS * 100:.1f}% of peak); back-to-back {copy_region * 1e3:.2f} us/launch")
 
+    # ---- fused depth softmax: the per-pixel log-sum-exp pre-pass, then the
+    # scheduled forward from the logits (scores formed on the fly)
+    lg_data = draw_inputs(cfg, with_grad=False, with_logits=True)
+    nlg = 4
+    lg = [torch.from_numpy(lg_data["logits"]).to(dev) for _ in range(nlg)]
+    lses = [torch.empty((cfg.B, cfg.N, cfg.H, cfg.W), dtype=torch.float64, device=dev) for _ in range(nlg)]
+    del lg_data
+
+    def lse_pass(i):
+        bp.bevpool_depth_lse(shape, code, lg[i], lses[i], stream)
+
+    def fused_fwd(i):
+        s_ = sets[i % len(sets)]
+        bp.bevpool_forward_scheduled_softmax(shape, code, ocode, lg[i], lses[i], s_.feat, s_.sched, sched_bytes,
+                                             nv, ni, n_slots, s_.out, ws_fs, ws_fs_bytes, stream)
+
+    for i in range(nlg):
+        lse_pass(i)
+    lse_per, lse_region = _cold(64, lambda i: i % nlg, lse_pass, stream)
+    sm_per, sm_region = _cold(64, lambda i: i % nlg, fused_fwd, stream)
+    s_in = 4 if cfg.dtype == "f32" else 2
+    lse_bytes = s_in * cfg.P + 8 * cfg.B * cfg.N * cfg.H * cfg.W
+    sm_bytes = forward_min_bytes(cfg, nv, ni) + 8 * cfg.B * cfg.N * cfg.H * cfg.W
+    fused = {"lse_ms": float(np.median(lse_per)), "lse_region_ms_per_launch": lse_region,
+             "lse_bytes": lse_bytes, "lse_gbs": round(lse_bytes / (float(np.median(lse_per)) * 1e-3) / 1e9, 1),
+             "forward_ms": float(np.median(sm_per)), "forward_region_ms_per_launch": sm_region,
+             "forward_bytes": sm_bytes,
+             "forward_gbs": round(sm_bytes / (float(np.median(sm_per)) * 1e-3) / 1e9, 1),
+             "note": "bevpool_depth_lse then bevpool_forward_scheduled_softmax (logits in, scores formed on the "
+                     "fly); medians of per-launch HIP events over 4 rotating logit sets"}
+    del lg, lses
+    log(f"fused softmax: lse pre-pass {fused['lse_ms'] * 1e3:.2f} us ({fused['lse_gbs']:.0f} GB/s), forward from "
+        f"logits {fused['forward_ms'] * 1e3:.2f} us")
+
     others = {}
     for name in [w for w in args.other_workloads.split(",") if w and w != cfg.name]:
         others[name] = measure_workload(name, dev, stream)
@@ -536,6 +570,7 @@ def main():
                                   "schedule_bytes": sched_bytes,
                                   "time": "mean over the steps of the step's schedule build (HIP events)"},
             "other_workloads": others,
+            "fused_softmax": fused,
             "prepare_roofline": {"algorithmic_bytes": plan_bytes, "achieved_gbs": round(plan_gbs, 1),
                                  "peak_gbs": HBM_PEAK_GBS, "frac": round(plan_gbs / HBM_PEAK_GBS, 4),
                                  "time": "mean over the steps of the step's prepare (HIP events)"},

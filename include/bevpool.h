@@ -223,6 +223,33 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                               size_t workspace_bytes, void* stream);
 
 /*
+ * Fused depth softmax (section 2.1: a pixel's depth score is a distribution
+ * over its D depth bins).  When the scores come from logits, the score of
+ * point (b, n, d, h, w) is exp(logit[b,n,d,h,w] - lse[b,n,h,w]) with
+ * lse[b,n,h,w] = log sum_d exp(logit[b,n,d,h,w]).
+ *
+ * bevpool_depth_lse reads logits (B, N, D, H, W; in_dtype) and writes lse
+ * (B, N, H, W; float64, caller's device memory): one double per pixel,
+ * m + log(sum exp(logit - m)) with m the pixel's largest logit.
+ *
+ * bevpool_forward_scheduled_softmax is bevpool_forward_scheduled with the
+ * depth scores formed on the fly from the logits and that lse (exponent in
+ * double, the device library's float32 expf), so the (B, N, D, H, W) score
+ * tensor is never written or read.  Arguments, workspace, results and
+ * errors as bevpool_forward_scheduled; lse may be NULL only when
+ * n_intervals is 0.  Logits must be finite.  There is no fused backward:
+ * a training step materialises the scores and uses bevpool_backward_scheduled.
+ */
+int bevpool_depth_lse(const bevpool_shape* shape, int in_dtype, const void* logits, double* lse,
+                      void* stream);
+int bevpool_forward_scheduled_softmax(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                                      const void* logits, const double* lse, const void* feat,
+                                      const void* schedule, size_t schedule_bytes,
+                                      int32_t n_valid, int32_t n_intervals, int32_t n_slots,
+                                      void* out, void* workspace, size_t workspace_bytes,
+                                      void* stream);
+
+/*
  * For callers that cannot allocate device memory (code under HIP graph
  * capture, tight serving loops, harnesses that forbid hipMalloc):
  * bevpool_forward_scheduled without a workspace.  The slots live in a

@@ -83,6 +83,11 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
                                               i32, vp, vp, sz, vp]
+    lib.bevpool_depth_lse.restype = ctypes.c_int
+    lib.bevpool_depth_lse.argtypes = [shp, ctypes.c_int, vp, vp, vp]
+    lib.bevpool_forward_scheduled_softmax.restype = ctypes.c_int
+    lib.bevpool_forward_scheduled_softmax.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, vp, sz, i32,
+                                                      i32, i32, vp, vp, sz, vp]
     lib.bevpool_forward_scheduled_noalloc.restype = ctypes.c_int
     lib.bevpool_forward_scheduled_noalloc.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32,
                                                       i32, i32, vp, vp]
@@ -228,6 +233,26 @@ def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule,
                                               int(n_valid), int(n_intervals), int(n_slots), _ptr(out),
                                               _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
+
+
+def bevpool_depth_lse(shape, in_dtype, logits, lse, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_depth_lse(ctypes.byref(s), int(in_dtype), _ptr(logits), _ptr(lse), _stream(stream)),
+           "bevpool_depth_lse")
+
+
+def bevpool_forward_scheduled_softmax(shape, in_dtype, out_dtype, logits, lse, feat, schedule, schedule_bytes,
+                                      n_valid, n_intervals, n_slots, out, workspace, workspace_bytes,
+                                      stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    _check(lib, lib.bevpool_forward_scheduled_softmax(ctypes.byref(s), int(in_dtype), int(out_dtype),
+                                                      _ptr(logits), _ptr(lse), _ptr(feat), _ptr(schedule),
+                                                      int(schedule_bytes), int(n_valid), int(n_intervals),
+                                                      int(n_slots), _ptr(out), _ptr(workspace),
+                                                      int(workspace_bytes), _stream(stream)),
+           "bevpool_forward_scheduled_softmax")
 
 
 def bevpool_forward_scheduled_noalloc(shape, in_dtype, out_dtype, depth, feat, schedule, schedule_bytes,
@@ -409,6 +434,50 @@ def forward_scheduled(depth: torch.Tensor, feat: torch.Tensor, sched: Schedule, 
     bevpool_forward_scheduled(sd, _DTYPE_CODE[depth.dtype], _DTYPE_CODE[odt], depth, feat, sched.buffer,
                               sched.buffer.numel(), plan.n_valid, plan.n_intervals, sched.n_slots, out,
                               workspace, workspace.numel() * workspace.element_size(), stream)
+    return out
+
+
+def depth_lse(logits: torch.Tensor, shape, stream=None) -> torch.Tensor:
+    """Per-pixel log-sum-exp over the depth bins of logits (B, N, D, H, W):
+    float64 (B, N, H, W)."""
+    sd = _shape_dict(shape)
+    B, N, D, H, W = (sd[k] for k in ("B", "N", "D", "H", "W"))
+    _require(logits, "logits")
+    if tuple(logits.shape) != (B, N, D, H, W):
+        raise ValueError(f"logits shape {tuple(logits.shape)} is not (B, N, D, H, W) = {(B, N, D, H, W)}")
+    lse = torch.empty((B, N, H, W), dtype=torch.float64, device=logits.device)
+    bevpool_depth_lse(sd, _DTYPE_CODE[logits.dtype], logits, lse, stream)
+    return lse
+
+
+def forward_scheduled_softmax(logits: torch.Tensor, feat: torch.Tensor, sched: Schedule,
+                              lse: torch.Tensor | None = None, out_dtype=None,
+                              out: torch.Tensor | None = None, workspace: torch.Tensor | None = None,
+                              stream=None) -> torch.Tensor:
+    """The scheduled forward with depth scores softmax(logits) over the depth
+    bins, formed on the fly (lse from depth_lse when not given)."""
+    plan = sched.plan
+    sd = plan.shape
+    B, N, D, H, W, C, X, Y, Z = (sd[k] for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z"))
+    _require(logits, "logits")
+    _require(feat, "feat", logits.dtype)
+    if tuple(logits.shape) != (B, N, D, H, W) or tuple(feat.shape) != (B, N, H, W, C):
+        raise ValueError("logits/feat shapes do not match the plan")
+    if lse is None:
+        lse = depth_lse(logits, sd, stream)
+    _require(lse, "lse", torch.float64)
+    if tuple(lse.shape) != (B, N, H, W):
+        raise ValueError(f"lse shape {tuple(lse.shape)} is not (B, N, H, W)")
+    odt = out_dtype or logits.dtype
+    if out is None:
+        out = torch.empty((B, Z, Y, X, C), dtype=odt, device=logits.device)
+    _require(out, "out", odt)
+    if workspace is None:
+        workspace = forward_scheduled_workspace(sched)
+    bevpool_forward_scheduled_softmax(sd, _DTYPE_CODE[logits.dtype], _DTYPE_CODE[odt], logits, lse, feat,
+                                      sched.buffer, sched.buffer.numel(), plan.n_valid, plan.n_intervals,
+                                      sched.n_slots, out, workspace, workspace.numel() * workspace.element_size(),
+                                      stream)
     return out
 
 

@@ -304,6 +304,44 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                   "bevpool_forward_scheduled");
 }
 
+int bevpool_depth_lse(const bevpool_shape* shape, int in_dtype, const void* logits, double* lse,
+                      void* stream) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  st = check_dtypes(in_dtype, BEVPOOL_F32);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(logits);
+  REQUIRE_PTR(lse);
+  return from_hip(bevpool::launch_depth_lse(d, in_dtype, logits, lse,
+                                            static_cast<hipStream_t>(stream)),
+                  "bevpool_depth_lse");
+}
+
+int bevpool_forward_scheduled_softmax(const bevpool_shape* shape, int in_dtype, int out_dtype,
+                                      const void* logits, const double* lse, const void* feat,
+                                      const void* schedule, size_t schedule_bytes,
+                                      int32_t n_valid, int32_t n_intervals, int32_t n_slots,
+                                      void* out, void* workspace, size_t workspace_bytes,
+                                      void* stream) {
+  bevpool::Dims d;
+  int st = check_forward_scheduled(shape, in_dtype, out_dtype, logits, feat, schedule,
+                                   schedule_bytes, n_valid, n_intervals, n_slots, out, &d);
+  if (st != BEVPOOL_OK) return st;
+  if (n_intervals > 0) {
+    REQUIRE_PTR(lse);
+    const size_t ws_need = bevpool::forward_scheduled_workspace_bytes(d, n_slots);
+    if (ws_need > 0 && (workspace == nullptr || workspace_bytes < ws_need))
+      return fail(BEVPOOL_EWORKSPACE, "%d slots need %zu workspace bytes, got %zu at %p", n_slots,
+                  ws_need, workspace_bytes, workspace);
+  }
+  return from_hip(bevpool::launch_forward_scheduled(d, in_dtype, out_dtype, logits, feat, schedule,
+                                                    n_valid, n_intervals, n_slots, out, workspace,
+                                                    workspace_bytes,
+                                                    static_cast<hipStream_t>(stream), lse),
+                  "bevpool_forward_scheduled_softmax");
+}
+
 int bevpool_forward_scheduled_noalloc(const bevpool_shape* shape, int in_dtype, int out_dtype,
                                       const void* depth, const void* feat, const void* schedule,
                                       size_t schedule_bytes, int32_t n_valid, int32_t n_intervals,

@@ -82,6 +82,8 @@ struct StripArgs {
   float* slots;
   int64_t slot_cap;  // slots the workspace holds
   int32_t n_valid, n_occ, n_slots, items_cap;  // counts the launch was sized from
+  const double* lse;  // fused depth softmax: per-pixel log-sum-exp of the logits (else unused)
+  int32_t dhw;       // D * H * W (points of one view)
   int32_t C, H, W, bh, bw, nhb, nwb, strips;
   int32_t hw32;    // H * W
   int64_t P, cells, n_empty;
@@ -175,7 +177,10 @@ struct ItemHdr {
   int32_t strip, p0, np, g0, nseg;
 };
 
-template <typename TIn, typename TOut, int VEC>
+// SM: `depth` holds depth logits, and a point's depth score is
+// exp(logit - lse[pixel]) (the softmax over the pixel's depth bins, with the
+// log-sum-exp from k_depth_lse), formed as the points are gathered.
+template <typename TIn, typename TOut, int VEC, bool SM>
 __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ depth,
                                                     const TIn* __restrict__ feat,
                                                     TOut* __restrict__ out, StripArgs a) {
@@ -237,6 +242,19 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   const int wave = tid / kWave;
   const int64_t hw = a.hw32;
   const TIn* const fchunk = feat + (int64_t)cbase * VEC;
+  // depth score of a gathered point: the stored score, or exp(logit - lse)
+  // of the point's pixel (SM)
+  auto score = [&](TIn x, double lse) -> float {
+    if constexpr (SM) return expf((float)((double)to_float(x) - lse));  // (exponent in double)
+    return to_float(x);
+  };
+  // log-sum-exp of the pixel of frustum point p (all points of a pair share
+  // it); 0 outside the index range (the pair's points then read nothing)
+  auto pixel_lse = [&](int32_t p) -> double {
+    if (p < 0 || (int64_t)p >= a.P) return 0.0;
+    const int32_t view = p / a.dhw;
+    return a.lse[(int64_t)view * hw + (p - view * a.dhw) % a.hw32];
+  };
 
   // Item headers, copied to LDS once (the launch gives no workgroup more
   // than kHdrCache items; scalar loads share their wait counter with LDS
@@ -348,14 +366,16 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         sg[q] = a.pair_seg[k];
       }
       float dv[kPB][kDepthBurst];
+      double lq[kPB];
 #pragma unroll
       for (int q = 0; q < kPB; ++q) {
         const int n = (q0 + q) * NT + lt < h.np ? (int)(ln[q] >> 16) : 0;
+        if constexpr (SM) lq[q] = pixel_lse(rd0[q]);
 #pragma unroll
         for (int j = 0; j < kDepthBurst; ++j) {
           const int64_t p = (int64_t)rd0[q] + j * hw;
           float v = 0.f;
-          if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
+          if (j < n && p >= 0 && p < a.P) v = score(depth[p], lq[q]);
           dv[q][j] = v;
         }
       }
@@ -370,7 +390,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
           for (int j = kDepthBurst; j < n; ++j) {
             const int64_t p = (int64_t)rd0[q] + j * hw;
-            if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+            if (p >= 0 && p < a.P) sum += score(depth[p], lq[q]);
           }
           const uint32_t lp = ln[q] & kPairPixel;
           const bool ok = lp < (uint32_t)g.npix;
@@ -412,14 +432,16 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     PairRec* const s_pr = buf_pr(b);
     int32_t* const s_dest = buf_dest(b);
     float dv[kLPL][kDepthBurst];
+    double lq[kLPL];
 #pragma unroll
     for (int q = 0; q < kLPL; ++q) {
       const int n = q * kLoadThreads + lt < h.np ? (int)(pf.ln[q] >> 16) : 0;
+      if constexpr (SM) lq[q] = pixel_lse(pf.rd0[q]);
 #pragma unroll
       for (int j = 0; j < kDepthBurst; ++j) {
         const int64_t p = (int64_t)pf.rd0[q] + j * hw;
         float v = 0.f;
-        if (j < n && p >= 0 && p < a.P) v = to_float(depth[p]);
+        if (j < n && p >= 0 && p < a.P) v = score(depth[p], lq[q]);
         dv[q][j] = v;
       }
     }
@@ -451,7 +473,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
         for (int j = kDepthBurst; j < n; ++j) {
           const int64_t p = (int64_t)pf.rd0[q] + j * hw;
-          if (p >= 0 && p < a.P) sum += to_float(depth[p]);
+          if (p >= 0 && p < a.P) sum += score(depth[p], lq[q]);
         }
         const uint32_t lp = pf.ln[q] & kPairPixel;
         const bool ok = lp < (uint32_t)g.npix;
@@ -776,7 +798,7 @@ __global__ __launch_bounds__(256) void k_zero_out(TOut* __restrict__ out, int64_
   if (i < nvec) store_zero<TOut, VEC>(out + i * VEC);
 }
 
-template <typename TIn, typename TOut, int VEC>
+template <typename TIn, typename TOut, int VEC, bool SM>
 hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void* feat,
                StripArgs a, void* out, hipStream_t stream) {
   TOut* o = static_cast<TOut*>(out);
@@ -788,7 +810,7 @@ hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void
   const int64_t per_die_slots = std::max<int64_t>(forward_workgroups() / kXcds,
                                                   a.items_cap / ((int64_t)kXcds * kHdrCache) + 1);
   const int blocks = (int)(per_die_slots * kXcds);
-  k_fwd_strips<TIn, TOut, VEC><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
+  k_fwd_strips<TIn, TOut, VEC, SM><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
       static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
   const int64_t gpw = kWave / (CV < kWave ? CV : kWave);
   const int64_t entries = (int64_t)a.n_occ + a.n_empty;
@@ -832,11 +854,27 @@ size_t forward_scheduled_workspace_bytes(const Dims& d, int64_t n_slots) {
   return (size_t)(n_slots > 0 ? n_slots : 0) * (size_t)d.C * sizeof(float);
 }
 
+template <bool SM>
+hipError_t dispatch_scheduled(const Dims& d, const StripDims& sd, bool half_in, bool half_out,
+                              int vec, const void* depth, const void* feat, const StripArgs& a,
+                              void* out, hipStream_t stream) {
+  if (!half_in) {
+    if (vec == 4) return run<float, float, 4, SM>(d, sd, depth, feat, a, out, stream);
+    return run<float, float, 1, SM>(d, sd, depth, feat, a, out, stream);
+  }
+  if (half_out) {
+    if (vec == 8) return run<half_t, half_t, 8, SM>(d, sd, depth, feat, a, out, stream);
+    return run<half_t, half_t, 1, SM>(d, sd, depth, feat, a, out, stream);
+  }
+  if (vec == 8) return run<half_t, float, 8, SM>(d, sd, depth, feat, a, out, stream);
+  return run<half_t, float, 1, SM>(d, sd, depth, feat, a, out, stream);
+}
+
 hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
                                     int32_t n_valid, int32_t n_intervals, int32_t n_slots,
                                     void* out, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream) {
+                                    hipStream_t stream, const double* lse) {
   const bool al = aligned16(feat) && aligned16(out) && aligned16(workspace);
   const bool half_in = in_dtype == BEVPOOL_F16;
   const bool half_out = out_dtype == BEVPOOL_F16;
@@ -881,16 +919,11 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.P = d.P;
   a.cells = d.cells;
   a.n_empty = L.n_empty;
-  if (!half_in) {
-    if (vec == 4) return run<float, float, 4>(d, L.sd, depth, feat, a, out, stream);
-    return run<float, float, 1>(d, L.sd, depth, feat, a, out, stream);
-  }
-  if (half_out) {
-    if (vec == 8) return run<half_t, half_t, 8>(d, L.sd, depth, feat, a, out, stream);
-    return run<half_t, half_t, 1>(d, L.sd, depth, feat, a, out, stream);
-  }
-  if (vec == 8) return run<half_t, float, 8>(d, L.sd, depth, feat, a, out, stream);
-  return run<half_t, float, 1>(d, L.sd, depth, feat, a, out, stream);
+  a.lse = lse;
+  a.dhw = (int32_t)(d.D * d.hw);
+  if (lse != nullptr)
+    return dispatch_scheduled<true>(d, L.sd, half_in, half_out, vec, depth, feat, a, out, stream);
+  return dispatch_scheduled<false>(d, L.sd, half_in, half_out, vec, depth, feat, a, out, stream);
 }
 
 // ---- allocation-free forward: the slots live in a file-scope device array.

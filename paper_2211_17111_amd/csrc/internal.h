@@ -155,7 +155,10 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     const void* depth, const void* feat, const void* schedule,
                                     int32_t n_valid, int32_t n_intervals, int32_t n_slots,
                                     void* out, void* workspace, size_t workspace_bytes,
-                                    hipStream_t stream);
+                                    hipStream_t stream, const double* lse = nullptr);
+// per-pixel log-sum-exp over the depth bins of depth logits (B, N, D, H, W)
+hipError_t launch_depth_lse(const Dims& d, int in_dtype, const void* logits, double* lse,
+                            hipStream_t stream);
 
 // ---- forward ---------------------------------------------------------------
 size_t forward_workspace_bytes(const Dims& d);

@@ -42,7 +42,7 @@ def test_exports_every_declared_symbol(lib):
         "bevpool_prepare_workspace_size", "bevpool_prepare", "bevpool_forward",
         "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
         "bevpool_forward_scheduled", "bevpool_forward_scheduled_workspace_size",
-        "bevpool_forward_scheduled_noalloc",
+        "bevpool_forward_scheduled_noalloc", "bevpool_depth_lse", "bevpool_forward_scheduled_softmax",
         "bevpool_backward_workspace_size", "bevpool_backward", "bevpool_backward_scheduled",
     }
     for n in names:
@@ -233,3 +233,29 @@ def test_noalloc_scratch_bound():
                                                n_slots, DUMMY, None)
     assert st == EWORKSPACE
     assert "allocation-free" in bp.bevpool_last_error()
+
+
+def test_softmax_validation():
+    """The fused softmax entry points check their arguments before any HIP
+    call."""
+    lib = bp.load_library()
+    s = bp.make_shape(dict(B=1, N=2, D=8, H=4, W=8, C=16, X=16, Y=16, Z=1))
+    lse = lambda **k: lib.bevpool_depth_lse(ctypes.byref(s), k.get("i", 0), k.get("x", DUMMY), k.get("l", DUMMY),
+                                            None)
+    assert lse(x=None) == EINVAL
+    assert lse(l=None) == EINVAL
+    assert lse(i=7) == EDTYPE
+    sb, wb = ctypes.c_size_t(0), ctypes.c_size_t(0)
+    assert lib.bevpool_schedule_size(ctypes.byref(s), 400, 100, ctypes.byref(sb), ctypes.byref(wb)) == OK
+    f = lambda **k: lib.bevpool_forward_scheduled_softmax(
+        ctypes.byref(s), k.get("i", 0), k.get("o", 0), k.get("x", DUMMY), k.get("l", DUMMY), DUMMY, DUMMY,
+        sb.value, 400, 100, k.get("ns", 4), k.get("out", DUMMY), k.get("ws", DUMMY), k.get("wb", 4 * 16 * 4),
+        None)
+    assert f(i=0, o=1) == EDTYPE
+    assert f(x=None) == EINVAL
+    assert f(l=None) == EINVAL
+    assert f(out=None) == EINVAL
+    assert f(ns=401) == EINVAL
+    assert f(ws=None) == EWORKSPACE
+    assert f(wb=4 * 16 * 4 - 1) == EWORKSPACE
+

@@ -1,0 +1,98 @@
+"""The fused depth-softmax forward against the oracle (section 2.1: the
+depth score of a pixel is its distribution over the depth bins, here the
+softmax of depth logits).
+
+bevpool_depth_lse is compared with the float64 log-sum-exp per pixel, and
+bevpool_forward_scheduled_softmax with oracle.forward_softmax_ref over every
+output element, to the forward's bound (tol * sum|terms| + 1e-6; tol 1e-5
+for float32 inputs, 2e-3 for float16).  The log-sum-exp bound: the terms
+are float32 expf values (within 2 ulp, relative 2^-23 each) summed and
+logged in double and kept in double, so |lse - lse_ref| <= 2^-23 plus the
+double rounding; the test allows 4 * 2^-24 + 1e-12 (the logits' own
+rounding does not enter: the oracle takes the same rounded logits).
+"""
+
+import numpy as np
+import pytest
+import torch
+
+import _gpu
+import oracle
+from paper_2211_17111_amd import bevpool as bp
+from workloads import CONFIGS, draw_inputs, draw_small, frustum_coor, random_coor
+
+pytestmark = pytest.mark.gpu
+
+_DT = {"f32": torch.float32, "f16": torch.float16}
+
+
+def _lse_bound(ref):
+    return 4 * 2.0 ** -24 + 1e-12 * np.abs(ref)
+
+
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large"])
+def test_lse_matches_oracle(name):
+    cfg = CONFIGS[name]
+    _gpu.say(f"depth log-sum-exp: {name}")
+    data = draw_inputs(cfg, with_grad=False, with_logits=True)
+    logits = _gpu.to_dev(data["logits"])
+    got = bp.depth_lse(logits, cfg.shape()).cpu().numpy()
+    ref = oracle.depth_lse_ref(data["logits"])
+    err = np.abs(got - ref)
+    worst = float((err / _lse_bound(ref)).max())
+    _gpu.say(f"  worst err/bound {worst:.3f}")
+    assert worst <= 1.0, name
+
+
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "voxel3d"])
+def test_fused_forward_every_element(name):
+    cfg = CONFIGS[name]
+    shape = cfg.shape()
+    _gpu.say(f"fused depth-softmax forward: {name}")
+    data = draw_inputs(cfg, with_grad=False, with_logits=True)
+    coor = frustum_coor(cfg)
+    plan = _gpu.run_prepare(coor, shape)
+    sched = bp.schedule(plan)
+    logits, feat = _gpu.to_dev(data["logits"]), _gpu.to_dev(data["feat"])
+    odt = _DT[cfg.out_dtype]
+    out = bp.forward_scheduled_softmax(logits, feat, sched, out_dtype=odt)
+    torch.cuda.synchronize()
+    ref, mag = oracle.forward_softmax_ref(data["logits"], data["feat"], coor, shape)
+    _gpu.assert_within(out.cpu().numpy(), ref, mag, cfg.dtype, label=name, log=True)
+
+
+def test_fused_forward_random_shapes_and_extreme_logits():
+    """Ragged shapes and logits far from zero (the per-pixel maximum shift
+    keeps every term finite)."""
+    rng = np.random.default_rng(21)
+    shape = dict(B=2, N=3, D=9, H=5, W=7, C=12, X=10, Y=9, Z=2)
+    coor = random_coor(rng, shape, p_out=0.25)
+    d = draw_small(rng, shape)
+    for scale, shift in ((3.0, 0.0), (20.0, 60.0), (20.0, -60.0)):
+        logits = (scale * rng.standard_normal((2, 3, 9, 5, 7)) + shift).astype(np.float32)
+        plan = _gpu.run_prepare(coor, shape)
+        sched = bp.schedule(plan)
+        out = bp.forward_scheduled_softmax(_gpu.to_dev(logits), _gpu.to_dev(d["feat"]), sched)
+        torch.cuda.synchronize()
+        ref, mag = oracle.forward_softmax_ref(logits, d["feat"], coor, shape)
+        _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", label=f"scale {scale} shift {shift}")
+
+
+def test_fused_equals_unfused_on_the_same_scores():
+    """With the scores materialised from the same logits and lse on the host
+    (float32 exp of the float32 difference), the plain scheduled forward and
+    the fused one see the same depth values up to the device expf: their
+    results agree to the forward's bound."""
+    cfg = CONFIGS["bevdet"]
+    shape = cfg.shape()
+    data = draw_inputs(cfg, with_grad=False, with_logits=True)
+    plan = _gpu.run_prepare(frustum_coor(cfg), shape)
+    sched = bp.schedule(plan)
+    logits, feat = _gpu.to_dev(data["logits"]), _gpu.to_dev(data["feat"])
+    lse = bp.depth_lse(logits, shape)
+    scores = torch.exp((logits.double() - lse[:, :, None]).float())
+    a = bp.forward_scheduled_softmax(logits, feat, sched, lse=lse)
+    b = bp.forward_scheduled(scores.contiguous(), feat, sched)
+    torch.cuda.synchronize()
+    _, mag = oracle.forward_ref(scores.cpu().numpy(), data["feat"], frustum_coor(cfg), shape)
+    _gpu.assert_within(a.cpu().numpy(), b.cpu().numpy().astype(np.float64), mag, "f32", label="fused vs unfused")
