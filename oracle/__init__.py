@@ -22,6 +22,7 @@ from .bevpool_ref import (
     depth_lse_ref,
     depth_softmax_ref,
     forward_softmax_ref,
+    geometry_ref,
 )
 
 __all__ = [
@@ -37,4 +38,5 @@ __all__ = [
     "depth_lse_ref",
     "depth_softmax_ref",
     "forward_softmax_ref",
+    "geometry_ref",
 ]

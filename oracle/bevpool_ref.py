@@ -268,3 +268,45 @@ def depth_softmax_ref(logits: np.ndarray) -> np.ndarray:
 def forward_softmax_ref(logits: np.ndarray, feat: np.ndarray, coor: np.ndarray, shape: dict):
     """forward_ref with the depth scores of depth_softmax_ref(logits)."""
     return forward_ref(depth_softmax_ref(logits), feat, coor, shape)
+
+
+# ---- voxel index from camera parameters (the on-device geometry) ----------
+#
+# Section 2.1 takes each frustum point's voxel index as computed offline from
+# the camera intrinsics and extrinsics.  The reading here (a pinhole model):
+# feature cell (h, w) looks through the pixel centre (u, v) = ((w + 0.5) s,
+# (h + 0.5) s) for stride s; depth bin k lies at depth_start + k depth_step
+# along the optical axis; the camera point is ((u - cx) dep / fx,
+# (v - cy) dep / fy, dep); the ego point is R @ cam + t, each coordinate
+# summed in the order (R0 X + R1 Y) + R2 Z + t; the voxel index is
+# floor((e - lo) / res), clipped to +-2^30 so it stays representable; points
+# outside the grid keep their index (the filter of prepare drops them).
+
+
+def geometry_ref(cams: np.ndarray, params: dict, shape: dict) -> np.ndarray:
+    """int32 (B*N*D*H*W, 3) voxel index (x, y, z) of every frustum point
+    from per-camera parameters cams (B, N, 16): fx, fy, cx, cy, R (3x3,
+    row-major), t."""
+    B, N, D, H, W, C, X, Y, Z = _dims(shape)
+    cams = np.asarray(cams, dtype=_F64)
+    s = _F64(params["stride"])
+    u = (np.arange(W, dtype=_F64) + 0.5) * s
+    v = (np.arange(H, dtype=_F64) + 0.5) * s
+    dep = _F64(params["depth_start"]) + np.arange(D, dtype=_F64) * _F64(params["depth_step"])
+    lo = np.asarray(params["lo"], dtype=_F64)
+    res = np.asarray(params["res"], dtype=_F64)
+    out = np.empty((B, N, D, H, W, 3), dtype=np.int64)
+    d3 = dep[:, None, None]
+    for b in range(B):
+        for n in range(N):
+            fx, fy, cx, cy = cams[b, n, :4]
+            R = cams[b, n, 4:13].reshape(3, 3)
+            t = cams[b, n, 13:16]
+            Xc = np.broadcast_to(((u[None, None, :] - cx) * d3) / fx, (D, H, W))
+            Yc = np.broadcast_to(((v[None, :, None] - cy) * d3) / fy, (D, H, W))
+            Zc = np.broadcast_to(d3, (D, H, W))
+            for i in range(3):
+                e = ((R[i, 0] * Xc + R[i, 1] * Yc) + R[i, 2] * Zc) + t[i]
+                idx = np.floor((e - lo[i]) / res[i])
+                out[b, n, ..., i] = np.clip(idx, -(2 ** 30), 2 ** 30).astype(np.int64)
+    return out.reshape(-1, 3).astype(np.int32)

@@ -12,7 +12,7 @@ Shapes follow BEVPoolv2 section 2.1: depth score (N, D, H, W), image feature
 """
 
 from .configs import CONFIGS, Config, get_config
-from .rig import frustum_coor, random_coor
+from .rig import frustum_coor, frustum_params, jittered_cameras, random_coor, rig_cameras
 from .data import draw_inputs, draw_small
 
 __all__ = [
@@ -21,6 +21,9 @@ __all__ = [
     "get_config",
     "frustum_coor",
     "random_coor",
+    "rig_cameras",
+    "jittered_cameras",
+    "frustum_params",
     "draw_inputs",
     "draw_small",
 ]

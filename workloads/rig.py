@@ -93,3 +93,53 @@ def random_coor(rng: np.random.Generator, shape: dict, p_out: float = 0.3,
     for col, ext in enumerate((X, Y, Z)):
         coor[inside, col] = rng.integers(0, ext, size=int(inside.sum()))
     return coor
+
+
+# ---- the rig as camera parameters (for the on-device geometry) -------------
+#
+# Per camera, 16 float64 values: fx, fy, cx, cy, then the camera-to-ego
+# rotation R (row-major 3x3) and translation t (ego = R @ cam + t).  The
+# rig's axis change and yaw above are R = Yaw(psi) @ A with A taking
+# (Xc, Yc, Zc) to (Zc, -Xc, -Yc), and t = (0, 0, cam_height).
+
+CAM_WORDS = 16
+
+
+def rig_cameras(cfg: Config) -> np.ndarray:
+    """float64 (B, N, 16): every sample's camera parameters of the rig."""
+    f = cfg.focal
+    cams = np.zeros((cfg.N, CAM_WORDS), dtype=np.float64)
+    for n in range(cfg.N):
+        psi = math.radians(n * cfg.yaw_step_deg)
+        c, s = math.cos(psi), math.sin(psi)
+        R = np.array([[s, 0.0, c], [-c, 0.0, s], [0.0, -1.0, 0.0]])
+        cams[n, :4] = (f, f, cfg.img_w / 2.0, cfg.img_h / 2.0)
+        cams[n, 4:13] = R.reshape(-1)
+        cams[n, 13:16] = (0.0, 0.0, cfg.cam_height)
+    return np.ascontiguousarray(np.broadcast_to(cams, (cfg.B, cfg.N, CAM_WORDS)))
+
+
+def frustum_params(cfg: Config) -> dict:
+    """The frustum and grid description the geometry takes."""
+    return dict(stride=float(cfg.stride), depth_start=float(cfg.depth_start),
+                depth_step=float(cfg.depth_step),
+                lo=(float(cfg.xy_lo), float(cfg.xy_lo), float(cfg.z_lo)),
+                res=(float(cfg.xy_res), float(cfg.xy_res), float(cfg.z_res)))
+
+
+def jittered_cameras(cfg: Config, rng: np.random.Generator, yaw_deg: float = 5.0,
+                     shift_m: float = 0.5) -> np.ndarray:
+    """The rig with an independent random yaw (up to +-yaw_deg) and ego
+    shift (up to +-shift_m in x and y) per sample: per-sample augmentation."""
+    cams = rig_cameras(cfg).copy()
+    for b in range(cfg.B):
+        dpsi = math.radians(rng.uniform(-yaw_deg, yaw_deg))
+        c, s = math.cos(dpsi), math.sin(dpsi)
+        Y = np.array([[c, -s, 0.0], [s, c, 0.0], [0.0, 0.0, 1.0]])
+        dx, dy = rng.uniform(-shift_m, shift_m, size=2)
+        for n in range(cfg.N):
+            R = cams[b, n, 4:13].reshape(3, 3)
+            cams[b, n, 4:13] = (Y @ R).reshape(-1)
+            t = cams[b, n, 13:16]
+            cams[b, n, 13:16] = Y @ t + np.array([dx, dy, 0.0])
+    return cams
