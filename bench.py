@@ -442,6 +442,20 @@ def main():
         f"written), cold median {copy_ms * 1e3:.2f} us -> {copy_gbs:.0f} GB/s "
         f"({copy_gbs / HBM_PEAK_GBS * 100:.1f}% of peak); back-to-back {copy_region * 1e3:.2f} us/launch")
 
+    # ---- on-device geometry (the voxel index of every point from the camera
+    # parameters), into each set's coor
+    from workloads import frustum_params, rig_cameras
+    cams_d = torch.from_numpy(rig_cameras(cfg)).to(dev)
+    fr = bp.make_frustum(frustum_params(cfg))
+
+    def geometry(i):
+        bp.bevpool_geometry(shape, fr, cams_d, sets[i % len(sets)].coor, stream)
+
+    geo_per, geo_region = _cold(64, lambda i: i, geometry, stream)
+    geo_ms = float(np.median(geo_per))
+    geo_bytes = 12 * cfg.P + 8 * bp.CAMERA_WORDS * cfg.B * cfg.N
+    log(f"geometry {geo_ms * 1e3:.2f} us ({geo_bytes / (geo_ms * 1e-3) / 1e9:.0f} GB/s of coor written)")
+
     # ---- fused depth softmax: the per-pixel log-sum-exp pre-pass, then the
     # scheduled forward from the logits (scores formed on the fly)
     lg_data = draw_inputs(cfg, with_grad=False, with_logits=True)
@@ -571,6 +585,10 @@ def main():
                                   "time": "mean over the steps of the step's schedule build (HIP events)"},
             "other_workloads": others,
             "fused_softmax": fused,
+            "geometry": {"ms": geo_ms, "region_ms_per_launch": geo_region, "bytes": geo_bytes,
+                         "gbs": round(geo_bytes / (geo_ms * 1e-3) / 1e9, 1),
+                         "note": "bevpool_geometry (float64 pinhole projection and voxelisation) of the rig's "
+                                 "cameras into each rotating set's coor; median of per-launch HIP events"},
             "prepare_roofline": {"algorithmic_bytes": plan_bytes, "achieved_gbs": round(plan_gbs, 1),
                                  "peak_gbs": HBM_PEAK_GBS, "frac": round(plan_gbs / HBM_PEAK_GBS, 4),
                                  "time": "mean over the steps of the step's prepare (HIP events)"},

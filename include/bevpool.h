@@ -96,6 +96,36 @@ const char* bevpool_strerror(int status);
 const char* bevpool_last_error(void);
 
 /*
+ * Geometry (section 2.1, paragraph 1: each frustum point's voxel index,
+ * computed from the camera intrinsics and extrinsics), on the device, for
+ * geometry that changes per sample (augmentation, ego motion).
+ *
+ * cams: device float64 (B, N, BEVPOOL_CAMERA_WORDS), per camera fx, fy, cx,
+ * cy, then the camera-to-ego rotation R (row-major 3x3) and translation t
+ * (ego = R cam + t; camera frame x right, y down, z forward).  Feature cell
+ * (h, w) looks through the pixel centre ((w + 0.5) stride, (h + 0.5) stride);
+ * depth bin k lies at depth_start + k depth_step along the optical axis.
+ * bevpool_geometry writes coor (P x 3 int32, the layout bevpool_prepare
+ * reads, points enumerated like the depth score): floor((e - lo) / res) of
+ * each ego coordinate e, clipped to +-2^30.  Points outside the grid keep
+ * their index (bevpool_prepare filters them).  All arithmetic is float64 in
+ * a fixed order with no fused multiply-add, so the indices match a float64
+ * evaluation of the same expressions bit for bit.  EINVAL for NULL pointers,
+ * a non-positive or non-finite stride, step or cell size, or non-finite
+ * bounds.
+ */
+#define BEVPOOL_CAMERA_WORDS 16
+typedef struct bevpool_frustum {
+  double stride;      /* input pixels per feature cell */
+  double depth_start; /* depth of bin 0 along the optical axis (metres) */
+  double depth_step;  /* depth between neighbouring bins (metres) */
+  double lo[3];       /* grid lower bounds x, y, z in the ego frame (metres) */
+  double res[3];      /* cell sizes x, y, z (metres) */
+} bevpool_frustum;
+int bevpool_geometry(const bevpool_shape* shape, const bevpool_frustum* frustum,
+                     const double* cams, int32_t* coor, void* stream);
+
+/*
  * Preprocessing (section 2.1, paragraphs 1-2): filter, sort, intervals.
  *
  * bevpool_prepare_workspace_size writes to *bytes the device scratch size

@@ -43,6 +43,24 @@ class bevpool_shape(ctypes.Structure):
     _fields_ = [(k, ctypes.c_int32) for k in ("B", "N", "D", "H", "W", "C", "X", "Y", "Z")]
 
 
+class bevpool_frustum(ctypes.Structure):
+    _fields_ = [("stride", ctypes.c_double), ("depth_start", ctypes.c_double), ("depth_step", ctypes.c_double),
+                ("lo", ctypes.c_double * 3), ("res", ctypes.c_double * 3)]
+
+
+CAMERA_WORDS = 16  # BEVPOOL_CAMERA_WORDS
+
+
+def make_frustum(params: dict) -> bevpool_frustum:
+    """bevpool_frustum from a dict with stride, depth_start, depth_step, lo (3), res (3)."""
+    f = bevpool_frustum()
+    f.stride, f.depth_start, f.depth_step = (float(params[k]) for k in ("stride", "depth_start", "depth_step"))
+    for i in range(3):
+        f.lo[i] = float(params["lo"][i])
+        f.res[i] = float(params["res"][i])
+    return f
+
+
 _lib = None
 
 
@@ -83,6 +101,8 @@ def load_library(path: str | None = None) -> ctypes.CDLL:
     lib.bevpool_forward_scheduled_workspace_size.argtypes = [shp, i32, ctypes.POINTER(sz)]
     lib.bevpool_forward_scheduled.argtypes = [shp, ctypes.c_int, ctypes.c_int, vp, vp, vp, sz, i32, i32,
                                               i32, vp, vp, sz, vp]
+    lib.bevpool_geometry.restype = ctypes.c_int
+    lib.bevpool_geometry.argtypes = [shp, ctypes.POINTER(bevpool_frustum), vp, vp, vp]
     lib.bevpool_depth_lse.restype = ctypes.c_int
     lib.bevpool_depth_lse.argtypes = [shp, ctypes.c_int, vp, vp, vp]
     lib.bevpool_forward_scheduled_softmax.restype = ctypes.c_int
@@ -233,6 +253,27 @@ def bevpool_forward_scheduled(shape, in_dtype, out_dtype, depth, feat, schedule,
                                               int(n_valid), int(n_intervals), int(n_slots), _ptr(out),
                                               _ptr(workspace), int(workspace_bytes), _stream(stream)),
            "bevpool_forward_scheduled")
+
+
+def bevpool_geometry(shape, frustum, cams, coor, stream=None) -> None:
+    lib = load_library()
+    s = make_shape(shape)
+    f = frustum if isinstance(frustum, bevpool_frustum) else make_frustum(frustum)
+    _check(lib, lib.bevpool_geometry(ctypes.byref(s), ctypes.byref(f), _ptr(cams), _ptr(coor), _stream(stream)),
+           "bevpool_geometry")
+
+
+def geometry(cams: torch.Tensor, params: dict, shape, stream=None) -> torch.Tensor:
+    """Voxel index (P, 3) int32 of every frustum point from cameras (B, N, 16)
+    float64 on the device."""
+    sd = _shape_dict(shape)
+    _require(cams, "cams", torch.float64)
+    if tuple(cams.shape) != (sd["B"], sd["N"], CAMERA_WORDS):
+        raise ValueError(f"cams shape {tuple(cams.shape)} is not (B, N, {CAMERA_WORDS})")
+    P = sd["B"] * sd["N"] * sd["D"] * sd["H"] * sd["W"]
+    coor = torch.empty((P, 3), dtype=torch.int32, device=cams.device)
+    bevpool_geometry(sd, params, cams, coor, stream)
+    return coor
 
 
 def bevpool_depth_lse(shape, in_dtype, logits, lse, stream=None) -> None:

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime_api.h>
 
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -302,6 +303,25 @@ int bevpool_forward_scheduled(const bevpool_shape* shape, int in_dtype, int out_
                                                     workspace_bytes,
                                                     static_cast<hipStream_t>(stream)),
                   "bevpool_forward_scheduled");
+}
+
+int bevpool_geometry(const bevpool_shape* shape, const bevpool_frustum* frustum,
+                     const double* cams, int32_t* coor, void* stream) {
+  bevpool::Dims d;
+  int st = check_shape(shape, &d);
+  if (st != BEVPOOL_OK) return st;
+  REQUIRE_PTR(frustum);
+  REQUIRE_PTR(cams);
+  REQUIRE_PTR(coor);
+  const bevpool_frustum& f = *frustum;
+  bool ok = std::isfinite(f.stride) && f.stride > 0 && std::isfinite(f.depth_start) &&
+            std::isfinite(f.depth_step) && f.depth_step > 0;
+  for (int i = 0; i < 3; ++i) ok = ok && std::isfinite(f.lo[i]) && std::isfinite(f.res[i]) && f.res[i] > 0;
+  if (!ok)
+    return fail(BEVPOOL_EINVAL, "frustum: stride, depth step and cell sizes must be finite and "
+                                "positive, depth start and bounds finite");
+  return from_hip(bevpool::launch_geometry(d, f, cams, coor, static_cast<hipStream_t>(stream)),
+                  "bevpool_geometry");
 }
 
 int bevpool_depth_lse(const bevpool_shape* shape, int in_dtype, const void* logits, double* lse,

@@ -156,6 +156,11 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
                                     int32_t n_valid, int32_t n_intervals, int32_t n_slots,
                                     void* out, void* workspace, size_t workspace_bytes,
                                     hipStream_t stream, const double* lse = nullptr);
+// voxel index of every frustum point from per-camera parameters (float64,
+// kCameraWords per camera of each (b, n))
+constexpr int kCameraWords = BEVPOOL_CAMERA_WORDS;
+hipError_t launch_geometry(const Dims& d, const bevpool_frustum& f, const double* cams,
+                           int32_t* coor, hipStream_t stream);
 // per-pixel log-sum-exp over the depth bins of depth logits (B, N, D, H, W)
 hipError_t launch_depth_lse(const Dims& d, int in_dtype, const void* logits, double* lse,
                             hipStream_t stream);

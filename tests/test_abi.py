@@ -43,6 +43,7 @@ def test_exports_every_declared_symbol(lib):
         "bevpool_forward_workspace_size", "bevpool_schedule_size", "bevpool_schedule",
         "bevpool_forward_scheduled", "bevpool_forward_scheduled_workspace_size",
         "bevpool_forward_scheduled_noalloc", "bevpool_depth_lse", "bevpool_forward_scheduled_softmax",
+        "bevpool_geometry",
         "bevpool_backward_workspace_size", "bevpool_backward", "bevpool_backward_scheduled",
     }
     for n in names:
@@ -258,4 +259,24 @@ def test_softmax_validation():
     assert f(ns=401) == EINVAL
     assert f(ws=None) == EWORKSPACE
     assert f(wb=4 * 16 * 4 - 1) == EWORKSPACE
+
+
+def test_geometry_validation():
+    lib = bp.load_library()
+    s = bp.make_shape(dict(B=1, N=2, D=8, H=4, W=8, C=16, X=16, Y=16, Z=1))
+    good = dict(stride=16.0, depth_start=1.0, depth_step=1.0, lo=(-8.0, -8.0, -5.0), res=(1.0, 1.0, 8.0))
+
+    def g(**k):
+        f = bp.make_frustum(dict(good, **k.get("f", {})))
+        return lib.bevpool_geometry(ctypes.byref(s), None if k.get("nof") else ctypes.byref(f),
+                                    k.get("cams", DUMMY), k.get("coor", DUMMY), None)
+
+    assert g(nof=True) == EINVAL
+    assert g(cams=None) == EINVAL
+    assert g(coor=None) == EINVAL
+    assert g(f=dict(stride=0.0)) == EINVAL
+    assert g(f=dict(depth_step=-1.0)) == EINVAL
+    assert g(f=dict(res=(1.0, 0.0, 8.0))) == EINVAL
+    assert g(f=dict(lo=(float("nan"), -8.0, -5.0))) == EINVAL
+    assert g(f=dict(depth_start=float("inf"))) == EINVAL
 
