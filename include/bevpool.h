@@ -324,10 +324,11 @@ int bevpool_backward(const bevpool_shape* shape, int in_dtype, int out_dtype,
 /* The same gradients from a schedule (bevpool_schedule of the same plan and
  * shape), which lists every pixel's pairs of kept points: each pixel's
  * feature row is read once and each pair (a cell and a run of consecutive
- * depth bins of the pixel) reads its grad_out row once.  grad_depth is
- * cleared first and the kept points are then written (every element once in
- * its final value, dropped points +0.0), grad_feat is written once per
- * element.  No workspace; no atomics (deterministic).  Arguments as for
+ * depth bins of the pixel) reads its grad_out row once.  Dropped points of
+ * grad_depth get +0.0 and kept points their gradient; in launches large
+ * enough to fill the device all of grad_depth is cleared first and the kept
+ * points are written again, in smaller ones each element is written once.
+ * grad_feat is written once per element.  No workspace; no atomics (deterministic).  Arguments as for
  * bevpool_backward and bevpool_forward_scheduled; an all-zero result when
  * n_valid or n_intervals is 0 (schedule may then be NULL). */
 int bevpool_backward_scheduled(const bevpool_shape* shape, int in_dtype, int out_dtype,
