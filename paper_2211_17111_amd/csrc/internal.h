@@ -134,8 +134,21 @@ struct ScheduleLayout {
       ws_strip, ws_tiles, ws_hist, ws_sums, ws_total;
   int64_t ntiles, nscan;
   int row_bits, cell_bits, pixel_bits, strip_bits;
+  // workspace of the build by strips in LDS (schedule_local.hip)
+  size_t wl_map, wl_rkey, wl_rnpts, wl_strip_np, wl_strip_p0, wl_strip_it0, wl_pix_count,
+      wl_item_nseg, wl_cell_nseg, wl_fill, wl_slot0, wl_head_cell, wl_slot_seg, wl_total;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
+
+// Build by strips in LDS: usable when a strip's frustum points fit one
+// workgroup's LDS sort (pixels * D <= kLocalPoints, pixels <= 256) and the
+// sort key (cell within the sample, local pixel, depth bin) fits 32 bits.
+constexpr int kLocalPoints = 12288;
+bool schedule_local_ok(const Dims& d, int64_t n_valid);
+void local_schedule_ws(const Dims& d, ScheduleLayout& L);
+hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t* rb,
+                                 int32_t n_valid, int32_t n_intervals, void* schedule,
+                                 void* workspace, hipStream_t stream);
 // Compute units of the current device (cached per device).
 int device_cus();
 // Workgroups of the scheduled forward on the current device: one per CU,

@@ -15,6 +15,7 @@
 
 #include "device_utils.h"
 #include "internal.h"
+#include "schedule_items.h"
 
 namespace bevpool {
 
@@ -604,40 +605,6 @@ __global__ void k_strips_end(const int32_t* __restrict__ hdr, int32_t* __restric
   if (threadIdx.x == 0 && blockIdx.x == 0) strip_p0[hdr[kHdrStrips]] = hdr[kHdrPairs];
 }
 
-// Share boundary w, floor(P * w / S), moved to the start or end of the strip
-// [a, b) it falls in when within kMinPiece pairs of it, so that no item is
-// a small remnant of a strip.
-__device__ __forceinline__ int64_t snap_bound(int64_t c, int64_t a, int64_t b) {
-  if (c - a < kMinPiece) return a;
-  if (b - c < kMinPiece) return b;
-  return c;
-}
-
-// The items of strip j: its pairs [a, b) are cut at the (snapped) share
-// boundaries inside (a, b), and each piece of L pairs into ceil(L /
-// kItemPairs) items starting at floor(i * L / K) of the piece.  visit(i,
-// first) is called for every item start in order; returns the count.
-template <typename F>
-__device__ int64_t strip_items(int64_t a, int64_t b, int64_t P, int64_t S, F visit) {
-  // shares w with a < floor(P w / S) < b: floor(P w / S) > a  <=>
-  // w >= ceil((a + 1) S / P); floor(P w / S) < b  <=>  w < ceil(b S / P)
-  const int64_t w_lo = ((a + 1) * S + P - 1) / P;
-  const int64_t w_hi = (b * S + P - 1) / P - 1;
-  int64_t n = 0;
-  int64_t q = a;
-  for (int64_t w = w_lo; w <= w_hi + 1; ++w) {
-    const int64_t e = w <= w_hi ? snap_bound((P * w) / S, a, b) : b;  // end of this piece
-    const int64_t L = e - q;
-    if (L > 0) {
-      const int64_t K = (L + kItemPairs - 1) / kItemPairs;
-      for (int64_t i = 0; i < K; ++i) visit(n + i, q + (i * L) / K);
-      n += K;
-      q = e;
-    }
-  }
-  return n;
-}
-
 // Items of every listed strip (0 past the last one, up to cap).
 __global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
                                                      const int32_t* __restrict__ strip_p0,
@@ -772,16 +739,6 @@ __global__ __launch_bounds__(256) void k_seg_flags(const int32_t* __restrict__ h
   const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= cap) return;
   flags[k] = (k < hdr[kHdrPairs] && segment_head(k, item_flag, pair_rb)) ? 1 : 0;
-}
-
-// Largest index i in [0, n) with a[i] <= v (a ascending, a[0] <= v).
-__device__ __forceinline__ int32_t upper_index(const int32_t* __restrict__ a, int32_t n, int32_t v) {
-  int32_t lo = 0, hi = n - 1;
-  while (lo < hi) {
-    const int32_t mid = (lo + hi + 1) >> 1;
-    if (a[mid] <= v) lo = mid; else hi = mid - 1;
-  }
-  return lo;
 }
 
 // With the segment flags exclusively scanned into `before`: each pair's
@@ -1071,6 +1028,8 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
   L.ws_hist = take((size_t)(256 * L.ntiles));
   L.ws_sums = take((size_t)L.nscan + 1);
   L.ws_total = off;
+  local_schedule_ws(d, L);
+  if (schedule_local_ok(d, n_valid)) L.ws_total = std::max(L.ws_total, L.wl_total);
   L.row_bits = bit_length(d.rows);
   L.cell_bits = bit_length(d.cells);
   L.pixel_bits = bit_length(L.sd.pixels);
@@ -1081,6 +1040,8 @@ ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_interva
 hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, int32_t n_valid,
                            int32_t n_intervals, void* schedule, void* workspace,
                            hipStream_t stream) {
+  if (schedule_local_ok(d, n_valid))
+    return launch_schedule_local(d, rd, rb, n_valid, n_intervals, schedule, workspace, stream);
   const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
   char* sc = static_cast<char*>(schedule);
   char* ws = static_cast<char*>(workspace);

@@ -1,0 +1,706 @@
+// Schedule build with each image strip regrouped inside one workgroup's LDS.
+//
+// The schedule (definitions in internal.h) orders the kept points of a plan
+// by (strip, BEV rank, local pixel, depth bin).  A strip's points are a small
+// set (bh x bw pixels x D bins), so instead of sorting all kept points
+// globally, one workgroup per strip gathers its kept points from a map of
+// frustum point -> BEV rank, sorts them in LDS and forms its pairs.  What
+// needs the whole plan (pair offsets, items and shares, pixel offsets,
+// segment offsets, slots, empty cells) is done by single-block scans and two
+// flat passes.  The result is bit for bit the schedule of the general
+// builder (prepare.hip), which remains for shapes whose strips exceed the
+// LDS bounds below.
+//
+// Launches: init, map, strips, plan, emit, cells, segments, slots.
+
+#include <algorithm>
+
+#include "device_utils.h"
+#include "internal.h"
+#include "schedule_items.h"
+
+namespace bevpool {
+
+namespace {
+
+constexpr int kLT = 1024;                  // threads of the per-strip kernels
+constexpr int kLW = kLT / kWave;           // 16 waves
+constexpr int kLR = kLocalPoints / kLT;    // 12 rounds of 64 lanes per wave
+constexpr int kLBuckets = 256;             // digits of one LDS sort pass (8 bits)
+constexpr int kLItems = kMaxShares + kLocalPoints / kItemPairs + 2;  // items of one strip
+static_assert(kLocalPoints % kLT == 0, "whole rounds");
+
+struct LGeom {
+  int32_t N, D, H, W, bh, bw, nhb, nwb, strips;
+  int32_t hw;      // H * W
+  int32_t zyx;     // cells of one sample
+  int32_t maxpts;  // bh * bw * D: region entries per strip
+  int d_bits, lp_bits, rb_bits;
+  // strip s: sample-view bn, first row h0 and column w0, its height and width
+  __device__ void strip(int32_t s, int32_t& bn, int32_t& h0, int32_t& w0, int32_t& bhs,
+                        int32_t& bws) const {
+    const int32_t wb = s % nwb;
+    const int32_t t = s / nwb;
+    const int32_t hb = t % nhb;
+    bn = t / nhb;
+    h0 = hb * bh;
+    w0 = wb * bw;
+    bhs = min(bh, H - h0);
+    bws = min(bw, W - w0);
+  }
+};
+
+// One stable counting pass over the n elements held by a workgroup in the
+// wave-round layout (element e = wave * span + round * 64 + lane): returns in
+// dest[r] each element's position in the order of digit, then element.  cnt
+// is kLW x kLBuckets ints of LDS; afterwards cnt[0][d] holds the first
+// position of digit d.  Every thread of the block must call it.
+__device__ void local_ranks(const uint32_t (&digit)[kLR], int n, int span, int bits,
+                            int32_t (*cnt)[kLBuckets], int32_t* s_scan, int32_t (&dest)[kLR]) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const int t = threadIdx.x;
+  for (int i = t; i < kLW * kLBuckets; i += kLT) (&cnt[0][0])[i] = 0;
+  __syncthreads();
+  const int rounds = span / kWave;
+  int32_t rank[kLR];
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    const bool valid = r < rounds && e < n;
+    uint64_t same = wave_ballot(valid);
+    for (int b = 0; b < bits; ++b) {
+      const bool bit = (digit[r] >> b) & 1u;
+      const uint64_t bb = wave_ballot(bit);
+      same &= bit ? bb : ~bb;
+    }
+    const int below = rank_below(same);
+    int prior = 0;
+    if (valid) prior = cnt[wid][digit[r]];
+    if (valid && below == 0) cnt[wid][digit[r]] = prior + __popcll(same);
+    rank[r] = prior + below;
+  }
+  __syncthreads();
+  int tot = 0;  // digit t: each wave's offset within the digit, and the digit's count
+  if (t < kLBuckets) {
+    for (int w = 0; w < kLW; ++w) {
+      const int c = cnt[w][t];
+      cnt[w][t] = tot;
+      tot += c;
+    }
+  }
+  int total;
+  const int start = block_exclusive_scan<kLT>(tot, s_scan, &total);
+  if (t < kLBuckets)
+    for (int w = 0; w < kLW; ++w) cnt[w][t] += start;
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) dest[r] = cnt[wid][digit[r]] + rank[r];
+}
+
+// Block-wide exclusive scan of per-wave counts: every lane gets the number of
+// items counted by earlier waves, and *total the block's count.
+__device__ int wave_offsets(int wave_count, int32_t* s_scan, int* total) {
+  const int lane = lane_id();
+  const int off = block_exclusive_scan<kLT>(lane == 0 ? wave_count : 0, s_scan, total);
+  return __shfl(off, 0, kWave);
+}
+
+// ---------------------------------------------------------------- kernels
+
+__global__ __launch_bounds__(256) void k_ls_init(int32_t* __restrict__ map, int64_t P,
+                                                 int32_t* __restrict__ cnt,
+                                                 int32_t* __restrict__ fill, int64_t cells,
+                                                 int32_t* __restrict__ hdr, int32_t n_valid,
+                                                 int32_t n_occ) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < P) map[i] = -1;
+  if (i < cells) {
+    cnt[i] = 0;
+    fill[i] = 0;
+  }
+  if (i < 16) hdr[i] = i == kHdrValid ? n_valid : (i == kHdrOcc ? n_occ : 0);
+}
+
+// map[p] = BEV rank of kept point p (points outside the shape's ranges are
+// skipped, so the map is never written out of bounds).
+__global__ __launch_bounds__(256) void k_ls_map(const int32_t* __restrict__ rd,
+                                                const int32_t* __restrict__ rb, int64_t n,
+                                                int64_t P, int64_t cells,
+                                                int32_t* __restrict__ map) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n) return;
+  const int32_t p = rd[i], r = rb[i];
+  if (p >= 0 && p < P && r >= 0 && r < cells) map[p] = r;
+}
+
+// One workgroup per strip: its kept points sorted by (BEV rank, local pixel,
+// depth bin) in LDS, cut into pairs; the pairs go to the strip's region
+// (key = rank within the sample << (lp_bits + d_bits) | pixel << d_bits |
+// first bin, and the point count), with the strip's pair count and the pair
+// count of each of its pixels.
+__global__ __launch_bounds__(kLT) void k_ls_strips(const int32_t* __restrict__ map, LGeom g,
+                                                   uint32_t* __restrict__ rkey,
+                                                   int32_t* __restrict__ rnpts,
+                                                   int32_t* __restrict__ strip_np,
+                                                   int32_t* __restrict__ pix_count) {
+  __shared__ uint32_t sa[kLocalPoints], sb[kLocalPoints];
+  __shared__ int32_t cnt[kLW][kLBuckets];
+  __shared__ int32_t s_scan[kLW];
+  __shared__ int32_t pc[kLBuckets];
+  __shared__ int32_t s_n;
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = t / kWave;
+  const int32_t s = blockIdx.x;
+  int32_t bn, h0, w0, bhs, bws;
+  g.strip(s, bn, h0, w0, bhs, bws);
+  const int32_t npix = bhs * bws;
+  const int32_t nf = g.D * npix;  // frustum points of the strip (<= kLocalPoints)
+  const int32_t rb_base = (bn / g.N) * g.zyx;
+  if (t == 0) s_n = 0;
+  if (t < kLBuckets) pc[t] = 0;
+  __syncthreads();
+
+  // kept points, in any order (the keys are unique, the sort fixes the order)
+  constexpr int kBatch = 4;
+  for (int32_t j0 = 0; j0 < nf; j0 += kBatch * kLT) {
+    int32_t r[kBatch];
+    int32_t jj[kBatch];
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int32_t j = j0 + q * kLT + t;
+      jj[q] = j;
+      r[q] = -1;
+      if (j < nf) {
+        const int32_t d = j / npix;
+        const int32_t lp = j - d * npix;
+        const int32_t hl = lp / bws;
+        const int64_t p = ((int64_t)(bn * g.D + d) * g.H + h0 + hl) * g.W + w0 + (lp - hl * bws);
+        r[q] = map[p];
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < kBatch; ++q) {
+      const int32_t rel = r[q] - rb_base;
+      const bool kept = r[q] >= 0 && rel >= 0 && rel < g.zyx;
+      const uint64_t m = wave_ballot(kept);
+      int base = 0;
+      if (lane == 0 && m != 0) base = atomicAdd(&s_n, __popcll(m));
+      base = __shfl(base, 0, kWave);
+      if (kept) {
+        const int32_t d = jj[q] / npix;
+        const int32_t lp = jj[q] - d * npix;
+        sa[base + rank_below(m)] =
+            ((uint32_t)rel << (g.lp_bits + g.d_bits)) | ((uint32_t)lp << g.d_bits) | (uint32_t)d;
+      }
+    }
+  }
+  __syncthreads();
+  const int n = s_n;
+  const int span = ((n + kLT - 1) / kLT) * kWave;  // elements per wave
+  uint32_t* src = sa;
+  uint32_t* dst = sb;
+  const int total_bits = g.rb_bits + g.lp_bits + g.d_bits;  // <= 32
+  if (n > 1 && total_bits > 0) {
+    const int passes = (total_bits + 7) / 8;
+    const int pbits = (total_bits + passes - 1) / passes;
+    for (int ps = 0; ps < passes; ++ps) {
+      const int shift = ps * pbits;
+      const int bits = min(pbits, total_bits - shift);
+      const uint32_t mask = (1u << bits) - 1u;
+      uint32_t key[kLR], digit[kLR];
+      int32_t dest[kLR];
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {
+        const int e = wid * span + r * kWave + lane;
+        key[r] = (r * kWave < span && e < n) ? src[e] : 0u;
+        digit[r] = (key[r] >> shift) & mask;
+      }
+      local_ranks(digit, n, span, bits, cnt, s_scan, dest);
+#pragma unroll
+      for (int r = 0; r < kLR; ++r) {
+        const int e = wid * span + r * kWave + lane;
+        if (r * kWave < span && e < n) dst[dest[r]] = key[r];
+      }
+      __syncthreads();
+      uint32_t* tmp = src;
+      src = dst;
+      dst = tmp;
+    }
+  }
+
+  // pairs: a head where the cell or pixel changes or the bin is not the next
+  const uint32_t dmask = (1u << g.d_bits) - 1u;
+  const uint32_t lpmask = (1u << g.lp_bits) - 1u;
+  int pre[kLR];
+  bool hd[kLR];
+  int wcount = 0;
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    const bool valid = r * kWave < span && e < n;
+    const uint32_t k = valid ? src[e] : 0u;
+    const uint32_t pk = (valid && e > 0) ? src[e - 1] : 0u;
+    hd[r] = valid && (e == 0 || (k >> g.d_bits) != (pk >> g.d_bits) ||
+                      (k & dmask) != (pk & dmask) + 1u);
+    const uint64_t m = wave_ballot(hd[r]);
+    pre[r] = wcount + rank_below(m);
+    wcount += __popcll(m);
+  }
+  int np;
+  const int woff = wave_offsets(wcount, s_scan, &np);
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    if (hd[r]) dst[woff + pre[r]] = (uint32_t)e;  // head position of each pair
+  }
+  __syncthreads();
+  const int64_t region = (int64_t)s * g.maxpts;
+  for (int j = t; j < np; j += kLT) {
+    const int e0 = (int)dst[j];
+    const int e1 = j + 1 < np ? (int)dst[j + 1] : n;
+    const uint32_t key = src[e0];
+    rkey[region + j] = key;
+    rnpts[region + j] = e1 - e0;
+    atomicAdd(&pc[(key >> g.d_bits) & lpmask], 1);
+  }
+  __syncthreads();
+  for (int lp = t; lp < npix; lp += kLT) {
+    const int32_t hl = lp / bws;
+    pix_count[(int64_t)bn * g.hw + (int64_t)(h0 + hl) * g.W + w0 + (lp - hl * bws)] = pc[lp];
+  }
+  if (t == 0) strip_np[s] = np;
+}
+
+// One block: pair offsets of the strips, the items (cut at the shares) and
+// their strips and first pairs, the shares' first items, and the first
+// pixel-major pair of every feature row.
+__global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ strip_np,
+                                                 int32_t strips, int32_t shares,
+                                                 int64_t items_cap, const int32_t* __restrict__ pix_count,
+                                                 int64_t rows, int32_t* __restrict__ strip_p0,
+                                                 int32_t* __restrict__ strip_it0,
+                                                 int32_t* __restrict__ hdr,
+                                                 int32_t* __restrict__ item_strip,
+                                                 int32_t* __restrict__ item_pair0,
+                                                 int32_t* __restrict__ share_item0,
+                                                 int32_t* __restrict__ pix_pair0) {
+  __shared__ int32_t s_scan[kLW];
+  __shared__ int32_t s_bad;
+  const int t = threadIdx.x;
+  if (t == 0) s_bad = 0;
+  // 1. pair offsets (contiguous strips per thread)
+  const int32_t per = (strips + kLT - 1) / kLT;
+  const int32_t s_lo = min(strips, t * per), s_hi = min(strips, s_lo + per);
+  int32_t sum = 0, ne = 0;
+  for (int32_t s = s_lo; s < s_hi; ++s) {
+    const int32_t v = strip_np[s];
+    sum += v;
+    ne += v > 0 ? 1 : 0;
+  }
+  int32_t P, n_strips;
+  int32_t off = block_exclusive_scan<kLT>(sum, s_scan, &P);
+  block_exclusive_scan<kLT>(ne, s_scan, &n_strips);
+  // 2. items of every strip
+  int64_t isum = 0;
+  {
+    int32_t a = off;
+    for (int32_t s = s_lo; s < s_hi; ++s) {
+      const int32_t v = strip_np[s];
+      strip_p0[s] = a;
+      if (v > 0) isum += strip_items(a, a + v, P, shares, [](int64_t, int64_t) {});
+      a += v;
+    }
+  }
+  int32_t n_items;
+  int32_t ioff = block_exclusive_scan<kLT>((int32_t)isum, s_scan, &n_items);
+  {
+    int32_t a = off;
+    for (int32_t s = s_lo; s < s_hi; ++s) {
+      const int32_t v = strip_np[s];
+      strip_it0[s] = ioff;
+      if (v > 0) {
+        const int32_t first_item = ioff;
+        ioff += (int32_t)strip_items(a, a + v, P, shares, [&](int64_t i, int64_t first) {
+          const int64_t item = first_item + i;
+          if (item < items_cap) {
+            item_strip[item] = s;
+            item_pair0[item] = (int32_t)first;
+          }
+        });
+      }
+      a += v;
+    }
+  }
+  if (t == 0) {
+    strip_p0[strips] = P;
+    strip_it0[strips] = n_items;
+    if (n_items <= items_cap) item_pair0[n_items] = P;
+    hdr[kHdrPairs] = P;
+    hdr[kHdrItems] = n_items;
+    hdr[kHdrStrips] = n_strips;
+  }
+  __syncthreads();  // (the block's global writes above are visible to it after the barrier)
+  // 3. shares: boundary w snapped within its strip, then the first item at
+  // or after it
+  const int32_t n_it = (int32_t)min<int64_t>(n_items, items_cap);
+  for (int w = t; w <= shares; w += kLT) {
+    int64_t c = ((int64_t)P * w) / shares;
+    if (c > 0 && c < P) {  // the last strip starting at or before c holds it
+      int32_t lo = 0, hi = strips - 1;
+      while (lo < hi) {
+        const int32_t mid = (lo + hi + 1) >> 1;
+        if (strip_p0[mid] <= c) lo = mid; else hi = mid - 1;
+      }
+      c = snap_bound(c, strip_p0[lo], strip_p0[lo + 1]);
+    }
+    int32_t lo = 0, hi = n_it;
+    while (lo < hi) {
+      const int32_t mid = (lo + hi) >> 1;
+      if (item_pair0[mid] < c) lo = mid + 1; else hi = mid;
+    }
+    share_item0[w] = lo;
+  }
+  __syncthreads();
+  for (int w = t; w < shares; w += kLT)
+    if (share_item0[w + 1] - share_item0[w] > kShareItems) s_bad = 1;
+  // 4. first pixel-major pair of every feature row
+  const int64_t rper = (rows + kLT - 1) / kLT;
+  const int64_t r_lo = min<int64_t>(rows, t * rper), r_hi = min<int64_t>(rows, r_lo + rper);
+  int32_t rsum = 0;
+  for (int64_t r = r_lo; r < r_hi; ++r) rsum += pix_count[r];
+  int32_t rtot;
+  int32_t roff = block_exclusive_scan<kLT>(rsum, s_scan, &rtot);
+  for (int64_t r = r_lo; r < r_hi; ++r) {
+    const int32_t v = pix_count[r];
+    pix_pair0[r] = roff;
+    roff += v;
+  }
+  __syncthreads();
+  if (t == 0) {
+    pix_pair0[rows] = rtot;
+    hdr[kHdrShares] = shares;
+    hdr[kHdrSharesOk] = s_bad ? 0 : 1;
+  }
+}
+
+// One workgroup per strip: the pair records at their global positions, the
+// segment index of each pair within its item, the segment count of each
+// item, the segment count of each cell, the BEV rank of each segment's first
+// pair, and the pixel-major pairs.
+__global__ __launch_bounds__(kLT) void k_ls_emit(
+    LGeom g, const uint32_t* __restrict__ rkey, const int32_t* __restrict__ rnpts,
+    const int32_t* __restrict__ strip_np, const int32_t* __restrict__ strip_p0,
+    const int32_t* __restrict__ strip_it0, const int32_t* __restrict__ item_pair0,
+    int64_t items_cap, const int32_t* __restrict__ pix_pair0, int32_t* __restrict__ item_nseg,
+    int32_t* __restrict__ cell_nseg, int32_t* __restrict__ head_cell,
+    int32_t* __restrict__ pair_rd0, uint32_t* __restrict__ pair_ln,
+    uint16_t* __restrict__ pair_seg, int32_t* __restrict__ bp_cell,
+    uint32_t* __restrict__ bp_dn) {
+  __shared__ int32_t cnt[kLW][kLBuckets];
+  __shared__ int32_t s_scan[kLW];
+  __shared__ int32_t s_items[kLItems + 1];
+  __shared__ int32_t s_iseg[kLItems + 1];
+  const int t = threadIdx.x;
+  const int lane = lane_id();
+  const int wid = t / kWave;
+  const int32_t s = blockIdx.x;
+  const int np = strip_np[s];
+  if (np == 0) return;  // (uniform over the block)
+  const int32_t P0 = strip_p0[s];
+  const int32_t it0 = strip_it0[s];
+  const int32_t K = strip_it0[s + 1] - it0;
+  if (K < 1 || K > kLItems || (int64_t)it0 + K > items_cap) return;  // (cannot happen)
+  int32_t bn, h0, w0, bhs, bws;
+  g.strip(s, bn, h0, w0, bhs, bws);
+  const int32_t rb_base = (bn / g.N) * g.zyx;
+  for (int k = t; k <= K; k += kLT) s_items[k] = item_pair0[it0 + k];
+  __syncthreads();
+
+  const int span = ((np + kLT - 1) / kLT) * kWave;
+  const int64_t region = (int64_t)s * g.maxpts;
+  const int rb_shift = g.lp_bits + g.d_bits;
+  const uint32_t dmask = (1u << g.d_bits) - 1u;
+  const uint32_t lpmask = (1u << g.lp_bits) - 1u;
+  uint32_t key[kLR], digit[kLR];
+  int32_t npts[kLR], item[kLR], sin[kLR];
+  bool hd[kLR];
+  int wcount = 0;
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    const bool valid = r * kWave < span && e < np;
+    key[r] = valid ? rkey[region + e] : 0u;
+    const uint32_t pk = (valid && e > 0) ? rkey[region + e - 1] : 0u;
+    npts[r] = valid ? rnpts[region + e] : 0;
+    const int32_t gp = P0 + e;
+    item[r] = valid ? upper_index(s_items, K, gp) : 0;
+    const bool start = valid && s_items[item[r]] == gp;
+    hd[r] = valid && (start || (key[r] >> rb_shift) != (pk >> rb_shift));
+    const uint64_t m = wave_ballot(hd[r]);
+    sin[r] = wcount + rank_below(m) + (hd[r] ? 1 : 0);  // inclusive, within the wave
+    wcount += __popcll(m);
+    digit[r] = (key[r] >> g.d_bits) & lpmask;
+  }
+  int nseg;
+  const int woff = wave_offsets(wcount, s_scan, &nseg);
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    sin[r] += woff - 1;  // segment of the pair within the strip
+    const int e = wid * span + r * kWave + lane;
+    if (r * kWave < span && e < np && s_items[item[r]] == P0 + e) s_iseg[item[r]] = sin[r];
+  }
+  __syncthreads();
+  for (int k = t; k < K; k += kLT)
+    item_nseg[it0 + k] = (k + 1 < K ? s_iseg[k + 1] : nseg) - s_iseg[k];
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    if (!(r * kWave < span && e < np)) continue;
+    const int32_t gp = P0 + e;
+    const uint32_t lp = (key[r] >> g.d_bits) & lpmask;
+    const int32_t d0 = (int32_t)(key[r] & dmask);
+    const int32_t hl = (int32_t)lp / bws;
+    const int32_t cell = rb_base + (int32_t)(key[r] >> rb_shift);
+    pair_rd0[gp] = (int32_t)(((int64_t)(bn * g.D + d0) * g.H + h0 + hl) * g.W + w0 +
+                             ((int32_t)lp - hl * bws));
+    pair_ln[gp] = (lp & kPairPixel) | (hd[r] ? kPairHead : 0u) | ((uint32_t)npts[r] << 16);
+    pair_seg[gp] = (uint16_t)(sin[r] - s_iseg[item[r]]);
+    if (hd[r]) {
+      atomicAdd(&cell_nseg[cell], 1);
+      head_cell[gp] = cell;
+    }
+  }
+  // pixel-major pairs: a stable pass by local pixel
+  int32_t dest[kLR];
+  local_ranks(digit, np, span, g.lp_bits, cnt, s_scan, dest);
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    const int e = wid * span + r * kWave + lane;
+    if (!(r * kWave < span && e < np)) continue;
+    const int32_t lp = (int32_t)digit[r];
+    const int32_t hl = lp / bws;
+    const int64_t row = (int64_t)bn * g.hw + (int64_t)(h0 + hl) * g.W + w0 + (lp - hl * bws);
+    const int32_t q = pix_pair0[row] + (dest[r] - cnt[0][lp]);
+    bp_cell[q] = rb_base + (int32_t)(key[r] >> rb_shift);
+    bp_dn[q] = (key[r] & dmask) | ((uint32_t)npts[r] << 16);
+  }
+}
+
+// One block: the first segment of every item, and over the cells: the first
+// slot of each cell with several segments, the list of those cells, the
+// empty cells, and the counts in the header.
+__global__ __launch_bounds__(kLT) void k_ls_cells(
+    int32_t* __restrict__ hdr, const int32_t* __restrict__ item_nseg, int64_t items_cap,
+    const int32_t* __restrict__ cell_nseg, int64_t cells, int32_t* __restrict__ item_seg0,
+    int32_t* __restrict__ slot0, int32_t* __restrict__ comb_cell,
+    int32_t* __restrict__ comb_slot0, int64_t comb_cap, int32_t* __restrict__ empty,
+    int64_t empty_cap) {
+  __shared__ int32_t s_scan[kLW];
+  const int t = threadIdx.x;
+  const int64_t n_items = min<int64_t>(hdr[kHdrItems], items_cap);
+  const int64_t iper = (n_items + kLT - 1) / kLT;
+  const int64_t i_lo = min<int64_t>(n_items, t * iper), i_hi = min<int64_t>(n_items, i_lo + iper);
+  int32_t isum = 0;
+  for (int64_t i = i_lo; i < i_hi; ++i) isum += item_nseg[i];
+  int32_t n_segs;
+  int32_t ioff = block_exclusive_scan<kLT>(isum, s_scan, &n_segs);
+  for (int64_t i = i_lo; i < i_hi; ++i) {
+    item_seg0[i] = ioff;
+    ioff += item_nseg[i];
+  }
+  const int64_t cper = (cells + kLT - 1) / kLT;
+  const int64_t c_lo = min<int64_t>(cells, t * cper), c_hi = min<int64_t>(cells, c_lo + cper);
+  int32_t ss = 0, sc = 0, se = 0;
+  for (int64_t c = c_lo; c < c_hi; ++c) {
+    const int32_t k = cell_nseg[c];
+    ss += k > 1 ? k : 0;
+    sc += k > 1 ? 1 : 0;
+    se += k == 0 ? 1 : 0;
+  }
+  int32_t n_slots, n_comb, n_empty;
+  int32_t so = block_exclusive_scan<kLT>(ss, s_scan, &n_slots);
+  int32_t co = block_exclusive_scan<kLT>(sc, s_scan, &n_comb);
+  int32_t eo = block_exclusive_scan<kLT>(se, s_scan, &n_empty);
+  for (int64_t c = c_lo; c < c_hi; ++c) {
+    const int32_t k = cell_nseg[c];
+    if (k > 1) {
+      slot0[c] = so;
+      if (co < comb_cap) {
+        comb_cell[co] = (int32_t)c;
+        comb_slot0[co] = so;
+      }
+      so += k;
+      ++co;
+    } else if (k == 0) {
+      if (eo < empty_cap) empty[eo] = (int32_t)c;
+      ++eo;
+    }
+  }
+  if (t == 0) {
+    if (n_items == hdr[kHdrItems]) item_seg0[n_items] = n_segs;
+    comb_slot0[min<int64_t>(n_comb, comb_cap)] = n_slots;
+    hdr[kHdrSegs] = n_segs;
+    hdr[kHdrSlots] = n_slots;
+    hdr[kHdrComb] = n_comb;
+    hdr[kHdrEmpty] = n_empty;
+    hdr[kHdrOccFound] = (int32_t)(cells - n_empty);
+  }
+}
+
+// Every segment: its destination when its cell has no other segment; else
+// its index joins its cell's list of slots (in any order; sorted below).
+__global__ __launch_bounds__(256) void k_ls_segments(
+    const int32_t* __restrict__ hdr, int64_t items_cap, const uint32_t* __restrict__ pair_ln,
+    const uint16_t* __restrict__ pair_seg, const int32_t* __restrict__ head_cell,
+    const int32_t* __restrict__ item_pair0, const int32_t* __restrict__ item_seg0,
+    const int32_t* __restrict__ cell_nseg, const int32_t* __restrict__ slot0,
+    int32_t* __restrict__ fill, int32_t* __restrict__ slot_seg, int32_t* __restrict__ seg_dest) {
+  const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (k >= hdr[kHdrPairs] || !(pair_ln[k] & kPairHead)) return;
+  const int32_t n_items = (int32_t)min<int64_t>(hdr[kHdrItems], items_cap);
+  if (n_items < 1) return;
+  const int32_t it = upper_index(item_pair0, n_items, (int32_t)k);
+  const int32_t seg = item_seg0[it] + pair_seg[k];
+  const int32_t cell = head_cell[k];
+  if (cell_nseg[cell] == 1) {
+    seg_dest[seg] = cell;
+  } else {
+    slot_seg[slot0[cell] + atomicAdd(&fill[cell], 1)] = seg;
+  }
+}
+
+// Every cell with several segments: its segments in ascending order get its
+// slots in order.
+__global__ __launch_bounds__(256) void k_ls_slots(const int32_t* __restrict__ cell_nseg,
+                                                  int64_t cells, const int32_t* __restrict__ slot0,
+                                                  int32_t* __restrict__ slot_seg,
+                                                  int32_t* __restrict__ seg_dest) {
+  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (c >= cells) return;
+  const int32_t k = cell_nseg[c];
+  if (k < 2) return;
+  int32_t* a = slot_seg + slot0[c];
+  for (int32_t i = 1; i < k; ++i) {  // insertion sort (a cell has few segments)
+    const int32_t v = a[i];
+    int32_t j = i - 1;
+    while (j >= 0 && a[j] > v) {
+      a[j + 1] = a[j];
+      --j;
+    }
+    a[j + 1] = v;
+  }
+  for (int32_t i = 0; i < k; ++i) seg_dest[a[i]] = ~(slot0[c] + i);
+}
+
+int bits_for(int64_t n) {  // bits of the values 0 .. n - 1
+  int b = 0;
+  while ((int64_t(1) << b) < n) ++b;
+  return b;
+}
+
+}  // namespace
+
+bool schedule_local_ok(const Dims& d, int64_t n_valid) {
+  const StripDims sd = strip_dims(d);
+  if (n_valid <= 0) return false;
+  if (sd.pixels > kLBuckets || sd.pixels * d.D > kLocalPoints) return false;
+  if (sd.strips > INT32_MAX - 1) return false;
+  const int64_t zyx = d.Z * d.Y * d.X;
+  return bits_for(zyx) + bits_for(sd.pixels) + bits_for(d.D) <= 32;
+}
+
+void local_schedule_ws(const Dims& d, ScheduleLayout& L) {
+  size_t off = 0;
+  auto take = [&](size_t n_ints) {
+    const size_t o = off;
+    off += (sizeof(int32_t) * n_ints + 255) & ~size_t(255);
+    return o;
+  };
+  const size_t nv = (size_t)(L.n_valid > 0 ? L.n_valid : 1);
+  const size_t region = (size_t)L.sd.strips * (size_t)(L.sd.pixels * d.D);
+  L.wl_map = take((size_t)d.P);
+  L.wl_rkey = take(region);
+  L.wl_rnpts = take(region);
+  L.wl_strip_np = take((size_t)L.sd.strips + 1);
+  L.wl_strip_p0 = take((size_t)L.sd.strips + 1);
+  L.wl_strip_it0 = take((size_t)L.sd.strips + 1);
+  L.wl_pix_count = take((size_t)d.rows);
+  L.wl_item_nseg = take((size_t)L.items_cap + 1);
+  L.wl_cell_nseg = take((size_t)d.cells);
+  L.wl_fill = take((size_t)d.cells);
+  L.wl_slot0 = take((size_t)d.cells);
+  L.wl_head_cell = take(nv);
+  L.wl_slot_seg = take(nv);
+  L.wl_total = off;
+}
+
+hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t* rb,
+                                 int32_t n_valid, int32_t n_intervals, void* schedule,
+                                 void* workspace, hipStream_t stream) {
+  const ScheduleLayout L = schedule_layout(d, n_valid, n_intervals);
+  char* sc = static_cast<char*>(schedule);
+  char* ws = static_cast<char*>(workspace);
+  auto S = [&](size_t o) { return reinterpret_cast<int32_t*>(sc + o); };
+  auto W = [&](size_t o) { return reinterpret_cast<int32_t*>(ws + o); };
+  int32_t* hdr = S(L.header);
+  LGeom g{};
+  g.N = (int32_t)d.N;
+  g.D = (int32_t)d.D;
+  g.H = (int32_t)d.H;
+  g.W = (int32_t)d.W;
+  g.bh = (int32_t)L.sd.bh;
+  g.bw = (int32_t)L.sd.bw;
+  g.nhb = (int32_t)L.sd.nhb;
+  g.nwb = (int32_t)L.sd.nwb;
+  g.strips = (int32_t)L.sd.strips;
+  g.hw = (int32_t)d.hw;
+  g.zyx = (int32_t)(d.Z * d.Y * d.X);
+  g.maxpts = (int32_t)(L.sd.pixels * d.D);
+  g.d_bits = bits_for(d.D);
+  g.lp_bits = bits_for(L.sd.pixels);
+  g.rb_bits = bits_for(g.zyx);
+  const int32_t shares = (int32_t)std::min<int64_t>(forward_workgroups(), kMaxShares);
+  int32_t* map = W(L.wl_map);
+  uint32_t* rkey = reinterpret_cast<uint32_t*>(W(L.wl_rkey));
+  int32_t* rnpts = W(L.wl_rnpts);
+  int32_t* strip_np = W(L.wl_strip_np);
+  int32_t* strip_p0 = W(L.wl_strip_p0);
+  int32_t* strip_it0 = W(L.wl_strip_it0);
+  int32_t* pix_count = W(L.wl_pix_count);
+  int32_t* item_nseg = W(L.wl_item_nseg);
+  int32_t* cell_nseg = W(L.wl_cell_nseg);
+  int32_t* fill = W(L.wl_fill);
+  int32_t* slot0 = W(L.wl_slot0);
+  int32_t* head_cell = W(L.wl_head_cell);
+  int32_t* slot_seg = W(L.wl_slot_seg);
+
+  const int64_t span = std::max<int64_t>(std::max<int64_t>(d.P, d.cells), 16);
+  k_ls_init<<<(unsigned)((span + 255) / 256), 256, 0, stream>>>(map, d.P, cell_nseg, fill, d.cells,
+                                                                 hdr, n_valid, n_intervals);
+  const unsigned g_nv = (unsigned)((n_valid + 255) / 256);
+  k_ls_map<<<g_nv, 256, 0, stream>>>(rd, rb, n_valid, d.P, d.cells, map);
+  k_ls_strips<<<(unsigned)L.sd.strips, kLT, 0, stream>>>(map, g, rkey, rnpts, strip_np, pix_count);
+  k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, L.items_cap, pix_count, d.rows,
+                                   strip_p0, strip_it0, hdr, S(L.item_strip), S(L.item_pair0),
+                                   S(L.share_item0), S(L.pix_pair0));
+  k_ls_emit<<<(unsigned)L.sd.strips, kLT, 0, stream>>>(
+      g, rkey, rnpts, strip_np, strip_p0, strip_it0, S(L.item_pair0), L.items_cap, S(L.pix_pair0),
+      item_nseg, cell_nseg, head_cell, S(L.pair_rd0), reinterpret_cast<uint32_t*>(S(L.pair_ln)),
+      reinterpret_cast<uint16_t*>(S(L.pair_seg)), S(L.bp_cell),
+      reinterpret_cast<uint32_t*>(S(L.bp_dn)));
+  k_ls_cells<<<1, kLT, 0, stream>>>(hdr, item_nseg, L.items_cap, cell_nseg, d.cells, S(L.item_seg0),
+                                    slot0, S(L.comb_cell), S(L.comb_slot0), L.n_occ, S(L.empty),
+                                    L.n_empty);
+  k_ls_segments<<<g_nv, 256, 0, stream>>>(hdr, L.items_cap,
+                                          reinterpret_cast<const uint32_t*>(S(L.pair_ln)),
+                                          reinterpret_cast<const uint16_t*>(S(L.pair_seg)),
+                                          head_cell, S(L.item_pair0), S(L.item_seg0), cell_nseg,
+                                          slot0, fill, slot_seg, S(L.seg_dest));
+  k_ls_slots<<<(unsigned)((d.cells + 255) / 256), 256, 0, stream>>>(cell_nseg, d.cells, slot0,
+                                                                    slot_seg, S(L.seg_dest));
+  return hipGetLastError();
+}
+
+}  // namespace bevpool
