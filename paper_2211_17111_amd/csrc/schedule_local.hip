@@ -50,52 +50,95 @@ struct LGeom {
   }
 };
 
+// Strip of workgroup b: each die (workgroup b runs on die b % kXcds) takes a
+// contiguous run of strips, so that neighbouring strips, which read the same
+// cache lines of the map, share one L2.  -1 for the padding workgroups.
+__device__ __forceinline__ int32_t strip_of_block(int32_t strips) {
+  const int32_t per = (strips + kXcds - 1) / kXcds;
+  const int32_t b = blockIdx.x;
+  const int32_t s = (b % kXcds) * per + b / kXcds;
+  return s < strips ? s : -1;
+}
+
 // One stable counting pass over the n elements held by a workgroup in the
 // wave-round layout (element e = wave * span + round * 64 + lane): returns in
 // dest[r] each element's position in the order of digit, then element.  cnt
-// is kLW x kLBuckets ints of LDS; afterwards cnt[0][d] holds the first
-// position of digit d.  Every thread of the block must call it.
-__device__ void local_ranks(const uint32_t (&digit)[kLR], int n, int span, int bits,
-                            int32_t (*cnt)[kLBuckets], int32_t* s_scan, int32_t (&dest)[kLR]) {
+// is kLW x kLBuckets ints of LDS and match kLW x kLBuckets x 2 words; after
+// the pass cnt[0][d] holds the first position of digit d.  Every thread of
+// the block must call it.
+//
+// In a round, the lanes holding one digit are found by each lane setting its
+// bit in the wave's 64-bit mask for that digit (one LDS OR), reading the mask
+// back and clearing it; LDS applies one wave's operations in order, so the
+// rounds need no waits between them.  The lowest lane of each digit then
+// adds the digit's count to the wave's counter with a returning LDS add; the
+// adds of all rounds are issued before any result is used, and each returns
+// the count of that digit in the wave's earlier rounds.
+__device__ void local_ranks(const uint32_t (&digit)[kLR], int n, int span,
+                            int32_t (*cnt)[kLBuckets], uint32_t (*match)[kLBuckets][2],
+                            int32_t* s_scan, int32_t (&dest)[kLR]) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
   const int t = threadIdx.x;
   for (int i = t; i < kLW * kLBuckets; i += kLT) (&cnt[0][0])[i] = 0;
+  for (int i = t; i < kLW * kLBuckets * 2; i += kLT) (&match[0][0][0])[i] = 0u;
   __syncthreads();
   const int rounds = span / kWave;
+  uint2 m[kLR];
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    if (r >= rounds) continue;
+    const bool valid = wid * span + r * kWave + lane < n;
+    uint32_t* w = match[wid][digit[r]];
+    m[r] = make_uint2(0u, 0u);
+    if (valid) {
+      atomicOr(&w[lane >> 5], 1u << (lane & 31));
+      m[r] = *reinterpret_cast<const uint2*>(w);
+      *reinterpret_cast<uint2*>(w) = make_uint2(0u, 0u);
+    }
+  }
+  int32_t below[kLR], leader[kLR], old[kLR];
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    if (r >= rounds) continue;
+    const uint64_t same = (uint64_t)m[r].x | ((uint64_t)m[r].y << 32);
+    below[r] = rank_below(same);
+    leader[r] = same != 0 ? (int32_t)__builtin_ctzll(same) : lane;
+    old[r] = 0;
+    if (same != 0 && below[r] == 0) old[r] = atomicAdd(&cnt[wid][digit[r]], __popcll(same));
+  }
   int32_t rank[kLR];
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
-    const int e = wid * span + r * kWave + lane;
-    const bool valid = r < rounds && e < n;
-    uint64_t same = wave_ballot(valid);
-    for (int b = 0; b < bits; ++b) {
-      const bool bit = (digit[r] >> b) & 1u;
-      const uint64_t bb = wave_ballot(bit);
-      same &= bit ? bb : ~bb;
-    }
-    const int below = rank_below(same);
-    int prior = 0;
-    if (valid) prior = cnt[wid][digit[r]];
-    if (valid && below == 0) cnt[wid][digit[r]] = prior + __popcll(same);
-    rank[r] = prior + below;
+    if (r >= rounds) continue;
+    rank[r] = __shfl(old[r], leader[r], kWave) + below[r];
   }
   __syncthreads();
-  int tot = 0;  // digit t: each wave's offset within the digit, and the digit's count
+  // digit t: each wave's offset within the digit, and the digit's count
+  int32_t c[kLW];
+  int tot = 0;
   if (t < kLBuckets) {
+#pragma unroll
+    for (int w = 0; w < kLW; ++w) c[w] = cnt[w][t];
+#pragma unroll
     for (int w = 0; w < kLW; ++w) {
-      const int c = cnt[w][t];
-      cnt[w][t] = tot;
-      tot += c;
+      const int x = c[w];
+      c[w] = tot;
+      tot += x;
     }
   }
   int total;
   const int start = block_exclusive_scan<kLT>(tot, s_scan, &total);
-  if (t < kLBuckets)
-    for (int w = 0; w < kLW; ++w) cnt[w][t] += start;
+  if (t < kLBuckets) {
+#pragma unroll
+    for (int w = 0; w < kLW; ++w) cnt[w][t] = c[w] + start;
+  }
   __syncthreads();
 #pragma unroll
-  for (int r = 0; r < kLR; ++r) dest[r] = cnt[wid][digit[r]] + rank[r];
+  for (int r = 0; r < kLR; ++r) {
+    if (r >= rounds) continue;
+    dest[r] = cnt[wid][digit[r]] + rank[r];
+  }
 }
 
 // Block-wide exclusive scan of per-wave counts: every lane gets the number of
@@ -122,16 +165,31 @@ __global__ __launch_bounds__(256) void k_ls_init(int32_t* __restrict__ map, int6
   if (i < 16) hdr[i] = i == kHdrValid ? n_valid : (i == kHdrOcc ? n_occ : 0);
 }
 
-// map[p] = BEV rank of kept point p (points outside the shape's ranges are
-// skipped, so the map is never written out of bounds).
+// map[q] = BEV rank of kept point p, with q the point's place in its strip's
+// region (strip * maxpts + bin * pixels of the strip + local pixel), so that
+// a strip reads its points contiguously in frustum order.  Points outside
+// the shape's ranges are skipped: the map is never written out of bounds.
 __global__ __launch_bounds__(256) void k_ls_map(const int32_t* __restrict__ rd,
                                                 const int32_t* __restrict__ rb, int64_t n,
-                                                int64_t P, int64_t cells,
+                                                int64_t P, int64_t cells, LGeom g,
                                                 int32_t* __restrict__ map) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= n) return;
   const int32_t p = rd[i], r = rb[i];
-  if (p >= 0 && p < P && r >= 0 && r < cells) map[p] = r;
+  if (p < 0 || p >= P || r < 0 || r >= cells) return;
+  // (32-bit unsigned: p < 2^31)
+  const uint32_t per_view = (uint32_t)g.D * (uint32_t)g.hw;
+  const uint32_t bn = (uint32_t)p / per_view;
+  const uint32_t rem = (uint32_t)p - bn * per_view;
+  const uint32_t d = rem / (uint32_t)g.hw;
+  const uint32_t pix = rem - d * (uint32_t)g.hw;
+  const uint32_t h = pix / (uint32_t)g.W, w = pix - h * (uint32_t)g.W;
+  const uint32_t hb = h / (uint32_t)g.bh, wb = w / (uint32_t)g.bw;
+  const uint32_t h0 = hb * (uint32_t)g.bh, w0 = wb * (uint32_t)g.bw;
+  const uint32_t bws = min((uint32_t)g.bw, (uint32_t)g.W - w0);
+  const uint32_t bhs = min((uint32_t)g.bh, (uint32_t)g.H - h0);
+  const int64_t s = ((int64_t)bn * g.nhb + hb) * g.nwb + wb;
+  map[s * g.maxpts + (int64_t)d * (bhs * bws) + (h - h0) * bws + (w - w0)] = r;
 }
 
 // One workgroup per strip: its kept points sorted by (BEV rank, local pixel,
@@ -146,82 +204,84 @@ __global__ __launch_bounds__(kLT) void k_ls_strips(const int32_t* __restrict__ m
                                                    int32_t* __restrict__ pix_count) {
   __shared__ uint32_t sa[kLocalPoints], sb[kLocalPoints];
   __shared__ int32_t cnt[kLW][kLBuckets];
+  __shared__ uint32_t match[kLW][kLBuckets][2];
   __shared__ int32_t s_scan[kLW];
   __shared__ int32_t pc[kLBuckets];
-  __shared__ int32_t s_n;
   const int t = threadIdx.x;
   const int lane = lane_id();
   const int wid = t / kWave;
-  const int32_t s = blockIdx.x;
+  const int32_t s = strip_of_block(g.strips);
+  if (s < 0) return;  // (uniform over the block)
   int32_t bn, h0, w0, bhs, bws;
   g.strip(s, bn, h0, w0, bhs, bws);
   const int32_t npix = bhs * bws;
   const int32_t nf = g.D * npix;  // frustum points of the strip (<= kLocalPoints)
   const int32_t rb_base = (bn / g.N) * g.zyx;
-  if (t == 0) s_n = 0;
   if (t < kLBuckets) pc[t] = 0;
-  __syncthreads();
 
-  // kept points, in any order (the keys are unique, the sort fixes the order)
-  constexpr int kBatch = 4;
-  for (int32_t j0 = 0; j0 < nf; j0 += kBatch * kLT) {
-    int32_t r[kBatch];
-    int32_t jj[kBatch];
+  // kept points in frustum order (depth bin, then pixel): an ordered
+  // compaction, so that the points of one cell and pixel stay in bin order
+  const int spanf = ((nf + kLT - 1) / kLT) * kWave;  // frustum points per wave
+  const int roundsf = spanf / kWave;
+  const int32_t* smap = map + (int64_t)s * g.maxpts;  // the strip's points, in frustum order
+  int32_t rv[kLR];
 #pragma unroll
-    for (int q = 0; q < kBatch; ++q) {
-      const int32_t j = j0 + q * kLT + t;
-      jj[q] = j;
-      r[q] = -1;
-      if (j < nf) {
-        const int32_t d = j / npix;
-        const int32_t lp = j - d * npix;
-        const int32_t hl = lp / bws;
-        const int64_t p = ((int64_t)(bn * g.D + d) * g.H + h0 + hl) * g.W + w0 + (lp - hl * bws);
-        r[q] = map[p];
-      }
-    }
+  for (int r = 0; r < kLR; ++r) {
+    const int32_t j = wid * spanf + r * kWave + lane;
+    rv[r] = (r < roundsf && j < nf) ? smap[j] : -1;
+  }
+  int pre[kLR];
+  int wkept = 0;
 #pragma unroll
-    for (int q = 0; q < kBatch; ++q) {
-      const int32_t rel = r[q] - rb_base;
-      const bool kept = r[q] >= 0 && rel >= 0 && rel < g.zyx;
-      const uint64_t m = wave_ballot(kept);
-      int base = 0;
-      if (lane == 0 && m != 0) base = atomicAdd(&s_n, __popcll(m));
-      base = __shfl(base, 0, kWave);
-      if (kept) {
-        const int32_t d = jj[q] / npix;
-        const int32_t lp = jj[q] - d * npix;
-        sa[base + rank_below(m)] =
-            ((uint32_t)rel << (g.lp_bits + g.d_bits)) | ((uint32_t)lp << g.d_bits) | (uint32_t)d;
-      }
-    }
+  for (int r = 0; r < kLR; ++r) {
+    if (r >= roundsf) continue;
+    const int32_t rel = rv[r] - rb_base;
+    const bool kept = rv[r] >= 0 && rel >= 0 && rel < g.zyx;
+    if (!kept) rv[r] = -1;
+    const uint64_t m = wave_ballot(kept);
+    pre[r] = wkept + rank_below(m);
+    wkept += __popcll(m);
+  }
+  int n;
+  const int koff = wave_offsets(wkept, s_scan, &n);
+#pragma unroll
+  for (int r = 0; r < kLR; ++r) {
+    if (r >= roundsf) continue;
+    if (rv[r] < 0) continue;
+    const int32_t j = wid * spanf + r * kWave + lane;
+    const int32_t d = j / npix;
+    const int32_t lp = j - d * npix;
+    sa[koff + pre[r]] = ((uint32_t)(rv[r] - rb_base) << (g.lp_bits + g.d_bits)) |
+                        ((uint32_t)lp << g.d_bits) | (uint32_t)d;
   }
   __syncthreads();
-  const int n = s_n;
   const int span = ((n + kLT - 1) / kLT) * kWave;  // elements per wave
   uint32_t* src = sa;
   uint32_t* dst = sb;
-  const int total_bits = g.rb_bits + g.lp_bits + g.d_bits;  // <= 32
-  if (n > 1 && total_bits > 0) {
-    const int passes = (total_bits + 7) / 8;
-    const int pbits = (total_bits + passes - 1) / passes;
+  // stable LSD passes over (cell, pixel); the bins are already in order
+  const int sort_bits = g.rb_bits + g.lp_bits;  // + d_bits <= 32
+  if (n > 1 && sort_bits > 0) {
+    const int passes = (sort_bits + 7) / 8;
+    const int pbits = (sort_bits + passes - 1) / passes;
     for (int ps = 0; ps < passes; ++ps) {
-      const int shift = ps * pbits;
-      const int bits = min(pbits, total_bits - shift);
+      const int shift = g.d_bits + ps * pbits;
+      const int bits = min(pbits, sort_bits - ps * pbits);
       const uint32_t mask = (1u << bits) - 1u;
       uint32_t key[kLR], digit[kLR];
       int32_t dest[kLR];
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
+        if (r * kWave >= span) continue;
         const int e = wid * span + r * kWave + lane;
-        key[r] = (r * kWave < span && e < n) ? src[e] : 0u;
+        key[r] = e < n ? src[e] : 0u;
         digit[r] = (key[r] >> shift) & mask;
       }
-      local_ranks(digit, n, span, bits, cnt, s_scan, dest);
+      local_ranks(digit, n, span, cnt, match, s_scan, dest);
 #pragma unroll
       for (int r = 0; r < kLR; ++r) {
+        if (r * kWave >= span) continue;
         const int e = wid * span + r * kWave + lane;
-        if (r * kWave < span && e < n) dst[dest[r]] = key[r];
+        if (e < n) dst[dest[r]] = key[r];
       }
       __syncthreads();
       uint32_t* tmp = src;
@@ -233,13 +293,14 @@ __global__ __launch_bounds__(kLT) void k_ls_strips(const int32_t* __restrict__ m
   // pairs: a head where the cell or pixel changes or the bin is not the next
   const uint32_t dmask = (1u << g.d_bits) - 1u;
   const uint32_t lpmask = (1u << g.lp_bits) - 1u;
-  int pre[kLR];
   bool hd[kLR];
   int wcount = 0;
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    hd[r] = false;
+    if (r * kWave >= span) continue;
     const int e = wid * span + r * kWave + lane;
-    const bool valid = r * kWave < span && e < n;
+    const bool valid = e < n;
     const uint32_t k = valid ? src[e] : 0u;
     const uint32_t pk = (valid && e > 0) ? src[e - 1] : 0u;
     hd[r] = valid && (e == 0 || (k >> g.d_bits) != (pk >> g.d_bits) ||
@@ -252,6 +313,7 @@ __global__ __launch_bounds__(kLT) void k_ls_strips(const int32_t* __restrict__ m
   const int woff = wave_offsets(wcount, s_scan, &np);
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    if (r * kWave >= span) continue;
     const int e = wid * span + r * kWave + lane;
     if (hd[r]) dst[woff + pre[r]] = (uint32_t)e;  // head position of each pair
   }
@@ -273,6 +335,56 @@ __global__ __launch_bounds__(kLT) void k_ls_strips(const int32_t* __restrict__ m
   if (t == 0) strip_np[s] = np;
 }
 
+// Sixteen consecutive ints a[i0 .. i0 + 16) (zero past n), loaded together
+// (a and i0 aligned to 16 ints).
+__device__ __forceinline__ void load16(const int32_t* __restrict__ a, int64_t i0, int64_t n,
+                                       int32_t (&v)[16]) {
+  if (i0 + 16 <= n) {
+    const int4* q = reinterpret_cast<const int4*>(a + i0);
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int4 x = q[k];
+      v[4 * k] = x.x;
+      v[4 * k + 1] = x.y;
+      v[4 * k + 2] = x.z;
+      v[4 * k + 3] = x.w;
+    }
+  } else {
+#pragma unroll
+    for (int k = 0; k < 16; ++k) v[k] = i0 + k < n ? a[i0 + k] : 0;
+  }
+}
+
+// Exclusive scan of a[0 .. n) by one block of kLT threads, 16 values per
+// thread per step; emit(i, exclusive prefix, a[i]) for every i < n, in
+// order within a thread.  Returns the total.
+template <typename F>
+__device__ int32_t block_scan16(const int32_t* __restrict__ a, int64_t n, int32_t* s_scan,
+                                F emit) {
+  constexpr int64_t kStep = 16 * (int64_t)kLT;
+  int32_t carry = 0;
+  for (int64_t base = 0; base < n; base += kStep) {
+    const int64_t i0 = base + 16 * (int64_t)threadIdx.x;
+    int32_t v[16];
+    load16(a, i0, n, v);
+    int32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) sum += v[k];
+    int32_t tot;
+    int32_t off = carry + block_exclusive_scan<kLT>(sum, s_scan, &tot);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      if (i0 + k < n) emit(i0 + k, off, v[k]);
+      off += v[k];
+    }
+    carry += tot;
+  }
+  return carry;
+}
+
+constexpr int kPlanStrips = 4096;  // strip offsets kept in LDS up to this many strips
+constexpr int kPlanItems = 8192;   // item starts kept in LDS up to this many items
+
 // One block: pair offsets of the strips, the items (cut at the shares) and
 // their strips and first pairs, the shares' first items, and the first
 // pixel-major pair of every feature row.
@@ -288,60 +400,83 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
                                                  int32_t* __restrict__ pix_pair0) {
   __shared__ int32_t s_scan[kLW];
   __shared__ int32_t s_bad;
+  __shared__ int32_t s_sp0[kPlanStrips + 1];
+  __shared__ int32_t s_ip0[kPlanItems + 1];
   const int t = threadIdx.x;
   if (t == 0) s_bad = 0;
-  // 1. pair offsets (contiguous strips per thread)
-  const int32_t per = (strips + kLT - 1) / kLT;
-  const int32_t s_lo = min(strips, t * per), s_hi = min(strips, s_lo + per);
-  int32_t sum = 0, ne = 0;
-  for (int32_t s = s_lo; s < s_hi; ++s) {
-    const int32_t v = strip_np[s];
-    sum += v;
-    ne += v > 0 ? 1 : 0;
-  }
-  int32_t P, n_strips;
-  int32_t off = block_exclusive_scan<kLT>(sum, s_scan, &P);
-  block_exclusive_scan<kLT>(ne, s_scan, &n_strips);
-  // 2. items of every strip
-  int64_t isum = 0;
+  const bool lds_strips = strips <= kPlanStrips;
+  // 1. pair offsets (16 consecutive strips per thread and step)
+  int32_t P = 0, n_strips = 0;
   {
-    int32_t a = off;
-    for (int32_t s = s_lo; s < s_hi; ++s) {
-      const int32_t v = strip_np[s];
-      strip_p0[s] = a;
-      if (v > 0) isum += strip_items(a, a + v, P, shares, [](int64_t, int64_t) {});
-      a += v;
-    }
-  }
-  int32_t n_items;
-  int32_t ioff = block_exclusive_scan<kLT>((int32_t)isum, s_scan, &n_items);
-  {
-    int32_t a = off;
-    for (int32_t s = s_lo; s < s_hi; ++s) {
-      const int32_t v = strip_np[s];
-      strip_it0[s] = ioff;
-      if (v > 0) {
-        const int32_t first_item = ioff;
-        ioff += (int32_t)strip_items(a, a + v, P, shares, [&](int64_t i, int64_t first) {
-          const int64_t item = first_item + i;
-          if (item < items_cap) {
-            item_strip[item] = s;
-            item_pair0[item] = (int32_t)first;
-          }
-        });
+    int32_t carry = 0, ncarry = 0;
+    for (int64_t base = 0; base < strips; base += 16 * kLT) {
+      const int64_t i0 = base + 16 * t;
+      int32_t v[16];
+      load16(strip_np, i0, strips, v);
+      int32_t sum = 0, ne = 0;
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        sum += v[k];
+        ne += v[k] > 0 ? 1 : 0;
       }
-      a += v;
+      int32_t tot, ntot;
+      int32_t off = carry + block_exclusive_scan<kLT>(sum, s_scan, &tot);
+      block_exclusive_scan<kLT>(ne, s_scan, &ntot);
+#pragma unroll
+      for (int k = 0; k < 16; ++k) {
+        if (i0 + k < strips) {
+          strip_p0[i0 + k] = off;
+          if (lds_strips) s_sp0[i0 + k] = off;
+        }
+        off += v[k];
+      }
+      carry += tot;
+      ncarry += ntot;
     }
+    P = carry;
+    n_strips = ncarry;
   }
   if (t == 0) {
     strip_p0[strips] = P;
+    if (lds_strips) s_sp0[strips] = P;
+  }
+  __syncthreads();  // (global and LDS writes above are visible to the block after it)
+  const int32_t* sp0 = lds_strips ? s_sp0 : strip_p0;
+  // 2. items of every strip (contiguous strips per thread)
+  const int32_t per = (strips + kLT - 1) / kLT;
+  const int32_t s_lo = min(strips, t * per), s_hi = min(strips, s_lo + per);
+  int64_t isum = 0;
+  for (int32_t s = s_lo; s < s_hi; ++s) {
+    const int32_t a = sp0[s], v = sp0[s + 1] - a;
+    if (v > 0) isum += strip_items(a, a + v, P, shares, [](int64_t, int64_t) {});
+  }
+  int32_t n_items;
+  int32_t ioff = block_exclusive_scan<kLT>((int32_t)isum, s_scan, &n_items);
+  const bool lds_items = n_items <= kPlanItems && n_items <= items_cap;
+  for (int32_t s = s_lo; s < s_hi; ++s) {
+    const int32_t a = sp0[s], v = sp0[s + 1] - a;
+    strip_it0[s] = ioff;
+    if (v > 0) {
+      const int32_t first_item = ioff;
+      ioff += (int32_t)strip_items(a, a + v, P, shares, [&](int64_t i, int64_t first) {
+        const int64_t item = first_item + i;
+        if (item < items_cap) {
+          item_strip[item] = s;
+          item_pair0[item] = (int32_t)first;
+          if (lds_items) s_ip0[item] = (int32_t)first;
+        }
+      });
+    }
+  }
+  if (t == 0) {
     strip_it0[strips] = n_items;
     if (n_items <= items_cap) item_pair0[n_items] = P;
     hdr[kHdrPairs] = P;
     hdr[kHdrItems] = n_items;
     hdr[kHdrStrips] = n_strips;
   }
-  __syncthreads();  // (the block's global writes above are visible to it after the barrier)
+  __syncthreads();
+  const int32_t* ip0 = lds_items ? s_ip0 : item_pair0;
   // 3. shares: boundary w snapped within its strip, then the first item at
   // or after it
   const int32_t n_it = (int32_t)min<int64_t>(n_items, items_cap);
@@ -351,14 +486,14 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
       int32_t lo = 0, hi = strips - 1;
       while (lo < hi) {
         const int32_t mid = (lo + hi + 1) >> 1;
-        if (strip_p0[mid] <= c) lo = mid; else hi = mid - 1;
+        if (sp0[mid] <= c) lo = mid; else hi = mid - 1;
       }
-      c = snap_bound(c, strip_p0[lo], strip_p0[lo + 1]);
+      c = snap_bound(c, sp0[lo], sp0[lo + 1]);
     }
     int32_t lo = 0, hi = n_it;
     while (lo < hi) {
       const int32_t mid = (lo + hi) >> 1;
-      if (item_pair0[mid] < c) lo = mid + 1; else hi = mid;
+      if (ip0[mid] < c) lo = mid + 1; else hi = mid;
     }
     share_item0[w] = lo;
   }
@@ -366,17 +501,8 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
   for (int w = t; w < shares; w += kLT)
     if (share_item0[w + 1] - share_item0[w] > kShareItems) s_bad = 1;
   // 4. first pixel-major pair of every feature row
-  const int64_t rper = (rows + kLT - 1) / kLT;
-  const int64_t r_lo = min<int64_t>(rows, t * rper), r_hi = min<int64_t>(rows, r_lo + rper);
-  int32_t rsum = 0;
-  for (int64_t r = r_lo; r < r_hi; ++r) rsum += pix_count[r];
-  int32_t rtot;
-  int32_t roff = block_exclusive_scan<kLT>(rsum, s_scan, &rtot);
-  for (int64_t r = r_lo; r < r_hi; ++r) {
-    const int32_t v = pix_count[r];
-    pix_pair0[r] = roff;
-    roff += v;
-  }
+  const int32_t rtot = block_scan16(pix_count, rows, s_scan,
+                                    [&](int64_t r, int32_t excl, int32_t) { pix_pair0[r] = excl; });
   __syncthreads();
   if (t == 0) {
     pix_pair0[rows] = rtot;
@@ -395,19 +521,22 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
     const int32_t* __restrict__ strip_it0, const int32_t* __restrict__ item_pair0,
     int64_t items_cap, const int32_t* __restrict__ pix_pair0, int32_t* __restrict__ item_nseg,
     int32_t* __restrict__ cell_nseg, int32_t* __restrict__ head_cell,
+    int32_t* __restrict__ head_item,
     int32_t* __restrict__ pair_rd0, uint32_t* __restrict__ pair_ln,
     uint16_t* __restrict__ pair_seg, int32_t* __restrict__ bp_cell,
     uint32_t* __restrict__ bp_dn) {
   __shared__ int32_t cnt[kLW][kLBuckets];
+  __shared__ uint32_t match[kLW][kLBuckets][2];
   __shared__ int32_t s_scan[kLW];
   __shared__ int32_t s_items[kLItems + 1];
   __shared__ int32_t s_iseg[kLItems + 1];
   const int t = threadIdx.x;
   const int lane = lane_id();
   const int wid = t / kWave;
-  const int32_t s = blockIdx.x;
+  const int32_t s = strip_of_block(g.strips);
+  if (s < 0) return;  // (uniform over the block)
   const int np = strip_np[s];
-  if (np == 0) return;  // (uniform over the block)
+  if (np == 0) return;
   const int32_t P0 = strip_p0[s];
   const int32_t it0 = strip_it0[s];
   const int32_t K = strip_it0[s + 1] - it0;
@@ -429,8 +558,10 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
   int wcount = 0;
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    hd[r] = false;
+    if (r * kWave >= span) continue;
     const int e = wid * span + r * kWave + lane;
-    const bool valid = r * kWave < span && e < np;
+    const bool valid = e < np;
     key[r] = valid ? rkey[region + e] : 0u;
     const uint32_t pk = (valid && e > 0) ? rkey[region + e - 1] : 0u;
     npts[r] = valid ? rnpts[region + e] : 0;
@@ -447,17 +578,19 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
   const int woff = wave_offsets(wcount, s_scan, &nseg);
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    if (r * kWave >= span) continue;
     sin[r] += woff - 1;  // segment of the pair within the strip
     const int e = wid * span + r * kWave + lane;
-    if (r * kWave < span && e < np && s_items[item[r]] == P0 + e) s_iseg[item[r]] = sin[r];
+    if (e < np && s_items[item[r]] == P0 + e) s_iseg[item[r]] = sin[r];
   }
   __syncthreads();
   for (int k = t; k < K; k += kLT)
     item_nseg[it0 + k] = (k + 1 < K ? s_iseg[k + 1] : nseg) - s_iseg[k];
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    if (r * kWave >= span) continue;
     const int e = wid * span + r * kWave + lane;
-    if (!(r * kWave < span && e < np)) continue;
+    if (e >= np) continue;
     const int32_t gp = P0 + e;
     const uint32_t lp = (key[r] >> g.d_bits) & lpmask;
     const int32_t d0 = (int32_t)(key[r] & dmask);
@@ -470,15 +603,17 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
     if (hd[r]) {
       atomicAdd(&cell_nseg[cell], 1);
       head_cell[gp] = cell;
+      head_item[gp] = it0 + item[r];
     }
   }
   // pixel-major pairs: a stable pass by local pixel
   int32_t dest[kLR];
-  local_ranks(digit, np, span, g.lp_bits, cnt, s_scan, dest);
+  local_ranks(digit, np, span, cnt, match, s_scan, dest);
 #pragma unroll
   for (int r = 0; r < kLR; ++r) {
+    if (r * kWave >= span) continue;
     const int e = wid * span + r * kWave + lane;
-    if (!(r * kWave < span && e < np)) continue;
+    if (e >= np) continue;
     const int32_t lp = (int32_t)digit[r];
     const int32_t hl = lp / bws;
     const int64_t row = (int64_t)bn * g.hw + (int64_t)(h0 + hl) * g.W + w0 + (lp - hl * bws);
@@ -500,69 +635,71 @@ __global__ __launch_bounds__(kLT) void k_ls_cells(
   __shared__ int32_t s_scan[kLW];
   const int t = threadIdx.x;
   const int64_t n_items = min<int64_t>(hdr[kHdrItems], items_cap);
-  const int64_t iper = (n_items + kLT - 1) / kLT;
-  const int64_t i_lo = min<int64_t>(n_items, t * iper), i_hi = min<int64_t>(n_items, i_lo + iper);
-  int32_t isum = 0;
-  for (int64_t i = i_lo; i < i_hi; ++i) isum += item_nseg[i];
-  int32_t n_segs;
-  int32_t ioff = block_exclusive_scan<kLT>(isum, s_scan, &n_segs);
-  for (int64_t i = i_lo; i < i_hi; ++i) {
-    item_seg0[i] = ioff;
-    ioff += item_nseg[i];
-  }
-  const int64_t cper = (cells + kLT - 1) / kLT;
-  const int64_t c_lo = min<int64_t>(cells, t * cper), c_hi = min<int64_t>(cells, c_lo + cper);
-  int32_t ss = 0, sc = 0, se = 0;
-  for (int64_t c = c_lo; c < c_hi; ++c) {
-    const int32_t k = cell_nseg[c];
-    ss += k > 1 ? k : 0;
-    sc += k > 1 ? 1 : 0;
-    se += k == 0 ? 1 : 0;
-  }
-  int32_t n_slots, n_comb, n_empty;
-  int32_t so = block_exclusive_scan<kLT>(ss, s_scan, &n_slots);
-  int32_t co = block_exclusive_scan<kLT>(sc, s_scan, &n_comb);
-  int32_t eo = block_exclusive_scan<kLT>(se, s_scan, &n_empty);
-  for (int64_t c = c_lo; c < c_hi; ++c) {
-    const int32_t k = cell_nseg[c];
-    if (k > 1) {
-      slot0[c] = so;
-      if (co < comb_cap) {
-        comb_cell[co] = (int32_t)c;
-        comb_slot0[co] = so;
-      }
-      so += k;
-      ++co;
-    } else if (k == 0) {
-      if (eo < empty_cap) empty[eo] = (int32_t)c;
-      ++eo;
+  const int32_t n_segs = block_scan16(item_nseg, n_items, s_scan,
+                                      [&](int64_t i, int32_t excl, int32_t) { item_seg0[i] = excl; });
+  // three scans over the cells at once: slots, cells with several segments,
+  // empty cells
+  constexpr int64_t kStep = 16 * (int64_t)kLT;
+  int32_t cs = 0, cc = 0, ce = 0;
+  for (int64_t base = 0; base < cells; base += kStep) {
+    const int64_t i0 = base + 16 * (int64_t)t;
+    int32_t v[16];
+    load16(cell_nseg, i0, cells, v);
+    int32_t ss = 0, sc = 0, se = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const bool in = i0 + k < cells;
+      ss += v[k] > 1 ? v[k] : 0;
+      sc += v[k] > 1 ? 1 : 0;
+      se += (in && v[k] == 0) ? 1 : 0;
     }
+    int32_t ts, tc, te;
+    int32_t so = cs + block_exclusive_scan<kLT>(ss, s_scan, &ts);
+    int32_t co = cc + block_exclusive_scan<kLT>(sc, s_scan, &tc);
+    int32_t eo = ce + block_exclusive_scan<kLT>(se, s_scan, &te);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      const int64_t c = i0 + k;
+      if (c >= cells) continue;
+      if (v[k] > 1) {
+        slot0[c] = so;
+        if (co < comb_cap) {
+          comb_cell[co] = (int32_t)c;
+          comb_slot0[co] = so;
+        }
+        so += v[k];
+        ++co;
+      } else if (v[k] == 0) {
+        if (eo < empty_cap) empty[eo] = (int32_t)c;
+        ++eo;
+      }
+    }
+    cs += ts;
+    cc += tc;
+    ce += te;
   }
   if (t == 0) {
     if (n_items == hdr[kHdrItems]) item_seg0[n_items] = n_segs;
-    comb_slot0[min<int64_t>(n_comb, comb_cap)] = n_slots;
+    comb_slot0[min<int64_t>(cc, comb_cap)] = cs;
     hdr[kHdrSegs] = n_segs;
-    hdr[kHdrSlots] = n_slots;
-    hdr[kHdrComb] = n_comb;
-    hdr[kHdrEmpty] = n_empty;
-    hdr[kHdrOccFound] = (int32_t)(cells - n_empty);
+    hdr[kHdrSlots] = cs;
+    hdr[kHdrComb] = cc;
+    hdr[kHdrEmpty] = ce;
+    hdr[kHdrOccFound] = (int32_t)(cells - ce);
   }
 }
 
 // Every segment: its destination when its cell has no other segment; else
-// its index joins its cell's list of slots (in any order; sorted below).
+// its index joins its cell's list of slots (in any order; ranked below).
 __global__ __launch_bounds__(256) void k_ls_segments(
-    const int32_t* __restrict__ hdr, int64_t items_cap, const uint32_t* __restrict__ pair_ln,
+    const int32_t* __restrict__ hdr, const uint32_t* __restrict__ pair_ln,
     const uint16_t* __restrict__ pair_seg, const int32_t* __restrict__ head_cell,
-    const int32_t* __restrict__ item_pair0, const int32_t* __restrict__ item_seg0,
+    const int32_t* __restrict__ head_item, const int32_t* __restrict__ item_seg0,
     const int32_t* __restrict__ cell_nseg, const int32_t* __restrict__ slot0,
     int32_t* __restrict__ fill, int32_t* __restrict__ slot_seg, int32_t* __restrict__ seg_dest) {
   const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (k >= hdr[kHdrPairs] || !(pair_ln[k] & kPairHead)) return;
-  const int32_t n_items = (int32_t)min<int64_t>(hdr[kHdrItems], items_cap);
-  if (n_items < 1) return;
-  const int32_t it = upper_index(item_pair0, n_items, (int32_t)k);
-  const int32_t seg = item_seg0[it] + pair_seg[k];
+  const int32_t seg = item_seg0[head_item[k]] + pair_seg[k];
   const int32_t cell = head_cell[k];
   if (cell_nseg[cell] == 1) {
     seg_dest[seg] = cell;
@@ -571,27 +708,33 @@ __global__ __launch_bounds__(256) void k_ls_segments(
   }
 }
 
-// Every cell with several segments: its segments in ascending order get its
-// slots in order.
-__global__ __launch_bounds__(256) void k_ls_slots(const int32_t* __restrict__ cell_nseg,
-                                                  int64_t cells, const int32_t* __restrict__ slot0,
-                                                  int32_t* __restrict__ slot_seg,
+// Every slot: the cells with several segments list their segments (in any
+// order); a segment's slot is its cell's first slot plus the number of the
+// cell's segments with a smaller index, so the segments of a cell get its
+// slots in ascending order.
+__global__ __launch_bounds__(256) void k_ls_slots(const int32_t* __restrict__ hdr,
+                                                  const int32_t* __restrict__ comb_slot0,
+                                                  int64_t comb_cap,
+                                                  const int32_t* __restrict__ slot_seg,
                                                   int32_t* __restrict__ seg_dest) {
-  const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (c >= cells) return;
-  const int32_t k = cell_nseg[c];
-  if (k < 2) return;
-  int32_t* a = slot_seg + slot0[c];
-  for (int32_t i = 1; i < k; ++i) {  // insertion sort (a cell has few segments)
-    const int32_t v = a[i];
-    int32_t j = i - 1;
-    while (j >= 0 && a[j] > v) {
-      a[j + 1] = a[j];
-      --j;
-    }
-    a[j + 1] = v;
+  const int64_t q = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (q >= hdr[kHdrSlots]) return;
+  const int32_t n_comb = (int32_t)min<int64_t>(hdr[kHdrComb], comb_cap);
+  if (n_comb < 1) return;
+  const int32_t j = upper_index(comb_slot0, n_comb, (int32_t)q);
+  const int32_t s0 = comb_slot0[j], s1 = comb_slot0[j + 1];
+  const int32_t v = slot_seg[q];
+  int32_t rank = 0;
+  int32_t i = s0;
+  for (; i + 8 <= s1; i += 8) {
+    int32_t a[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) a[k] = slot_seg[i + k];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) rank += a[k] < v ? 1 : 0;
   }
-  for (int32_t i = 0; i < k; ++i) seg_dest[a[i]] = ~(slot0[c] + i);
+  for (; i < s1; ++i) rank += slot_seg[i] < v ? 1 : 0;
+  seg_dest[v] = ~(s0 + rank);
 }
 
 int bits_for(int64_t n) {  // bits of the values 0 .. n - 1
@@ -620,7 +763,7 @@ void local_schedule_ws(const Dims& d, ScheduleLayout& L) {
   };
   const size_t nv = (size_t)(L.n_valid > 0 ? L.n_valid : 1);
   const size_t region = (size_t)L.sd.strips * (size_t)(L.sd.pixels * d.D);
-  L.wl_map = take((size_t)d.P);
+  L.wl_map = take(region);
   L.wl_rkey = take(region);
   L.wl_rnpts = take(region);
   L.wl_strip_np = take((size_t)L.sd.strips + 1);
@@ -632,6 +775,7 @@ void local_schedule_ws(const Dims& d, ScheduleLayout& L) {
   L.wl_fill = take((size_t)d.cells);
   L.wl_slot0 = take((size_t)d.cells);
   L.wl_head_cell = take(nv);
+  L.wl_head_item = take(nv);
   L.wl_slot_seg = take(nv);
   L.wl_total = off;
 }
@@ -674,32 +818,33 @@ hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t
   int32_t* fill = W(L.wl_fill);
   int32_t* slot0 = W(L.wl_slot0);
   int32_t* head_cell = W(L.wl_head_cell);
+  int32_t* head_item = W(L.wl_head_item);
   int32_t* slot_seg = W(L.wl_slot_seg);
 
-  const int64_t span = std::max<int64_t>(std::max<int64_t>(d.P, d.cells), 16);
-  k_ls_init<<<(unsigned)((span + 255) / 256), 256, 0, stream>>>(map, d.P, cell_nseg, fill, d.cells,
-                                                                 hdr, n_valid, n_intervals);
+  const int64_t region = L.sd.strips * (L.sd.pixels * d.D);
+  const int64_t span = std::max<int64_t>(std::max<int64_t>(region, d.cells), 16);
+  k_ls_init<<<(unsigned)((span + 255) / 256), 256, 0, stream>>>(map, region, cell_nseg, fill,
+                                                                 d.cells, hdr, n_valid, n_intervals);
   const unsigned g_nv = (unsigned)((n_valid + 255) / 256);
-  k_ls_map<<<g_nv, 256, 0, stream>>>(rd, rb, n_valid, d.P, d.cells, map);
-  k_ls_strips<<<(unsigned)L.sd.strips, kLT, 0, stream>>>(map, g, rkey, rnpts, strip_np, pix_count);
+  k_ls_map<<<g_nv, 256, 0, stream>>>(rd, rb, n_valid, d.P, d.cells, g, map);
+  const unsigned strip_blocks = (unsigned)((L.sd.strips + kXcds - 1) / kXcds * kXcds);
+  k_ls_strips<<<strip_blocks, kLT, 0, stream>>>(map, g, rkey, rnpts, strip_np, pix_count);
   k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, L.items_cap, pix_count, d.rows,
                                    strip_p0, strip_it0, hdr, S(L.item_strip), S(L.item_pair0),
                                    S(L.share_item0), S(L.pix_pair0));
-  k_ls_emit<<<(unsigned)L.sd.strips, kLT, 0, stream>>>(
+  k_ls_emit<<<strip_blocks, kLT, 0, stream>>>(
       g, rkey, rnpts, strip_np, strip_p0, strip_it0, S(L.item_pair0), L.items_cap, S(L.pix_pair0),
-      item_nseg, cell_nseg, head_cell, S(L.pair_rd0), reinterpret_cast<uint32_t*>(S(L.pair_ln)),
+      item_nseg, cell_nseg, head_cell, head_item, S(L.pair_rd0), reinterpret_cast<uint32_t*>(S(L.pair_ln)),
       reinterpret_cast<uint16_t*>(S(L.pair_seg)), S(L.bp_cell),
       reinterpret_cast<uint32_t*>(S(L.bp_dn)));
   k_ls_cells<<<1, kLT, 0, stream>>>(hdr, item_nseg, L.items_cap, cell_nseg, d.cells, S(L.item_seg0),
                                     slot0, S(L.comb_cell), S(L.comb_slot0), L.n_occ, S(L.empty),
                                     L.n_empty);
-  k_ls_segments<<<g_nv, 256, 0, stream>>>(hdr, L.items_cap,
-                                          reinterpret_cast<const uint32_t*>(S(L.pair_ln)),
+  k_ls_segments<<<g_nv, 256, 0, stream>>>(hdr, reinterpret_cast<const uint32_t*>(S(L.pair_ln)),
                                           reinterpret_cast<const uint16_t*>(S(L.pair_seg)),
-                                          head_cell, S(L.item_pair0), S(L.item_seg0), cell_nseg,
-                                          slot0, fill, slot_seg, S(L.seg_dest));
-  k_ls_slots<<<(unsigned)((d.cells + 255) / 256), 256, 0, stream>>>(cell_nseg, d.cells, slot0,
-                                                                    slot_seg, S(L.seg_dest));
+                                          head_cell, head_item, S(L.item_seg0), cell_nseg, slot0,
+                                          fill, slot_seg, S(L.seg_dest));
+  k_ls_slots<<<g_nv, 256, 0, stream>>>(hdr, S(L.comb_slot0), L.n_occ, slot_seg, S(L.seg_dest));
   return hipGetLastError();
 }
 
