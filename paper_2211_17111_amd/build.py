@@ -21,7 +21,7 @@ LIB_NAME = "libbevpool.so"
 LIB_PATH = os.path.join(PKG, LIB_NAME)
 
 ARCH = "gfx950"
-SOURCES = ["prepare.hip", "schedule_local.hip", "forward.hip", "forward_strips.hip", "backward.hip", "softmax.hip",
+SOURCES = ["prepare.hip", "prepare_plan.hip", "schedule_local.hip", "forward.hip", "forward_strips.hip", "backward.hip", "softmax.hip",
            "geometry.hip",
            "api.cpp"]
 # measurement probe for bench.py, built into a library of its own

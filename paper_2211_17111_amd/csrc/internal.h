@@ -34,12 +34,11 @@ constexpr int kScanTile = kScanThreads * kScanItems;   // 2048
 
 struct PrepareLayout {
   size_t keys_tmp, vals_tmp;   // int32[P] each (radix ping-pong)
-  size_t tile_counts;          // int32[ntiles + 1]
-  size_t hist;                 // int32[256 * ntiles]
-  size_t scan_sums;            // int32[nscan + 1]
+  size_t hist;                 // int32[256 * ntiles]: digit-major tile counts
+  size_t digit_totals;         // int32[256]
+  size_t cell_counts;          // int32[cells]
   size_t total;                // bytes
-  int64_t ntiles;
-  int64_t nscan;
+  int64_t ntiles;              // tiles of 1024 frustum points
   int key_bits, passes, digit_bits;
 };
 PrepareLayout prepare_layout(const Dims& d);
@@ -136,7 +135,8 @@ struct ScheduleLayout {
   int row_bits, cell_bits, pixel_bits, strip_bits;
   // workspace of the build by strips in LDS (schedule_local.hip)
   size_t wl_map, wl_rkey, wl_rnpts, wl_strip_np, wl_strip_p0, wl_strip_it0, wl_pix_count,
-      wl_item_nseg, wl_cell_nseg, wl_fill, wl_slot0, wl_head_cell, wl_slot_seg, wl_total;
+      wl_item_nseg, wl_cell_nseg, wl_fill, wl_slot0, wl_head_cell, wl_head_item, wl_slot_seg,
+      wl_total;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
 
