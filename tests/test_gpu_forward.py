@@ -282,6 +282,23 @@ def test_schedule_edge_shapes():
     assert want["n"]["items"] > want["n"]["strips"]   # strips cut into several items
 
 
+@pytest.mark.parametrize("label,shape", [
+    # strips of 32 x 3 pixels (C = 80) over D bins: the build by strips in LDS
+    # takes up to 12288 points per strip and keys (cell within the sample,
+    # pixel, bin) of up to 32 bits; past either bound the general builder runs
+    ("12288 points per strip", dict(B=1, N=1, D=128, H=32, W=6, C=80, X=40, Y=40, Z=1)),
+    ("12384 points per strip", dict(B=1, N=1, D=129, H=32, W=6, C=80, X=40, Y=40, Z=1)),
+    ("32-bit keys", dict(B=1, N=1, D=128, H=32, W=3, C=80, X=512, Y=512, Z=1)),
+    ("33-bit keys", dict(B=1, N=1, D=128, H=32, W=3, C=80, X=512, Y=512, Z=2)),
+])
+def test_schedule_local_bounds(label, shape):
+    """Shapes on both sides of the bounds of the strip-local build give the
+    schedule of the definitions (both builders are exact)."""
+    rng = np.random.default_rng(23)
+    _gpu.say(f"schedule at the local-build bounds: {label}")
+    _check_schedule(random_coor(rng, shape, p_out=0.3), shape, label)
+
+
 def test_scheduled_matches_ranges():
     cfg = CONFIGS["headline"]
     coor = frustum_coor(cfg)
