@@ -150,6 +150,26 @@ class BufferSet:
         return sum(t.numel() * t.element_size() for t in vars(self).values() if isinstance(t, torch.Tensor))
 
 
+# Launches whose event pairs are enqueued behind one spin kernel: the host
+# enqueues a launch in about 30 us, no faster than the GPU runs one, so
+# without it the GPU would at times reach a launch's start event before the
+# launch itself is submitted, and the event pair would time the host.
+TIMED_CHUNK = 32
+SPIN_CYCLES = 4_000_000  # about 2 ms of the spin kernel, longer than a chunk's enqueue
+
+
+def _timed_pairs(n, pick, fn, stream, starts, ends):
+    """Event pairs around n launches on `stream` (the current stream), each
+    chunk of launches enqueued while a spin kernel keeps the GPU busy."""
+    for c0 in range(0, n, TIMED_CHUNK):
+        torch.cuda._sleep(SPIN_CYCLES)
+        for i in range(c0, min(n, c0 + TIMED_CHUNK)):
+            starts[i].record(stream)
+            fn(pick(i))
+            ends[i].record(stream)
+    torch.cuda.synchronize()
+
+
 def _cold(n, pick, fn, stream):
     """Per-launch HIP event pairs on `stream` over n launches (after a short
     warm-up), and the back-to-back region per launch."""
@@ -157,11 +177,7 @@ def _cold(n, pick, fn, stream):
         fn(pick(i))
     torch.cuda.synchronize()
     ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(n)]
-    for i in range(n):
-        ev[i][0].record(stream)
-        fn(pick(i))
-        ev[i][1].record(stream)
-    torch.cuda.synchronize()
+    _timed_pairs(n, pick, fn, stream, [e[0] for e in ev], [e[1] for e in ev])
     per = np.array([a.elapsed_time(b) for a, b in ev])
     r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     r0.record(stream)
@@ -373,15 +389,10 @@ def main():
         """Per-launch event pairs and the whole back-to-back region."""
         starts = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
         ends = [torch.cuda.Event(enable_timing=True) for _ in range(n)]
-        for i in range(min(n, 16)):
+        for i in range(min(n, 64)):  # (every rotating set once: none is first touched while timed)
             fn(pick(i))
         torch.cuda.synchronize()
-        for i in range(n):
-            s = pick(i)
-            starts[i].record(stream)
-            fn(s)
-            ends[i].record(stream)
-        torch.cuda.synchronize()
+        _timed_pairs(n, pick, fn, stream, starts, ends)
         per = np.array([a.elapsed_time(b) for a, b in zip(starts, ends)])
         r0, r1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         r0.record(stream)
@@ -402,11 +413,12 @@ def main():
     log(f"{args.forward} forward back-to-back region: cold {cold_region * 1e3:.2f} us/launch, warm "
         f"{warm_region * 1e3:.2f}; {other_name} forward cold median {np.median(cold_oth) * 1e3:.2f} us "
         f"(region {cold_oth_region * 1e3:.2f})")
-    # the median per launch (a rare host stall before a launch lands in its
-    # events and would move a mean)
+    # the median per launch
     fwd_ms = float(np.median(cold))
     min_bytes = forward_min_bytes(cfg, nv, ni)
     achieved = min_bytes / (fwd_ms * 1e-3) / 1e9
+    slow = np.argsort(cold)[::-1][:4]
+    log("slowest cold launches: " + ", ".join(f"#{i} {cold[i] * 1e3:.1f} us" for i in slow))
     log(f"forward cold median {fwd_ms * 1e3:.2f} us (p10 {np.percentile(cold, 10) * 1e3:.2f}, mean "
         f"{cold.mean() * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
         f"{warm.mean() * 1e3:.2f} us; {min_bytes / 1e6:.2f} MB -> {achieved:.0f} GB/s")
