@@ -27,13 +27,15 @@ namespace bevpool {
 
 namespace {
 
-// A block takes 64 pixels; its four waves split each pixel's depth bins
-// into four ranges (lane = pixel, so every load of a wave reads 64
+// A block takes 64 pixels; its eight waves split each pixel's depth bins
+// into eight ranges (lane = pixel, so every load of a wave reads 64
 // consecutive logits) and combine their partial maxima and sums in LDS, in
-// wave order.
-constexpr int kLseWaves = 4;
+// wave order.  When a range fits kLseRegs bins it is loaded once, into
+// registers, for both the maximum and the sum.
+constexpr int kLseWaves = 8;
 constexpr int kLseThreads = kLseWaves * kWave;
-constexpr int kLseBatch = 8;  // logits in flight per thread
+constexpr int kLseBatch = 8;  // logits in flight per thread (two-pass form)
+constexpr int kLseRegs = 16;  // a wave share of at most this many bins stays in registers
 
 template <typename TIn>
 __global__ __launch_bounds__(kLseThreads) void k_depth_lse(const TIn* __restrict__ logits,
@@ -49,33 +51,51 @@ __global__ __launch_bounds__(kLseThreads) void k_depth_lse(const TIn* __restrict
   const int64_t view = pxc / hw;
   const TIn* p = logits + view * (int64_t)D * hw + (pxc - view * hw);
   const int d0 = (int)((int64_t)D * wv / kLseWaves), d1 = (int)((int64_t)D * (wv + 1) / kLseWaves);
-  // this wave's share of the largest logit
   float m = -INFINITY;
-  int d = d0;
-  for (; d + kLseBatch <= d1; d += kLseBatch) {
-    float v[kLseBatch];
-#pragma unroll
-    for (int u = 0; u < kLseBatch; ++u) v[u] = to_float(p[(int64_t)(d + u) * hw]);
-#pragma unroll
-    for (int u = 0; u < kLseBatch; ++u) m = fmaxf(m, v[u]);
-  }
-  for (; d < d1; ++d) m = fmaxf(m, to_float(p[(int64_t)d * hw]));
-  s_max[wv][lane] = m;
-  __syncthreads();
-  m = s_max[0][lane];
-#pragma unroll
-  for (int w = 1; w < kLseWaves; ++w) m = fmaxf(m, s_max[w][lane]);
-  // this wave's share of the sum of exp(logit - m), in double
   double s = 0.0;
-  d = d0;
-  for (; d + kLseBatch <= d1; d += kLseBatch) {
-    float v[kLseBatch];
+  if ((D + kLseWaves - 1) / kLseWaves <= kLseRegs) {  // (the same for every wave: both forms hold a barrier)
+    // the wave's share, loaded once: its largest logit, then (with the
+    // pixel's largest) the sum of exp(logit - m) in double
+    float v[kLseRegs];
 #pragma unroll
-    for (int u = 0; u < kLseBatch; ++u) v[u] = to_float(p[(int64_t)(d + u) * hw]);
+    for (int u = 0; u < kLseRegs; ++u) v[u] = d0 + u < d1 ? to_float(p[(int64_t)(d0 + u) * hw]) : -INFINITY;
 #pragma unroll
-    for (int u = 0; u < kLseBatch; ++u) s += (double)expf(v[u] - m);
+    for (int u = 0; u < kLseRegs; ++u) m = fmaxf(m, v[u]);
+    s_max[wv][lane] = m;
+    __syncthreads();
+    m = s_max[0][lane];
+#pragma unroll
+    for (int w = 1; w < kLseWaves; ++w) m = fmaxf(m, s_max[w][lane]);
+#pragma unroll
+    for (int u = 0; u < kLseRegs; ++u)
+      if (d0 + u < d1) s += (double)expf(v[u] - m);
+  } else {
+    // this wave's share of the largest logit
+    int d = d0;
+    for (; d + kLseBatch <= d1; d += kLseBatch) {
+      float v[kLseBatch];
+#pragma unroll
+      for (int u = 0; u < kLseBatch; ++u) v[u] = to_float(p[(int64_t)(d + u) * hw]);
+#pragma unroll
+      for (int u = 0; u < kLseBatch; ++u) m = fmaxf(m, v[u]);
+    }
+    for (; d < d1; ++d) m = fmaxf(m, to_float(p[(int64_t)d * hw]));
+    s_max[wv][lane] = m;
+    __syncthreads();
+    m = s_max[0][lane];
+#pragma unroll
+    for (int w = 1; w < kLseWaves; ++w) m = fmaxf(m, s_max[w][lane]);
+    // this wave's share of the sum of exp(logit - m), in double
+    d = d0;
+    for (; d + kLseBatch <= d1; d += kLseBatch) {
+      float v[kLseBatch];
+#pragma unroll
+      for (int u = 0; u < kLseBatch; ++u) v[u] = to_float(p[(int64_t)(d + u) * hw]);
+#pragma unroll
+      for (int u = 0; u < kLseBatch; ++u) s += (double)expf(v[u] - m);
+    }
+    for (; d < d1; ++d) s += (double)expf(to_float(p[(int64_t)d * hw]) - m);
   }
-  for (; d < d1; ++d) s += (double)expf(to_float(p[(int64_t)d * hw]) - m);
   s_sum[wv][lane] = s;
   __syncthreads();
   if (wv == 0 && on) {

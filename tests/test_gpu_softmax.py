@@ -44,6 +44,21 @@ def test_lse_matches_oracle(name):
     assert worst <= 1.0, name
 
 
+@pytest.mark.parametrize("D", [1, 7, 128, 129, 150, 300])
+def test_lse_depth_bins(D):
+    """Depth-bin counts on both sides of the kernel's register form (a wave's
+    share of at most 16 bins, D <= 128) and its two-pass form, with logits
+    far from zero."""
+    rng = np.random.default_rng(31 + D)
+    shape = dict(B=2, N=1, D=D, H=3, W=70, C=4, X=4, Y=4, Z=1)
+    logits = (8.0 * rng.standard_normal((2, 1, D, 3, 70)) + 40.0).astype(np.float32)
+    got = bp.depth_lse(_gpu.to_dev(logits), shape).cpu().numpy()
+    ref = oracle.depth_lse_ref(logits)
+    worst = float((np.abs(got - ref) / _lse_bound(ref)).max())
+    _gpu.say(f"  lse D={D}: worst err/bound {worst:.3f}")
+    assert worst <= 1.0, D
+
+
 @pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "voxel3d"])
 def test_fused_forward_every_element(name):
     cfg = CONFIGS[name]
