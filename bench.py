@@ -156,6 +156,8 @@ class BufferSet:
 # launch itself is submitted, and the event pair would time the host.
 TIMED_CHUNK = 32
 SPIN_CYCLES = 4_000_000  # about 2 ms of the spin kernel, longer than a chunk's enqueue
+# event pairs longer than this many medians are counted as queue stalls
+STALL_FACTOR = 10
 
 
 def _timed_pairs(n, pick, fn, stream, starts, ends):
@@ -419,6 +421,14 @@ def main():
     achieved = min_bytes / (fwd_ms * 1e-3) / 1e9
     slow = np.argsort(cold)[::-1][:4]
     log("slowest cold launches: " + ", ".join(f"#{i} {cold[i] * 1e3:.1f} us" for i in slow))
+    # A launch whose event pair spans more than ten times the median was held
+    # up outside the kernel (the device or the host stalled the queue); such
+    # launches are counted and the mean is also given without them.
+    stalled = cold > STALL_FACTOR * fwd_ms
+    cold_mean_ok = float(cold[~stalled].mean())
+    if stalled.any():
+        log(f"{int(stalled.sum())} of {cold.size} cold launches above {STALL_FACTOR}x the median "
+            f"(queue stalls); mean without them {cold_mean_ok * 1e3:.2f} us")
     log(f"forward cold median {fwd_ms * 1e3:.2f} us (p10 {np.percentile(cold, 10) * 1e3:.2f}, mean "
         f"{cold.mean() * 1e3:.2f}, p90 {np.percentile(cold, 90) * 1e3:.2f}); warm mean "
         f"{warm.mean() * 1e3:.2f} us; {min_bytes / 1e6:.2f} MB -> {achieved:.0f} GB/s")
@@ -573,6 +583,8 @@ def main():
         "detail": {
             "forward_cold_ms": {"mean": float(cold.mean()), "p10": float(np.percentile(cold, 10)),
                                 "p50": fwd_ms, "p90": float(np.percentile(cold, 90)),
+                                "stalled_launches": int(stalled.sum()),
+                                "mean_without_stalled": cold_mean_ok,
                                 "launches": int(cold.size), "rotating_sets": len(sets),
                                 "rotating_bytes": int(sum(s.nbytes() for s in sets))},
             "forward_cold_region_ms_per_launch": cold_region,
