@@ -32,27 +32,6 @@ __device__ __forceinline__ int wave_inclusive_scan(int v) {
   return v;
 }
 
-// Exclusive scan of one int per thread over a block of NT threads.
-// `lds` must hold NT/64 ints.  Writes the block total to *total (all threads).
-template <int NT>
-__device__ __forceinline__ int block_exclusive_scan(int v, int* lds, int* total) {
-  const int lane = lane_id();
-  const int wid = threadIdx.x / kWave;
-  const int inc = wave_inclusive_scan(v);
-  if (lane == kWave - 1) lds[wid] = inc;
-  __syncthreads();
-  int off = 0, tot = 0;
-#pragma unroll
-  for (int w = 0; w < NT / kWave; ++w) {
-    const int s = lds[w];
-    off += (w < wid) ? s : 0;
-    tot += s;
-  }
-  __syncthreads();
-  *total = tot;
-  return off + inc - v;
-}
-
 // Workgroup barrier that orders LDS accesses only.  __syncthreads() also
 // waits for the calling wave's outstanding global loads and stores, which
 // stalls a barrier behind unrelated stores; callers that exchange data only
@@ -61,6 +40,28 @@ __device__ __forceinline__ void lds_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+// Exclusive scan of one int per thread over a block of NT threads.
+// `lds` must hold NT/64 ints.  Writes the block total to *total (all threads).
+// With LDS_ONLY its barriers leave outstanding global loads in flight.
+template <int NT, bool LDS_ONLY = false>
+__device__ __forceinline__ int block_exclusive_scan(int v, int* lds, int* total) {
+  const int lane = lane_id();
+  const int wid = threadIdx.x / kWave;
+  const int inc = wave_inclusive_scan(v);
+  if (lane == kWave - 1) lds[wid] = inc;
+  if (LDS_ONLY) lds_barrier(); else __syncthreads();
+  int off = 0, tot = 0;
+#pragma unroll
+  for (int w = 0; w < NT / kWave; ++w) {
+    const int s = lds[w];
+    off += (w < wid) ? s : 0;
+    tot += s;
+  }
+  if (LDS_ONLY) lds_barrier(); else __syncthreads();
+  *total = tot;
+  return off + inc - v;
 }
 
 }  // namespace bevpool

@@ -37,9 +37,12 @@ struct PrepareLayout {
   size_t hist;                 // int32[256 * ntiles]: digit-major tile counts
   size_t digit_totals;         // int32[256]
   size_t cell_counts;          // int32[cells]
+  size_t chunk_totals;         // int2[nchunks]: points and occupied cells per chunk
   size_t total;                // bytes
   int64_t ntiles;              // tiles of 1024 frustum points
   int key_bits, passes, digit_bits;
+  int chunk_shift;               // log2 of the cells per chunk
+  int64_t nchunks;
 };
 PrepareLayout prepare_layout(const Dims& d);
 

@@ -13,8 +13,10 @@
 //              kept points, writing the plan's three rank arrays and the
 //              point count of every cell
 //   (more passes in between for grids of more than 2^16 cells)
-//   intervals  one block: the cells with points in ascending order, their
-//              first point (exclusive scan of the counts) and their count
+//   chunk totals / intervals   per chunk of cells, its point total and
+//              occupied-cell count; then the cells with points in ascending
+//              order, their first point (exclusive scan of the counts) and
+//              their count
 //
 // Every step is deterministic: tiles are ranked in element order and the
 // cell counts are sums.
@@ -43,23 +45,27 @@ struct PGrid {
   int32_t X, Y, Z;
 };
 
-// BEV rank of point p, or -1 when its voxel index lies outside the grid.
-__device__ __forceinline__ int32_t rank_or_drop(const int32_t* __restrict__ coor, int64_t p,
-                                                const PGrid& g) {
-  const int32_t x = coor[3 * p + 0];
-  const int32_t y = coor[3 * p + 1];
-  const int32_t z = coor[3 * p + 2];
+// BEV rank of point p with voxel index (x, y, z), or -1 when that index lies
+// outside the grid.
+__device__ __forceinline__ int32_t rank_xyz(int32_t x, int32_t y, int32_t z, int64_t p,
+                                            const PGrid& g) {
   const bool in = (x >= 0) & (x < g.X) & (y >= 0) & (y < g.Y) & (z >= 0) & (z < g.Z);
   if (!in) return -1;
   const int32_t b = (int32_t)((uint32_t)p / (uint32_t)g.per_sample);
   return ((b * g.Z + z) * g.Y + y) * g.X + x;
 }
 
+__device__ __forceinline__ int32_t rank_or_drop(const int32_t* __restrict__ coor, int64_t p,
+                                                const PGrid& g) {
+  return rank_xyz(coor[3 * p + 0], coor[3 * p + 1], coor[3 * p + 2], p, g);
+}
+
 // Ranks of one tile held in the wave-round layout (element = tile base +
 // wave * 256 + round * 64 + lane): pos[r] = the element's place among the
 // tile's valid elements ordered by (digit, element), s_start[d] the first
 // place of digit d, *n_tile the number of valid elements.  cnt and match are
-// LDS scratch; all threads call it.
+// LDS scratch; all threads call it.  Its barriers order LDS only, so global
+// loads issued before it stay in flight.
 __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR],
                            int32_t (*cnt)[kBuckets], uint32_t (*match)[kBuckets][2],
                            int32_t* s_start, int32_t* s_scan, int32_t (&pos)[kPR],
@@ -69,7 +75,7 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
   const int t = threadIdx.x;
   for (int i = t; i < kPW * kBuckets; i += kPT) (&cnt[0][0])[i] = 0;
   for (int i = t; i < kPW * kBuckets * 2; i += kPT) (&match[0][0][0])[i] = 0u;
-  __syncthreads();
+  lds_barrier();
   // lanes with equal digits: each sets its bit in the wave's mask of its
   // digit, reads the mask back and clears it (LDS keeps one wave's order)
   uint2 m[kPR];
@@ -97,7 +103,7 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
   int32_t rank[kPR];
 #pragma unroll
   for (int r = 0; r < kPR; ++r) rank[r] = __shfl(old[r], leader[r], kWave) + below[r];
-  __syncthreads();
+  lds_barrier();
   int32_t c[kPW];
   int tot = 0;  // digit t: each wave's offset within the digit, and its count
 #pragma unroll
@@ -108,11 +114,11 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
     c[w] = tot;
     tot += x;
   }
-  const int start = block_exclusive_scan<kPT>(tot, s_scan, n_tile);
+  const int start = block_exclusive_scan<kPT, true>(tot, s_scan, n_tile);
 #pragma unroll
   for (int w = 0; w < kPW; ++w) cnt[w][t] = c[w] + start;
   s_start[t] = start;
-  __syncthreads();
+  lds_barrier();
 #pragma unroll
   for (int r = 0; r < kPR; ++r) pos[r] = cnt[wid][digit[r]] + rank[r];
 }
@@ -120,9 +126,10 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
 static_assert(kBuckets == kPT, "one thread per digit");
 
 // Pass 0 histogram over the frustum points; the tiles also clear the cell
-// counts, which the last pass adds to.
+// counts, which the last pass adds to.  With `vec` (coor 16-byte aligned) each thread of a whole tile reads its
+// four consecutive points as three 16-byte loads.
 __global__ __launch_bounds__(kPT) void k_pp_hist0(const int32_t* __restrict__ coor, PGrid g,
-                                                  int bits, int32_t* __restrict__ hist,
+                                                  bool vec, int bits, int32_t* __restrict__ hist,
                                                   int64_t ntiles, int32_t* __restrict__ cell_cnt,
                                                   int64_t cells) {
   __shared__ int32_t h[kBuckets];
@@ -136,10 +143,21 @@ __global__ __launch_bounds__(kPT) void k_pp_hist0(const int32_t* __restrict__ co
   const int64_t base = (int64_t)blockIdx.x * kTile;
   const uint32_t mask = (1u << bits) - 1u;
   int32_t rk[kPR];
+  if (vec && base + kTile <= g.P) {
+    static_assert(kPR == 4, "four points per thread: three 16-byte loads");
+    const int64_t p0 = base + 4 * t;
+    const int4* q = reinterpret_cast<const int4*>(coor + 3 * p0);
+    const int4 a = q[0], b = q[1], c = q[2];
+    rk[0] = rank_xyz(a.x, a.y, a.z, p0 + 0, g);
+    rk[1] = rank_xyz(a.w, b.x, b.y, p0 + 1, g);
+    rk[2] = rank_xyz(b.z, b.w, c.x, p0 + 2, g);
+    rk[3] = rank_xyz(c.y, c.z, c.w, p0 + 3, g);
+  } else {
 #pragma unroll
-  for (int k = 0; k < kPR; ++k) {
-    const int64_t p = base + k * kPT + t;
-    rk[k] = p < g.P ? rank_or_drop(coor, p, g) : -1;
+    for (int k = 0; k < kPR; ++k) {
+      const int64_t p = base + k * kPT + t;
+      rk[k] = p < g.P ? rank_or_drop(coor, p, g) : -1;
+    }
   }
 #pragma unroll
   for (int k = 0; k < kPR; ++k)
@@ -198,138 +216,248 @@ __global__ __launch_bounds__(kPT) void k_pp_digit_scan(int32_t* __restrict__ his
   if (threadIdx.x == 0) dtot[blockIdx.x] = carry;
 }
 
-// Scatter of one radix pass.  Pass 0 reads the frustum points (filter and
-// pass in one), later passes the previous pass's keys and values.  Every tile
-// goes out sorted by digit through LDS, so that lanes store consecutive
-// positions.  The last pass also writes each point's feature rank and counts
-// the points of every cell: its LDS tile is sorted by the whole rank, and each
-// run of one rank adds its length to the cell's count (the run's first
-// element adds -i, its last i + 1), so that every cell takes a few adds.
-template <bool FIRST>
-__global__ __launch_bounds__(kPT) void k_pp_scatter(
-    const int32_t* __restrict__ coor, PGrid g, const int32_t* __restrict__ keys_in,
-    const int32_t* __restrict__ vals_in, const int32_t* __restrict__ n_ptr, int shift, int bits,
-    const int32_t* __restrict__ hist, const int32_t* __restrict__ dtot, int64_t ntiles,
-    int32_t* __restrict__ keys_out, int32_t* __restrict__ vals_out,
-    int32_t* __restrict__ feat_out, int32_t* __restrict__ count_out,
-    int32_t* __restrict__ cell_cnt) {
-  __shared__ int32_t cnt[kPW][kBuckets];
-  __shared__ uint32_t match[kPW][kBuckets][2];
-  __shared__ int32_t s_start[kBuckets];
-  __shared__ int32_t s_delta[kBuckets];
-  __shared__ int32_t s_scan[kPW];
-  __shared__ int32_t s_key[kTile], s_val[kTile];
+// LDS of the scatter kernels.
+struct ScatterLds {
+  int32_t (*cnt)[kBuckets];
+  uint32_t (*match)[kBuckets][2];
+  int32_t *start, *delta, *scan, *key, *val;
+};
+
+#define BEVPOOL_SCATTER_LDS(S)                                                   \
+  __shared__ int32_t S##_cnt[kPW][kBuckets];                                     \
+  __shared__ uint32_t S##_match[kPW][kBuckets][2];                               \
+  __shared__ int32_t S##_start[kBuckets], S##_delta[kBuckets], S##_scan[kPW];     \
+  __shared__ int32_t S##_key[kTile], S##_val[kTile];                             \
+  const ScatterLds S{S##_cnt, S##_match, S##_start, S##_delta, S##_scan, S##_key, S##_val}
+
+struct ScatterOut {
+  int32_t *keys, *vals;
+  int32_t* feat;      // last pass: each point's feature rank, else null
+  int32_t* cell_cnt;  // last pass: the point count of every cell
+};
+
+// One tile of a radix pass: its valid elements ranked by digit in LDS and
+// stored at their places, so that lanes store consecutive positions.  dstart
+// is digit t's first place over all tiles and tile_off the earlier tiles'
+// count of digit t (thread t).  The last pass also writes each point's
+// feature rank and counts the points of every cell: its LDS tile is sorted by
+// the whole rank, and each run of one rank adds its length to the cell's count
+// (the run's first element adds -i, its last i + 1), so that every cell takes
+// a few adds.  (Counting per chunk of cells the same way puts thousands of
+// adds on a few addresses, which serialises them.)
+__device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t (&key)[kPR],
+                                             const int32_t (&val)[kPR], const bool (&valid)[kPR],
+                                             const uint32_t (&digit)[kPR], int32_t dstart,
+                                             int32_t tile_off, int shift, uint32_t mask,
+                                             const PGrid& g, const ScatterOut& o) {
   const int t = threadIdx.x;
-  const int lane = lane_id();
-  const int wid = t / kWave;
-  const int64_t n = FIRST ? g.P : (int64_t)*n_ptr;
+  int32_t pos[kPR];
+  int32_t n_valid_tile;
+  tile_ranks(digit, valid, S.cnt, S.match, S.start, S.scan, pos, &n_valid_tile);
+  S.delta[t] = dstart + tile_off - S.start[t];
+#pragma unroll
+  for (int r = 0; r < kPR; ++r) {
+    if (valid[r]) {
+      S.key[pos[r]] = key[r];
+      S.val[pos[r]] = val[r];
+    }
+  }
+  lds_barrier();
+  for (int i = t; i < n_valid_tile; i += kPT) {
+    const int32_t k = S.key[i];
+    const int32_t v = S.val[i];
+    const int32_t q = S.delta[((uint32_t)k >> shift) & mask] + i;
+    o.keys[q] = k;
+    o.vals[q] = v;
+    if (o.feat != nullptr) {  // (last pass; 32-bit: p < 2^31)
+      const uint32_t u = (uint32_t)v;
+      o.feat[q] = (int32_t)((u / (uint32_t)g.per_view) * (uint32_t)g.hw + u % (uint32_t)g.hw);
+      if (i == 0 || S.key[i - 1] != k) atomicAdd(&o.cell_cnt[k], -i);
+      if (i + 1 == n_valid_tile || S.key[i + 1] != k) atomicAdd(&o.cell_cnt[k], i + 1);
+    }
+  }
+}
+
+// Voxel indices of one tile's points in the wave-round layout (element =
+// tile base + wave * 256 + round * 64 + lane); past the end: -1 (dropped).
+__device__ __forceinline__ void load_tile_coor(const int32_t* __restrict__ coor, int64_t base,
+                                               int64_t n, int32_t (&x)[kPR], int32_t (&y)[kPR],
+                                               int32_t (&z)[kPR]) {
+  const int64_t e0 = base + threadIdx.x / kWave * kWaveSpan + lane_id();
+#pragma unroll
+  for (int r = 0; r < kPR; ++r) {
+    const int64_t e = e0 + r * kWave;
+    x[r] = e < n ? coor[3 * e + 0] : -1;
+    y[r] = e < n ? coor[3 * e + 1] : -1;
+    z[r] = e < n ? coor[3 * e + 2] : -1;
+  }
+}
+
+__device__ __forceinline__ void tile_keys(const int32_t (&x)[kPR], const int32_t (&y)[kPR],
+                                          const int32_t (&z)[kPR], int64_t base, const PGrid& g,
+                                          int shift, uint32_t mask, int32_t (&key)[kPR],
+                                          int32_t (&val)[kPR], bool (&valid)[kPR],
+                                          uint32_t (&digit)[kPR]) {
+  const int64_t e0 = base + threadIdx.x / kWave * kWaveSpan + lane_id();
+#pragma unroll
+  for (int r = 0; r < kPR; ++r) {
+    const int64_t e = e0 + r * kWave;
+    key[r] = rank_xyz(x[r], y[r], z[r], e, g);
+    val[r] = (int32_t)e;
+    valid[r] = key[r] >= 0;
+    digit[r] = valid[r] ? ((uint32_t)key[r] >> shift) & mask : 0u;
+  }
+}
+
+// First radix pass over the frustum points: a filter and a pass in one.
+__global__ __launch_bounds__(kPT) void k_pp_scatter_first(
+    const int32_t* __restrict__ coor, PGrid g, int shift, int bits,
+    const int32_t* __restrict__ hist, const int32_t* __restrict__ dtot, int64_t ntiles,
+    ScatterOut o, int32_t* __restrict__ count_out) {
+  BEVPOOL_SCATTER_LDS(S);
+  const int t = threadIdx.x;
+  const uint32_t mask = (1u << bits) - 1u;
+  const int64_t base = (int64_t)blockIdx.x * kTile;
+  int32_t x[kPR], y[kPR], z[kPR];
+  load_tile_coor(coor, base, g.P, x, y, z);
+  // digit t's first place (an exclusive scan of the digit totals) and the
+  // earlier tiles' count of it
+  const int32_t dt = t <= (int)mask ? dtot[t] : 0;
+  const int32_t tile_off = t <= (int)mask ? hist[(int64_t)t * ntiles + blockIdx.x] : 0;
+  int32_t n_kept;
+  const int32_t dstart = block_exclusive_scan<kPT, true>(dt, S.scan, &n_kept);
+  if (blockIdx.x == 0 && t == 0) *count_out = n_kept;
+  int32_t key[kPR], val[kPR];
+  bool valid[kPR];
+  uint32_t digit[kPR];
+  tile_keys(x, y, z, base, g, shift, mask, key, val, valid, digit);
+  scatter_tile(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
+}
+
+// A later radix pass over the n kept points (tiles past n do nothing).
+__global__ __launch_bounds__(kPT) void k_pp_scatter_next(
+    PGrid g, const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
+    const int32_t* __restrict__ n_ptr, int shift, int bits, const int32_t* __restrict__ hist,
+    const int32_t* __restrict__ dtot, int64_t ntiles, ScatterOut o) {
+  BEVPOOL_SCATTER_LDS(S);
+  const int t = threadIdx.x;
+  const int64_t n = *n_ptr;
   const int64_t tile0 = (int64_t)blockIdx.x * kTile;
-  if (!FIRST && tile0 >= n) return;  // (uniform: a tile past the kept points)
-  const int64_t base = tile0 + wid * kWaveSpan;
+  if (tile0 >= n) return;  // (uniform: a tile past the kept points)
+  const int64_t base = tile0 + t / kWave * kWaveSpan + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
   int32_t key[kPR], val[kPR];
   bool valid[kPR];
   uint32_t digit[kPR];
 #pragma unroll
   for (int r = 0; r < kPR; ++r) {
-    const int64_t e = base + r * kWave + lane;
-    if (FIRST) {
-      key[r] = e < n ? rank_or_drop(coor, e, g) : -1;
-      val[r] = (int32_t)e;
-      valid[r] = key[r] >= 0;
-    } else {
-      valid[r] = e < n;
-      key[r] = valid[r] ? keys_in[e] : 0;
-      val[r] = valid[r] ? vals_in[e] : 0;
-    }
-    digit[r] = ((uint32_t)key[r] >> shift) & mask;
-    if (!valid[r]) digit[r] = 0;
+    const int64_t e = base + r * kWave;
+    valid[r] = e < n;
+    key[r] = valid[r] ? keys_in[e] : 0;
+    val[r] = valid[r] ? vals_in[e] : 0;
+    digit[r] = valid[r] ? ((uint32_t)key[r] >> shift) & mask : 0u;
   }
-  // this tile's first place of each digit: the digit's global start (an
-  // exclusive scan of the digit totals) plus the earlier tiles' counts
   const int32_t dt = t <= (int)mask ? dtot[t] : 0;
   const int32_t tile_off = t <= (int)mask ? hist[(int64_t)t * ntiles + blockIdx.x] : 0;
   int32_t n_kept;
-  const int32_t dstart = block_exclusive_scan<kPT>(dt, s_scan, &n_kept);
-  int32_t pos[kPR];
-  int32_t n_valid_tile;
-  tile_ranks(digit, valid, cnt, match, s_start, s_scan, pos, &n_valid_tile);
-  s_delta[t] = dstart + tile_off - s_start[t];
-#pragma unroll
-  for (int r = 0; r < kPR; ++r) {
-    if (valid[r]) {
-      s_key[pos[r]] = key[r];
-      s_val[pos[r]] = val[r];
-    }
-  }
-  if (FIRST && blockIdx.x == 0 && t == 0) *count_out = n_kept;
-  __syncthreads();
-  for (int i = t; i < n_valid_tile; i += kPT) {
-    const int32_t k = s_key[i];
-    const int32_t v = s_val[i];
-    const int32_t q = s_delta[((uint32_t)k >> shift) & mask] + i;
-    keys_out[q] = k;
-    vals_out[q] = v;
-    if (feat_out != nullptr) {  // (last pass; 32-bit: p < 2^31)
-      const uint32_t u = (uint32_t)v;
-      feat_out[q] = (int32_t)((u / (uint32_t)g.per_view) * (uint32_t)g.hw + u % (uint32_t)g.hw);
-      if (i == 0 || s_key[i - 1] != k) atomicAdd(&cell_cnt[k], -i);
-      if (i + 1 == n_valid_tile || s_key[i + 1] != k) atomicAdd(&cell_cnt[k], i + 1);
-    }
-  }
+  const int32_t dstart = block_exclusive_scan<kPT, true>(dt, S.scan, &n_kept);
+  scatter_tile(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
 }
 
-// One block: the occupied cells in ascending order with their first point
-// and point count, and the number of them.
-__global__ __launch_bounds__(1024) void k_pp_intervals(const int32_t* __restrict__ cell_cnt,
-                                                       int64_t cells, int64_t cap,
-                                                       int32_t* __restrict__ starts,
-                                                       int32_t* __restrict__ lengths,
-                                                       int32_t* __restrict__ count_out) {
-  constexpr int kT = 1024, kPer = 16;
-  __shared__ int32_t s_scan[kT / kWave];
-  int32_t carry = 0, icarry = 0;
-  for (int64_t b0 = 0; b0 < cells; b0 += (int64_t)kT * kPer) {
-    const int64_t i0 = b0 + (int64_t)threadIdx.x * kPer;
-    int32_t v[kPer];
-    if (i0 + kPer <= cells) {
-      const int4* q = reinterpret_cast<const int4*>(cell_cnt + i0);
-#pragma unroll
-      for (int k = 0; k < kPer / 4; ++k) {
-        const int4 x = q[k];
-        v[4 * k] = x.x;
-        v[4 * k + 1] = x.y;
-        v[4 * k + 2] = x.z;
-        v[4 * k + 3] = x.w;
-      }
-    } else {
-#pragma unroll
-      for (int k = 0; k < kPer; ++k) v[k] = i0 + k < cells ? cell_cnt[i0 + k] : 0;
-    }
+// The cells are taken in chunks of 2^chunk_shift >= kIChunk cells, at most
+// kMaxIChunks of them.  First the point total and the occupied-cell count of
+// every chunk; then each chunk's block adds up those of the chunks before it,
+// scans its own cells and stores its intervals through LDS, so that
+// consecutive lanes store consecutive entries.
+constexpr int kIChunkShift = 10;
+constexpr int kIChunk = 1 << kIChunkShift;  // cells per sub-chunk: one int4 per thread
+static_assert(kIChunk == 4 * kPT, "one int4 of counts per thread");
+constexpr int kMaxIChunks = 1024;
+
+__device__ __forceinline__ int4 load_counts4(const int32_t* __restrict__ cnt, int64_t c0,
+                                             int64_t cells) {
+  if (c0 + 4 <= cells) return *reinterpret_cast<const int4*>(cnt + c0);  // (c0 % 4 == 0)
+  int4 v;
+  v.x = c0 + 0 < cells ? cnt[c0 + 0] : 0;
+  v.y = c0 + 1 < cells ? cnt[c0 + 1] : 0;
+  v.z = c0 + 2 < cells ? cnt[c0 + 2] : 0;
+  v.w = c0 + 3 < cells ? cnt[c0 + 3] : 0;
+  return v;
+}
+
+__global__ __launch_bounds__(kPT) void k_pp_chunk_totals(const int32_t* __restrict__ cell_cnt,
+                                                         int64_t cells, int chunk_shift,
+                                                         int2* __restrict__ chunk_tot) {
+  __shared__ int32_t s_scan[kPW];
+  const int64_t c_begin = (int64_t)blockIdx.x << chunk_shift;
+  const int64_t c_end = min<int64_t>(cells, c_begin + (int64_t(1) << chunk_shift));
+  int32_t s = 0, o = 0;
+  for (int64_t c0 = c_begin + 4 * threadIdx.x; c0 < c_end; c0 += kIChunk) {
+    const int4 v = load_counts4(cell_cnt, c0, c_end);
+    s += v.x + v.y + v.z + v.w;
+    o += (v.x > 0) + (v.y > 0) + (v.z > 0) + (v.w > 0);
+  }
+  int32_t st, ot;
+  block_exclusive_scan<kPT>(s, s_scan, &st);
+  block_exclusive_scan<kPT>(o, s_scan, &ot);
+  if (threadIdx.x == 0) chunk_tot[blockIdx.x] = make_int2(st, ot);
+}
+
+__global__ __launch_bounds__(kPT) void k_pp_intervals(const int32_t* __restrict__ cell_cnt,
+                                                      int64_t cells, int chunk_shift,
+                                                      const int2* __restrict__ chunk_tot,
+                                                      int64_t cap, int32_t* __restrict__ starts,
+                                                      int32_t* __restrict__ lengths,
+                                                      int32_t* __restrict__ count_out) {
+  __shared__ int32_t s_scan[kPW];
+  __shared__ int32_t s_st[kIChunk], s_ln[kIChunk];
+  const int t = threadIdx.x;
+  // the points and the occupied cells of the earlier chunks
+  int32_t ps = 0, po = 0;
+  for (int k = t; k < (int)blockIdx.x; k += kPT) {
+    const int2 x = chunk_tot[k];
+    ps += x.x;
+    po += x.y;
+  }
+  int32_t carry, icarry;
+  block_exclusive_scan<kPT>(ps, s_scan, &carry);
+  block_exclusive_scan<kPT>(po, s_scan, &icarry);
+  const int64_t c_begin = (int64_t)blockIdx.x << chunk_shift;
+  const int64_t c_end = min<int64_t>(cells, c_begin + (int64_t(1) << chunk_shift));
+  for (int64_t b0 = c_begin; b0 < c_end; b0 += kIChunk) {
+    const int4 x = load_counts4(cell_cnt, b0 + 4 * t, c_end);
+    const int32_t v[4] = {x.x, x.y, x.z, x.w};
     int32_t s = 0, o = 0;
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) {
+    for (int k = 0; k < 4; ++k) {
       s += v[k];
       o += v[k] > 0 ? 1 : 0;
     }
     int32_t tot, otot;
-    int32_t off = carry + block_exclusive_scan<kT>(s, s_scan, &tot);
-    int32_t ioff = icarry + block_exclusive_scan<kT>(o, s_scan, &otot);
+    int32_t off = carry + block_exclusive_scan<kPT>(s, s_scan, &tot);
+    int32_t loc = block_exclusive_scan<kPT>(o, s_scan, &otot);
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) {
+    for (int k = 0; k < 4; ++k) {
       if (v[k] > 0) {
-        if (ioff < cap) {
-          starts[ioff] = off;
-          lengths[ioff] = v[k];
-        }
-        ++ioff;
+        s_st[loc] = off;
+        s_ln[loc] = v[k];
+        ++loc;
       }
       off += v[k];
     }
+    __syncthreads();
+    for (int i = t; i < otot; i += kPT) {
+      const int64_t q = (int64_t)icarry + i;
+      if (q < cap) {
+        starts[q] = s_st[i];
+        lengths[q] = s_ln[i];
+      }
+    }
+    __syncthreads();
     carry += tot;
     icarry += otot;
   }
-  if (threadIdx.x == 0) *count_out = icarry;
+  if (blockIdx.x == gridDim.x - 1 && t == 0) *count_out = icarry;
 }
 
 int bits_for_cells(int64_t cells) {  // bits of the ranks 0 .. cells - 1 (at least 1)
@@ -357,6 +485,10 @@ PrepareLayout prepare_layout(const Dims& d) {
   L.hist = take((size_t)kBuckets * (size_t)L.ntiles);
   L.digit_totals = take(kBuckets);
   L.cell_counts = take((size_t)d.cells);
+  L.chunk_shift = kIChunkShift;
+  while (((d.cells - 1) >> L.chunk_shift) + 1 > kMaxIChunks) ++L.chunk_shift;
+  L.nchunks = ((d.cells - 1) >> L.chunk_shift) + 1;
+  L.chunk_totals = take(2 * (size_t)L.nchunks);
   L.total = off;
   return L;
 }
@@ -373,6 +505,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
   int32_t* hist = W(L.hist);
   int32_t* dtot = W(L.digit_totals);
   int32_t* cell_cnt = W(L.cell_counts);
+  int2* chunk_tot = reinterpret_cast<int2*>(ws + L.chunk_totals);
   PGrid g;
   g.P = d.P;
   g.per_sample = (int32_t)(d.N * d.per_view);
@@ -382,6 +515,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
   g.Y = (int32_t)d.Y;
   g.Z = (int32_t)d.Z;
   const unsigned tiles = (unsigned)L.ntiles;
+  const bool vec = reinterpret_cast<uintptr_t>(coor) % 16 == 0;  // 16-byte loads of coor
   // The passes alternate between the workspace and the output arrays so
   // that the last lands in (ranks_bev, ranks_depth).
   auto keys_of = [&](int pass) { return ((L.passes - 1 - pass) % 2 == 0) ? ranks_bev : keys_tmp; };
@@ -390,23 +524,25 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
     const int shift = pass * L.digit_bits;
     const int bits = std::min(L.digit_bits, L.key_bits - shift);
     const bool last = pass == L.passes - 1;
+    const ScatterOut o{keys_of(pass), vals_of(pass), last ? ranks_feat : nullptr, cell_cnt};
     if (pass == 0)
-      k_pp_hist0<<<tiles, kPT, 0, stream>>>(coor, g, bits, hist, L.ntiles, cell_cnt, d.cells);
+      k_pp_hist0<<<tiles, kPT, 0, stream>>>(coor, g, vec, bits, hist, L.ntiles, cell_cnt,
+                                            d.cells);
     else
       k_pp_hist<<<tiles, kPT, 0, stream>>>(keys_of(pass - 1), counts, shift, bits, hist, L.ntiles);
     k_pp_digit_scan<<<1u << bits, kPT, 0, stream>>>(hist, L.ntiles, dtot);
     if (pass == 0)
-      k_pp_scatter<true><<<tiles, kPT, 0, stream>>>(coor, g, nullptr, nullptr, nullptr, shift, bits,
-                                                    hist, dtot, L.ntiles, keys_of(0), vals_of(0),
-                                                    last ? ranks_feat : nullptr, counts + 0,
-                                                    cell_cnt);
+      k_pp_scatter_first<<<tiles, kPT, 0, stream>>>(coor, g, shift, bits, hist, dtot, L.ntiles, o,
+                                                    counts + 0);
     else
-      k_pp_scatter<false><<<tiles, kPT, 0, stream>>>(
-          nullptr, g, keys_of(pass - 1), vals_of(pass - 1), counts, shift, bits, hist, dtot,
-          L.ntiles, keys_of(pass), vals_of(pass), last ? ranks_feat : nullptr, nullptr, cell_cnt);
+      k_pp_scatter_next<<<tiles, kPT, 0, stream>>>(g, keys_of(pass - 1), vals_of(pass - 1), counts,
+                                                   shift, bits, hist, dtot, L.ntiles, o);
   }
   const int64_t cap = d.P < d.cells ? d.P : d.cells;
-  k_pp_intervals<<<1, 1024, 0, stream>>>(cell_cnt, d.cells, cap, starts, lengths, counts + 1);
+  const unsigned nchunks = (unsigned)L.nchunks;
+  k_pp_chunk_totals<<<nchunks, kPT, 0, stream>>>(cell_cnt, d.cells, L.chunk_shift, chunk_tot);
+  k_pp_intervals<<<nchunks, kPT, 0, stream>>>(cell_cnt, d.cells, L.chunk_shift, chunk_tot, cap,
+                                              starts, lengths, counts + 1);
   return hipGetLastError();
 }
 

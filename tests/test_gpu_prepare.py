@@ -19,14 +19,16 @@ def test_prepare_configs(name):
     _gpu.assert_plan_equal(got, oracle.prepare_ref(coor, cfg.shape()), name)
 
 
-# Shapes chosen to span several 4096-point tiles with ragged tails, one to
-# three radix passes (key bits 1..18) and B > 1.
+# Shapes chosen to span several 1024-point tiles with ragged tails, one to
+# three radix passes (key bits 1..21), B > 1, and interval chunks of one to
+# two 1024-cell parts (the last shape has 2^21 cells).
 RANDOM_SHAPES = [
     dict(B=1, N=1, D=1, H=1, W=1, C=4, X=1, Y=1, Z=1),          # P = 1, one cell
     dict(B=1, N=1, D=3, H=5, W=7, C=4, X=3, Y=2, Z=1),          # P = 105
     dict(B=2, N=3, D=11, H=13, W=17, C=8, X=40, Y=30, Z=2),     # P = 14586, 4 tiles + tail
     dict(B=3, N=2, D=7, H=9, W=100, C=8, X=256, Y=256, Z=1),    # 18-bit keys, 3 passes
     dict(B=1, N=6, D=5, H=16, W=44, C=64, X=512, Y=300, Z=1),   # 18 bits
+    dict(B=1, N=1, D=2, H=40, W=50, C=4, X=1024, Y=1024, Z=2),  # 21 bits, 2^21 cells
 ]
 
 
@@ -60,6 +62,22 @@ def test_prepare_edge_cases():
         _gpu.say(f"prepare edge case: {label}")
         got = _gpu.plan_to_numpy(_gpu.run_prepare(coor, shape))
         _gpu.assert_plan_equal(got, oracle.prepare_ref(coor, shape), label)
+
+
+def test_prepare_unaligned_coor():
+    """coor at a 4-byte offset from a 16-byte boundary takes the scalar loads;
+    the result is the same plan."""
+    import torch
+    from paper_2211_17111_amd import bevpool as bp
+    cfg = CONFIGS["bevdet"]
+    coor = frustum_coor(cfg)
+    _gpu.say("prepare with coor at a 4-byte offset")
+    flat = torch.empty(coor.size + 1, dtype=torch.int32, device=_gpu.DEV)
+    flat[1:].copy_(torch.from_numpy(coor.reshape(-1)))
+    dev_coor = flat[1:].view(coor.shape)
+    assert dev_coor.data_ptr() % 16 != 0
+    got = _gpu.plan_to_numpy(bp.prepare(dev_coor, cfg.shape()))
+    _gpu.assert_plan_equal(got, oracle.prepare_ref(coor, cfg.shape()), "unaligned coor")
 
 
 def test_prepare_deterministic():
