@@ -130,7 +130,8 @@ int bevpool_geometry(const bevpool_shape* shape, const bevpool_frustum* frustum,
  *
  * bevpool_prepare_workspace_size writes to *bytes the device scratch size
  * bevpool_prepare needs for `shape` (radix ping-pong buffers, digit
- * histograms of the tiles, the point count of every cell).
+ * histograms of the tiles, the point count of every cell and the totals of
+ * every chunk of cells).
  *
  * bevpool_prepare reads coor (P x 3 int32) and writes:
  *   ranks_depth, ranks_feat, ranks_bev   capacity P each; the first n_valid

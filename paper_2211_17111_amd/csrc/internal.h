@@ -39,7 +39,8 @@ struct PrepareLayout {
   size_t cell_counts;          // int32[cells]
   size_t chunk_totals;         // int2[nchunks]: points and occupied cells per chunk
   size_t total;                // bytes
-  int64_t ntiles;              // tiles of 1024 frustum points
+  int64_t ntiles0;             // first-pass tiles (1536 frustum points)
+  int64_t ntiles;              // later-pass tiles (1024 points; the hist's row length)
   int key_bits, passes, digit_bits;
   int chunk_shift;               // log2 of the cells per chunk
   int64_t nchunks;

@@ -3,15 +3,15 @@
 // trace (ties in frustum order), and find the interval of every occupied
 // cell.
 //
-//   hist0      per tile of 1024 frustum points: the BEV rank of each point
+//   hist0      per tile of 1536 frustum points: the BEV rank of each point
 //              (or drop) and the tile's histogram of the rank's low digit
 //   digit scan per digit, the exclusive scan of its tile counts
 //   scatter0   the kept points of each tile, stably ranked by the low digit
 //              in LDS, stored at their place of the first pass: a filter
 //              and a radix pass in one
 //   hist1 / digit scan / scatter1   the second (last) radix pass over the
-//              kept points, writing the plan's three rank arrays and the
-//              point count of every cell
+//              kept points in tiles of 1024, writing the plan's three rank
+//              arrays and the point count of every cell
 //   (more passes in between for grids of more than 2^16 cells)
 //   chunk totals / intervals   per chunk of cells, its point total and
 //              occupied-cell count; then the cells with points in ascending
@@ -19,7 +19,9 @@
 //              their count
 //
 // Every step is deterministic: tiles are ranked in element order and the
-// cell counts are sums.
+// cell counts are sums.  The first pass's tiles are larger so that its grid
+// (a wave per 384 frustum points) fits the GPU at once; the scatter's ranked
+// tile reuses the LDS of the ranking's counters for the same reason.
 
 #include <algorithm>
 
@@ -32,9 +34,10 @@ namespace {
 
 constexpr int kPT = 256;                 // threads per tile
 constexpr int kPW = kPT / kWave;         // 4 waves
-constexpr int kPR = 4;                   // rounds of 64 per wave
-constexpr int kTile = kPT * kPR;         // 1024 elements per tile
-constexpr int kWaveSpan = kPR * kWave;   // 256 consecutive elements per wave
+constexpr int kR0 = 6;                   // rounds of 64 per wave in the first pass
+constexpr int kR1 = 4;                   //   and in later passes
+constexpr int kTile0 = kPT * kR0;        // 1536 frustum points per first-pass tile
+constexpr int kTile1 = kPT * kR1;        // 1024 kept points per later tile
 constexpr int kBuckets = 256;            // most digits of a pass (8 bits)
 
 struct PGrid {
@@ -61,14 +64,15 @@ __device__ __forceinline__ int32_t rank_or_drop(const int32_t* __restrict__ coor
 }
 
 // Ranks of one tile held in the wave-round layout (element = tile base +
-// wave * 256 + round * 64 + lane): pos[r] = the element's place among the
+// wave * 64 * R + round * 64 + lane): pos[r] = the element's place among the
 // tile's valid elements ordered by (digit, element), s_start[d] the first
 // place of digit d, *n_tile the number of valid elements.  cnt and match are
 // LDS scratch; all threads call it.  Its barriers order LDS only, so global
 // loads issued before it stay in flight.
-__device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR],
+template <int R>
+__device__ void tile_ranks(const uint32_t (&digit)[R], const bool (&valid)[R],
                            int32_t (*cnt)[kBuckets], uint32_t (*match)[kBuckets][2],
-                           int32_t* s_start, int32_t* s_scan, int32_t (&pos)[kPR],
+                           int32_t* s_start, int32_t* s_scan, int32_t (&pos)[R],
                            int32_t* n_tile) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
@@ -78,9 +82,9 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
   lds_barrier();
   // lanes with equal digits: each sets its bit in the wave's mask of its
   // digit, reads the mask back and clears it (LDS keeps one wave's order)
-  uint2 m[kPR];
+  uint2 m[R];
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) {
+  for (int r = 0; r < R; ++r) {
     uint32_t* w = match[wid][digit[r]];
     m[r] = make_uint2(0u, 0u);
     if (valid[r]) {
@@ -91,18 +95,18 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
   }
   // the lowest lane of each digit adds the digit's count to the wave's
   // counter; the returned value is the count in the wave's earlier rounds
-  int32_t below[kPR], leader[kPR], old[kPR];
+  int32_t below[R], leader[R], old[R];
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) {
+  for (int r = 0; r < R; ++r) {
     const uint64_t same = (uint64_t)m[r].x | ((uint64_t)m[r].y << 32);
     below[r] = rank_below(same);
     leader[r] = same != 0 ? (int32_t)__builtin_ctzll(same) : lane;
     old[r] = 0;
     if (same != 0 && below[r] == 0) old[r] = atomicAdd(&cnt[wid][digit[r]], __popcll(same));
   }
-  int32_t rank[kPR];
+  int32_t rank[R];
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) rank[r] = __shfl(old[r], leader[r], kWave) + below[r];
+  for (int r = 0; r < R; ++r) rank[r] = __shfl(old[r], leader[r], kWave) + below[r];
   lds_barrier();
   int32_t c[kPW];
   int tot = 0;  // digit t: each wave's offset within the digit, and its count
@@ -120,18 +124,21 @@ __device__ void tile_ranks(const uint32_t (&digit)[kPR], const bool (&valid)[kPR
   s_start[t] = start;
   lds_barrier();
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) pos[r] = cnt[wid][digit[r]] + rank[r];
+  for (int r = 0; r < R; ++r) pos[r] = cnt[wid][digit[r]] + rank[r];
 }
 
 static_assert(kBuckets == kPT, "one thread per digit");
 
 // Pass 0 histogram over the frustum points; the tiles also clear the cell
-// counts, which the last pass adds to.  With `vec` (coor 16-byte aligned) each thread of a whole tile reads its
-// four consecutive points as three 16-byte loads.
+// counts, which the last pass adds to.  A tile's points are read in groups of
+// four consecutive points per thread; with `vec` (coor 16-byte aligned) a
+// whole group is three 16-byte loads.
 __global__ __launch_bounds__(kPT) void k_pp_hist0(const int32_t* __restrict__ coor, PGrid g,
                                                   bool vec, int bits, int32_t* __restrict__ hist,
                                                   int64_t ntiles, int32_t* __restrict__ cell_cnt,
                                                   int64_t cells) {
+  constexpr int kGroups = kTile0 / 4;                 // groups of four points per tile
+  constexpr int kGPT = (kGroups + kPT - 1) / kPT;     // per thread
   __shared__ int32_t h[kBuckets];
   const int t = threadIdx.x;
   h[t] = 0;
@@ -140,28 +147,31 @@ __global__ __launch_bounds__(kPT) void k_pp_hist0(const int32_t* __restrict__ co
        c += kPT)
     cell_cnt[c] = 0;
   __syncthreads();
-  const int64_t base = (int64_t)blockIdx.x * kTile;
+  const int64_t base = (int64_t)blockIdx.x * kTile0;
   const uint32_t mask = (1u << bits) - 1u;
-  int32_t rk[kPR];
-  if (vec && base + kTile <= g.P) {
-    static_assert(kPR == 4, "four points per thread: three 16-byte loads");
-    const int64_t p0 = base + 4 * t;
-    const int4* q = reinterpret_cast<const int4*>(coor + 3 * p0);
-    const int4 a = q[0], b = q[1], c = q[2];
-    rk[0] = rank_xyz(a.x, a.y, a.z, p0 + 0, g);
-    rk[1] = rank_xyz(a.w, b.x, b.y, p0 + 1, g);
-    rk[2] = rank_xyz(b.z, b.w, c.x, p0 + 2, g);
-    rk[3] = rank_xyz(c.y, c.z, c.w, p0 + 3, g);
-  } else {
+  int32_t rk[kGPT][4];
 #pragma unroll
-    for (int k = 0; k < kPR; ++k) {
-      const int64_t p = base + k * kPT + t;
-      rk[k] = p < g.P ? rank_or_drop(coor, p, g) : -1;
+  for (int j = 0; j < kGPT; ++j) {
+    const int grp = t + j * kPT;
+    const int64_t p0 = base + 4 * grp;
+    if (grp < kGroups && vec && p0 + 4 <= g.P) {
+      const int4* q = reinterpret_cast<const int4*>(coor + 3 * p0);
+      const int4 a = q[0], b = q[1], c = q[2];
+      rk[j][0] = rank_xyz(a.x, a.y, a.z, p0 + 0, g);
+      rk[j][1] = rank_xyz(a.w, b.x, b.y, p0 + 1, g);
+      rk[j][2] = rank_xyz(b.z, b.w, c.x, p0 + 2, g);
+      rk[j][3] = rank_xyz(c.y, c.z, c.w, p0 + 3, g);
+    } else {
+#pragma unroll
+      for (int k = 0; k < 4; ++k)
+        rk[j][k] = grp < kGroups && p0 + k < g.P ? rank_or_drop(coor, p0 + k, g) : -1;
     }
   }
 #pragma unroll
-  for (int k = 0; k < kPR; ++k)
-    if (rk[k] >= 0) atomicAdd(&h[(uint32_t)rk[k] & mask], 1);
+  for (int j = 0; j < kGPT; ++j)
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      if (rk[j][k] >= 0) atomicAdd(&h[(uint32_t)rk[j][k] & mask], 1);
   __syncthreads();
   if (t <= (int)mask) hist[(int64_t)t * ntiles + blockIdx.x] = h[t];
 }
@@ -176,10 +186,10 @@ __global__ __launch_bounds__(kPT) void k_pp_hist(const int32_t* __restrict__ key
   h[t] = 0;
   __syncthreads();
   const int64_t n = *n_ptr;
-  const int64_t base = (int64_t)blockIdx.x * kTile;
+  const int64_t base = (int64_t)blockIdx.x * kTile1;
   const uint32_t mask = (1u << bits) - 1u;
 #pragma unroll
-  for (int k = 0; k < kPR; ++k) {
+  for (int k = 0; k < kR1; ++k) {
     const int64_t e = base + k * kPT + t;
     if (e < n) atomicAdd(&h[((uint32_t)keys[e] >> shift) & mask], 1);
   }
@@ -216,19 +226,23 @@ __global__ __launch_bounds__(kPT) void k_pp_digit_scan(int32_t* __restrict__ his
   if (threadIdx.x == 0) dtot[blockIdx.x] = carry;
 }
 
-// LDS of the scatter kernels.
+// LDS of the scatter kernels: the ranking's counters and digit masks, which
+// the ranked tile (keys, then values) takes over once the ranks are known.
 struct ScatterLds {
   int32_t (*cnt)[kBuckets];
   uint32_t (*match)[kBuckets][2];
   int32_t *start, *delta, *scan, *key, *val;
 };
 
-#define BEVPOOL_SCATTER_LDS(S)                                                   \
-  __shared__ int32_t S##_cnt[kPW][kBuckets];                                     \
-  __shared__ uint32_t S##_match[kPW][kBuckets][2];                               \
-  __shared__ int32_t S##_start[kBuckets], S##_delta[kBuckets], S##_scan[kPW];     \
-  __shared__ int32_t S##_key[kTile], S##_val[kTile];                             \
-  const ScatterLds S{S##_cnt, S##_match, S##_start, S##_delta, S##_scan, S##_key, S##_val}
+#define BEVPOOL_SCATTER_LDS(S, R)                                                   \
+  __shared__ __align__(16) int32_t S##_raw[kPW * kBuckets * 3];                    \
+  static_assert(2 * kPT * (R) <= kPW * kBuckets * 3, "the ranked tile fits");      \
+  __shared__ int32_t S##_start[kBuckets], S##_delta[kBuckets], S##_scan[kPW];       \
+  const ScatterLds S {                                                             \
+    reinterpret_cast<int32_t(*)[kBuckets]>(S##_raw),                               \
+        reinterpret_cast<uint32_t(*)[kBuckets][2]>(S##_raw + kPW * kBuckets),      \
+        S##_start, S##_delta, S##_scan, S##_raw, S##_raw + kPT * (R)               \
+  }
 
 struct ScatterOut {
   int32_t *keys, *vals;
@@ -245,18 +259,20 @@ struct ScatterOut {
 // (the run's first element adds -i, its last i + 1), so that every cell takes
 // a few adds.  (Counting per chunk of cells the same way puts thousands of
 // adds on a few addresses, which serialises them.)
-__device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t (&key)[kPR],
-                                             const int32_t (&val)[kPR], const bool (&valid)[kPR],
-                                             const uint32_t (&digit)[kPR], int32_t dstart,
+template <int R>
+__device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t (&key)[R],
+                                             const int32_t (&val)[R], const bool (&valid)[R],
+                                             const uint32_t (&digit)[R], int32_t dstart,
                                              int32_t tile_off, int shift, uint32_t mask,
                                              const PGrid& g, const ScatterOut& o) {
   const int t = threadIdx.x;
-  int32_t pos[kPR];
+  int32_t pos[R];
   int32_t n_valid_tile;
-  tile_ranks(digit, valid, S.cnt, S.match, S.start, S.scan, pos, &n_valid_tile);
+  tile_ranks<R>(digit, valid, S.cnt, S.match, S.start, S.scan, pos, &n_valid_tile);
   S.delta[t] = dstart + tile_off - S.start[t];
+  lds_barrier();  // (every rank read: the tile takes over the counters)
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) {
+  for (int r = 0; r < R; ++r) {
     if (valid[r]) {
       S.key[pos[r]] = key[r];
       S.val[pos[r]] = val[r];
@@ -278,48 +294,24 @@ __device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t 
   }
 }
 
-// Voxel indices of one tile's points in the wave-round layout (element =
-// tile base + wave * 256 + round * 64 + lane); past the end: -1 (dropped).
-__device__ __forceinline__ void load_tile_coor(const int32_t* __restrict__ coor, int64_t base,
-                                               int64_t n, int32_t (&x)[kPR], int32_t (&y)[kPR],
-                                               int32_t (&z)[kPR]) {
-  const int64_t e0 = base + threadIdx.x / kWave * kWaveSpan + lane_id();
-#pragma unroll
-  for (int r = 0; r < kPR; ++r) {
-    const int64_t e = e0 + r * kWave;
-    x[r] = e < n ? coor[3 * e + 0] : -1;
-    y[r] = e < n ? coor[3 * e + 1] : -1;
-    z[r] = e < n ? coor[3 * e + 2] : -1;
-  }
-}
-
-__device__ __forceinline__ void tile_keys(const int32_t (&x)[kPR], const int32_t (&y)[kPR],
-                                          const int32_t (&z)[kPR], int64_t base, const PGrid& g,
-                                          int shift, uint32_t mask, int32_t (&key)[kPR],
-                                          int32_t (&val)[kPR], bool (&valid)[kPR],
-                                          uint32_t (&digit)[kPR]) {
-  const int64_t e0 = base + threadIdx.x / kWave * kWaveSpan + lane_id();
-#pragma unroll
-  for (int r = 0; r < kPR; ++r) {
-    const int64_t e = e0 + r * kWave;
-    key[r] = rank_xyz(x[r], y[r], z[r], e, g);
-    val[r] = (int32_t)e;
-    valid[r] = key[r] >= 0;
-    digit[r] = valid[r] ? ((uint32_t)key[r] >> shift) & mask : 0u;
-  }
-}
-
 // First radix pass over the frustum points: a filter and a pass in one.
+// Element e of a tile is point base + wave * 64 * kR0 + round * 64 + lane.
 __global__ __launch_bounds__(kPT) void k_pp_scatter_first(
     const int32_t* __restrict__ coor, PGrid g, int shift, int bits,
     const int32_t* __restrict__ hist, const int32_t* __restrict__ dtot, int64_t ntiles,
     ScatterOut o, int32_t* __restrict__ count_out) {
-  BEVPOOL_SCATTER_LDS(S);
+  BEVPOOL_SCATTER_LDS(S, kR0);
   const int t = threadIdx.x;
   const uint32_t mask = (1u << bits) - 1u;
-  const int64_t base = (int64_t)blockIdx.x * kTile;
-  int32_t x[kPR], y[kPR], z[kPR];
-  load_tile_coor(coor, base, g.P, x, y, z);
+  const int64_t e0 = (int64_t)blockIdx.x * kTile0 + t / kWave * (kR0 * kWave) + lane_id();
+  int32_t x[kR0], y[kR0], z[kR0];
+#pragma unroll
+  for (int r = 0; r < kR0; ++r) {
+    const int64_t e = e0 + r * kWave;
+    x[r] = e < g.P ? coor[3 * e + 0] : -1;  // (-1: dropped)
+    y[r] = e < g.P ? coor[3 * e + 1] : -1;
+    z[r] = e < g.P ? coor[3 * e + 2] : -1;
+  }
   // digit t's first place (an exclusive scan of the digit totals) and the
   // earlier tiles' count of it
   const int32_t dt = t <= (int)mask ? dtot[t] : 0;
@@ -327,11 +319,18 @@ __global__ __launch_bounds__(kPT) void k_pp_scatter_first(
   int32_t n_kept;
   const int32_t dstart = block_exclusive_scan<kPT, true>(dt, S.scan, &n_kept);
   if (blockIdx.x == 0 && t == 0) *count_out = n_kept;
-  int32_t key[kPR], val[kPR];
-  bool valid[kPR];
-  uint32_t digit[kPR];
-  tile_keys(x, y, z, base, g, shift, mask, key, val, valid, digit);
-  scatter_tile(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
+  int32_t key[kR0], val[kR0];
+  bool valid[kR0];
+  uint32_t digit[kR0];
+#pragma unroll
+  for (int r = 0; r < kR0; ++r) {
+    const int64_t e = e0 + r * kWave;
+    key[r] = rank_xyz(x[r], y[r], z[r], e, g);
+    val[r] = (int32_t)e;
+    valid[r] = key[r] >= 0;
+    digit[r] = valid[r] ? ((uint32_t)key[r] >> shift) & mask : 0u;
+  }
+  scatter_tile<kR0>(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
 }
 
 // A later radix pass over the n kept points (tiles past n do nothing).
@@ -339,18 +338,18 @@ __global__ __launch_bounds__(kPT) void k_pp_scatter_next(
     PGrid g, const int32_t* __restrict__ keys_in, const int32_t* __restrict__ vals_in,
     const int32_t* __restrict__ n_ptr, int shift, int bits, const int32_t* __restrict__ hist,
     const int32_t* __restrict__ dtot, int64_t ntiles, ScatterOut o) {
-  BEVPOOL_SCATTER_LDS(S);
+  BEVPOOL_SCATTER_LDS(S, kR1);
   const int t = threadIdx.x;
   const int64_t n = *n_ptr;
-  const int64_t tile0 = (int64_t)blockIdx.x * kTile;
+  const int64_t tile0 = (int64_t)blockIdx.x * kTile1;
   if (tile0 >= n) return;  // (uniform: a tile past the kept points)
-  const int64_t base = tile0 + t / kWave * kWaveSpan + lane_id();
+  const int64_t base = tile0 + t / kWave * (kR1 * kWave) + lane_id();
   const uint32_t mask = (1u << bits) - 1u;
-  int32_t key[kPR], val[kPR];
-  bool valid[kPR];
-  uint32_t digit[kPR];
+  int32_t key[kR1], val[kR1];
+  bool valid[kR1];
+  uint32_t digit[kR1];
 #pragma unroll
-  for (int r = 0; r < kPR; ++r) {
+  for (int r = 0; r < kR1; ++r) {
     const int64_t e = base + r * kWave;
     valid[r] = e < n;
     key[r] = valid[r] ? keys_in[e] : 0;
@@ -361,7 +360,7 @@ __global__ __launch_bounds__(kPT) void k_pp_scatter_next(
   const int32_t tile_off = t <= (int)mask ? hist[(int64_t)t * ntiles + blockIdx.x] : 0;
   int32_t n_kept;
   const int32_t dstart = block_exclusive_scan<kPT, true>(dt, S.scan, &n_kept);
-  scatter_tile(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
+  scatter_tile<kR1>(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
 }
 
 // The cells are taken in chunks of 2^chunk_shift >= kIChunk cells, at most
@@ -470,7 +469,8 @@ int bits_for_cells(int64_t cells) {  // bits of the ranks 0 .. cells - 1 (at lea
 
 PrepareLayout prepare_layout(const Dims& d) {
   PrepareLayout L{};
-  L.ntiles = (d.P + kTile - 1) / kTile;
+  L.ntiles0 = (d.P + kTile0 - 1) / kTile0;
+  L.ntiles = (d.P + kTile1 - 1) / kTile1;
   L.key_bits = bits_for_cells(d.cells);
   L.passes = (L.key_bits + 7) / 8;
   L.digit_bits = (L.key_bits + L.passes - 1) / L.passes;
@@ -514,6 +514,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
   g.X = (int32_t)d.X;
   g.Y = (int32_t)d.Y;
   g.Z = (int32_t)d.Z;
+  const unsigned tiles0 = (unsigned)L.ntiles0;
   const unsigned tiles = (unsigned)L.ntiles;
   const bool vec = reinterpret_cast<uintptr_t>(coor) % 16 == 0;  // 16-byte loads of coor
   // The passes alternate between the workspace and the output arrays so
@@ -525,18 +526,18 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
     const int bits = std::min(L.digit_bits, L.key_bits - shift);
     const bool last = pass == L.passes - 1;
     const ScatterOut o{keys_of(pass), vals_of(pass), last ? ranks_feat : nullptr, cell_cnt};
+    const int64_t nt = pass == 0 ? L.ntiles0 : L.ntiles;  // tiles of this pass
     if (pass == 0)
-      k_pp_hist0<<<tiles, kPT, 0, stream>>>(coor, g, vec, bits, hist, L.ntiles, cell_cnt,
-                                            d.cells);
+      k_pp_hist0<<<tiles0, kPT, 0, stream>>>(coor, g, vec, bits, hist, nt, cell_cnt, d.cells);
     else
-      k_pp_hist<<<tiles, kPT, 0, stream>>>(keys_of(pass - 1), counts, shift, bits, hist, L.ntiles);
-    k_pp_digit_scan<<<1u << bits, kPT, 0, stream>>>(hist, L.ntiles, dtot);
+      k_pp_hist<<<tiles, kPT, 0, stream>>>(keys_of(pass - 1), counts, shift, bits, hist, nt);
+    k_pp_digit_scan<<<1u << bits, kPT, 0, stream>>>(hist, nt, dtot);
     if (pass == 0)
-      k_pp_scatter_first<<<tiles, kPT, 0, stream>>>(coor, g, shift, bits, hist, dtot, L.ntiles, o,
-                                                    counts + 0);
+      k_pp_scatter_first<<<tiles0, kPT, 0, stream>>>(coor, g, shift, bits, hist, dtot, nt, o,
+                                                     counts + 0);
     else
       k_pp_scatter_next<<<tiles, kPT, 0, stream>>>(g, keys_of(pass - 1), vals_of(pass - 1), counts,
-                                                   shift, bits, hist, dtot, L.ntiles, o);
+                                                   shift, bits, hist, dtot, nt, o);
   }
   const int64_t cap = d.P < d.cells ? d.P : d.cells;
   const unsigned nchunks = (unsigned)L.nchunks;
