@@ -32,6 +32,7 @@ Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import gc
 import hashlib
 import json
 import os
@@ -162,13 +163,21 @@ STALL_FACTOR = 10
 
 def _timed_pairs(n, pick, fn, stream, starts, ends):
     """Event pairs around n launches on `stream` (the current stream), each
-    chunk of launches enqueued while a spin kernel keeps the GPU busy."""
-    for c0 in range(0, n, TIMED_CHUNK):
-        torch.cuda._sleep(SPIN_CYCLES)
-        for i in range(c0, min(n, c0 + TIMED_CHUNK)):
-            starts[i].record(stream)
-            fn(pick(i))
-            ends[i].record(stream)
+    chunk of launches enqueued while a spin kernel keeps the GPU busy.
+    Python's cyclic garbage collector is run before and paused during the
+    enqueue: a full collection blocks the host for tens of ms, longer than
+    the spin kernel covers, and the GPU then waits inside an event pair."""
+    gc.collect()
+    gc.disable()
+    try:
+        for c0 in range(0, n, TIMED_CHUNK):
+            torch.cuda._sleep(SPIN_CYCLES)
+            for i in range(c0, min(n, c0 + TIMED_CHUNK)):
+                starts[i].record(stream)
+                fn(pick(i))
+                ends[i].record(stream)
+    finally:
+        gc.enable()
     torch.cuda.synchronize()
 
 
