@@ -140,7 +140,9 @@ struct ScheduleLayout {
   // workspace of the build by strips in LDS (schedule_local.hip)
   size_t wl_map, wl_rkey, wl_rnpts, wl_strip_np, wl_strip_p0, wl_strip_it0, wl_pix_count,
       wl_item_nseg, wl_cell_nseg, wl_fill, wl_slot0, wl_head_cell, wl_head_item, wl_slot_seg,
-      wl_total;
+      wl_cell_tot, wl_total;
+  int wl_cell_shift;        // log2 of the cells per chunk of the cell scans
+  int64_t wl_cell_chunks;
 };
 ScheduleLayout schedule_layout(const Dims& d, int64_t n_valid, int64_t n_intervals);
 

@@ -11,7 +11,7 @@
 // builder (prepare.hip), which remains for shapes whose strips exceed the
 // LDS bounds below.
 //
-// Launches: init, map, strips, plan, emit, cells, segments, slots.
+// Launches: init, map, strips, plan, emit, cell totals, cells, segments, slots.
 
 #include <algorithm>
 
@@ -402,6 +402,7 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
   __shared__ int32_t s_bad;
   __shared__ int32_t s_sp0[kPlanStrips + 1];
   __shared__ int32_t s_ip0[kPlanItems + 1];
+  __shared__ int32_t s_rows[17 * kLT];
   const int t = threadIdx.x;
   if (t == 0) s_bad = 0;
   const bool lds_strips = strips <= kPlanStrips;
@@ -500,10 +501,33 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
   __syncthreads();
   for (int w = t; w < shares; w += kLT)
     if (share_item0[w + 1] - share_item0[w] > kShareItems) s_bad = 1;
-  // 4. first pixel-major pair of every feature row
-  const int32_t rtot = block_scan16(pix_count, rows, s_scan,
-                                    [&](int64_t r, int32_t excl, int32_t) { pix_pair0[r] = excl; });
-  __syncthreads();
+  // 4. first pixel-major pair of every feature row, 16 rows per thread and
+  // step; the prefixes go through LDS (17 words per thread, against bank
+  // conflicts) so that lanes store consecutive entries
+  int32_t rtot = 0;
+  for (int64_t base = 0; base < rows; base += 16 * kLT) {
+    const int64_t i0 = base + 16 * (int64_t)t;
+    int32_t v[16];
+    load16(pix_count, i0, rows, v);
+    int32_t sum = 0;
+#pragma unroll
+    for (int k = 0; k < 16; ++k) sum += v[k];
+    int32_t tot;
+    int32_t off = rtot + block_exclusive_scan<kLT>(sum, s_scan, &tot);
+#pragma unroll
+    for (int k = 0; k < 16; ++k) {
+      s_rows[17 * t + k] = off;
+      off += v[k];
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < 16; ++j) {
+      const int e = j * kLT + t;  // element of this step, staged at 17 * (e / 16) + e % 16
+      if (base + e < rows) pix_pair0[base + e] = s_rows[17 * (e >> 4) + (e & 15)];
+    }
+    __syncthreads();
+    rtot += tot;
+  }
   if (t == 0) {
     pix_pair0[rows] = rtot;
     hdr[kHdrShares] = shares;
@@ -623,65 +647,150 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
   }
 }
 
-// One block: the first segment of every item, and over the cells: the first
-// slot of each cell with several segments, the list of those cells, the
-// empty cells, and the counts in the header.
-__global__ __launch_bounds__(kLT) void k_ls_cells(
+// The cells in chunks of 2^chunk_shift >= kCChunk cells, at most
+// kMaxCChunks of them.  First each chunk's totals: the slots of its cells with
+// several segments, their number, and its number of empty cells.
+constexpr int kCT = 256;             // threads of the cell-scan kernels
+constexpr int kCChunkShift = 10;
+constexpr int kCChunk = 1 << kCChunkShift;  // cells per step of a block: 4 per thread
+static_assert(kCChunk == 4 * kCT, "one int4 of counts per thread");
+constexpr int kMaxCChunks = 1024;
+
+// a[i0 .. i0 + 4) with in-range flags (a and i0 aligned to 4 ints)
+__device__ __forceinline__ int4 load4(const int32_t* __restrict__ a, int64_t i0, int64_t n) {
+  if (i0 + 4 <= n) return *reinterpret_cast<const int4*>(a + i0);
+  return make_int4(i0 < n ? a[i0] : 0, i0 + 1 < n ? a[i0 + 1] : 0, i0 + 2 < n ? a[i0 + 2] : 0,
+                   i0 + 3 < n ? a[i0 + 3] : 0);
+}
+
+__global__ __launch_bounds__(kCT) void k_ls_cell_totals(const int32_t* __restrict__ cell_nseg,
+                                                        int64_t cells, int chunk_shift,
+                                                        int4* __restrict__ chunk_tot) {
+  __shared__ int32_t s_scan[kCT / kWave];
+  const int64_t c_begin = (int64_t)blockIdx.x << chunk_shift;
+  const int64_t c_end = min<int64_t>(cells, c_begin + (int64_t(1) << chunk_shift));
+  int32_t ss = 0, sc = 0, se = 0;
+  for (int64_t c0 = c_begin + 4 * threadIdx.x; c0 < c_end; c0 += kCChunk) {
+    const int4 x = load4(cell_nseg, c0, c_end);
+    const int32_t v[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      ss += v[k] > 1 ? v[k] : 0;
+      sc += v[k] > 1 ? 1 : 0;
+      se += (c0 + k < c_end && v[k] == 0) ? 1 : 0;
+    }
+  }
+  int32_t ts, tc, te;
+  block_exclusive_scan<kCT>(ss, s_scan, &ts);
+  block_exclusive_scan<kCT>(sc, s_scan, &tc);
+  block_exclusive_scan<kCT>(se, s_scan, &te);
+  if (threadIdx.x == 0) chunk_tot[blockIdx.x] = make_int4(ts, tc, te, 0);
+}
+
+// Blocks 0 .. nchunks - 1: the first slot of each cell with several segments,
+// the list of those cells with their first slots, and the list of empty
+// cells, each chunk adding the totals of the chunks before it; the lists go
+// through LDS so that lanes store consecutive entries.  Block nchunks: the
+// first segment of every item (an exclusive scan of the items' segment
+// counts) and the segment count.
+__global__ __launch_bounds__(kCT) void k_ls_cells(
     int32_t* __restrict__ hdr, const int32_t* __restrict__ item_nseg, int64_t items_cap,
-    const int32_t* __restrict__ cell_nseg, int64_t cells, int32_t* __restrict__ item_seg0,
+    const int32_t* __restrict__ cell_nseg, int64_t cells, int chunk_shift,
+    const int4* __restrict__ chunk_tot, int32_t nchunks, int32_t* __restrict__ item_seg0,
     int32_t* __restrict__ slot0, int32_t* __restrict__ comb_cell,
     int32_t* __restrict__ comb_slot0, int64_t comb_cap, int32_t* __restrict__ empty,
     int64_t empty_cap) {
-  __shared__ int32_t s_scan[kLW];
+  __shared__ int32_t s_scan[kCT / kWave];
+  __shared__ int32_t s_a[kCChunk], s_b[kCChunk], s_e[kCChunk];
   const int t = threadIdx.x;
-  const int64_t n_items = min<int64_t>(hdr[kHdrItems], items_cap);
-  const int32_t n_segs = block_scan16(item_nseg, n_items, s_scan,
-                                      [&](int64_t i, int32_t excl, int32_t) { item_seg0[i] = excl; });
-  // three scans over the cells at once: slots, cells with several segments,
-  // empty cells
-  constexpr int64_t kStep = 16 * (int64_t)kLT;
-  int32_t cs = 0, cc = 0, ce = 0;
-  for (int64_t base = 0; base < cells; base += kStep) {
-    const int64_t i0 = base + 16 * (int64_t)t;
-    int32_t v[16];
-    load16(cell_nseg, i0, cells, v);
+  if ((int32_t)blockIdx.x == nchunks) {  // (uniform)
+    const int64_t n_items = min<int64_t>(hdr[kHdrItems], items_cap);
+    int32_t carry = 0;
+    for (int64_t b0 = 0; b0 < n_items; b0 += kCChunk) {
+      const int4 x = load4(item_nseg, b0 + 4 * t, n_items);
+      const int32_t v[4] = {x.x, x.y, x.z, x.w};
+      int32_t tot;
+      int32_t off = carry + block_exclusive_scan<kCT>(v[0] + v[1] + v[2] + v[3], s_scan, &tot);
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        s_a[4 * t + k] = off;
+        off += v[k];
+      }
+      __syncthreads();
+      for (int i = t; i < kCChunk; i += kCT)
+        if (b0 + i < n_items) item_seg0[b0 + i] = s_a[i];
+      __syncthreads();
+      carry += tot;
+    }
+    if (t == 0) {
+      if (n_items == hdr[kHdrItems]) item_seg0[n_items] = carry;
+      hdr[kHdrSegs] = carry;
+    }
+    return;
+  }
+  // the totals of the chunks before this one
+  int32_t ps = 0, pc = 0, pe = 0;
+  for (int k = t; k < (int)blockIdx.x; k += kCT) {
+    const int4 x = chunk_tot[k];
+    ps += x.x;
+    pc += x.y;
+    pe += x.z;
+  }
+  int32_t cs, cc, ce;
+  block_exclusive_scan<kCT>(ps, s_scan, &cs);
+  block_exclusive_scan<kCT>(pc, s_scan, &cc);
+  block_exclusive_scan<kCT>(pe, s_scan, &ce);
+  const int64_t c_begin = (int64_t)blockIdx.x << chunk_shift;
+  const int64_t c_end = min<int64_t>(cells, c_begin + (int64_t(1) << chunk_shift));
+  for (int64_t b0 = c_begin; b0 < c_end; b0 += kCChunk) {
+    const int64_t c0 = b0 + 4 * t;
+    const int4 x = load4(cell_nseg, c0, c_end);
+    const int32_t v[4] = {x.x, x.y, x.z, x.w};
     int32_t ss = 0, sc = 0, se = 0;
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const bool in = i0 + k < cells;
+    for (int k = 0; k < 4; ++k) {
       ss += v[k] > 1 ? v[k] : 0;
       sc += v[k] > 1 ? 1 : 0;
-      se += (in && v[k] == 0) ? 1 : 0;
+      se += (c0 + k < c_end && v[k] == 0) ? 1 : 0;
     }
     int32_t ts, tc, te;
-    int32_t so = cs + block_exclusive_scan<kLT>(ss, s_scan, &ts);
-    int32_t co = cc + block_exclusive_scan<kLT>(sc, s_scan, &tc);
-    int32_t eo = ce + block_exclusive_scan<kLT>(se, s_scan, &te);
+    int32_t so = cs + block_exclusive_scan<kCT>(ss, s_scan, &ts);
+    int32_t co = block_exclusive_scan<kCT>(sc, s_scan, &tc);
+    int32_t eo = block_exclusive_scan<kCT>(se, s_scan, &te);
 #pragma unroll
-    for (int k = 0; k < 16; ++k) {
-      const int64_t c = i0 + k;
-      if (c >= cells) continue;
+    for (int k = 0; k < 4; ++k) {
+      const int64_t c = c0 + k;
+      if (c >= c_end) continue;
       if (v[k] > 1) {
         slot0[c] = so;
-        if (co < comb_cap) {
-          comb_cell[co] = (int32_t)c;
-          comb_slot0[co] = so;
-        }
+        s_a[co] = (int32_t)c;
+        s_b[co] = so;
         so += v[k];
         ++co;
       } else if (v[k] == 0) {
-        if (eo < empty_cap) empty[eo] = (int32_t)c;
+        s_e[eo] = (int32_t)c;
         ++eo;
       }
     }
+    __syncthreads();
+    for (int i = t; i < tc; i += kCT) {
+      const int64_t q = (int64_t)cc + i;
+      if (q < comb_cap) {
+        comb_cell[q] = s_a[i];
+        comb_slot0[q] = s_b[i];
+      }
+    }
+    for (int i = t; i < te; i += kCT) {
+      const int64_t q = (int64_t)ce + i;
+      if (q < empty_cap) empty[q] = s_e[i];
+    }
+    __syncthreads();
     cs += ts;
     cc += tc;
     ce += te;
   }
-  if (t == 0) {
-    if (n_items == hdr[kHdrItems]) item_seg0[n_items] = n_segs;
+  if ((int32_t)blockIdx.x == nchunks - 1 && t == 0) {
     comb_slot0[min<int64_t>(cc, comb_cap)] = cs;
-    hdr[kHdrSegs] = n_segs;
     hdr[kHdrSlots] = cs;
     hdr[kHdrComb] = cc;
     hdr[kHdrEmpty] = ce;
@@ -777,6 +886,10 @@ void local_schedule_ws(const Dims& d, ScheduleLayout& L) {
   L.wl_head_cell = take(nv);
   L.wl_head_item = take(nv);
   L.wl_slot_seg = take(nv);
+  L.wl_cell_shift = kCChunkShift;
+  while (((d.cells - 1) >> L.wl_cell_shift) + 1 > kMaxCChunks) ++L.wl_cell_shift;
+  L.wl_cell_chunks = ((d.cells - 1) >> L.wl_cell_shift) + 1;
+  L.wl_cell_tot = take(4 * (size_t)L.wl_cell_chunks);
   L.wl_total = off;
 }
 
@@ -837,9 +950,13 @@ hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t
       item_nseg, cell_nseg, head_cell, head_item, S(L.pair_rd0), reinterpret_cast<uint32_t*>(S(L.pair_ln)),
       reinterpret_cast<uint16_t*>(S(L.pair_seg)), S(L.bp_cell),
       reinterpret_cast<uint32_t*>(S(L.bp_dn)));
-  k_ls_cells<<<1, kLT, 0, stream>>>(hdr, item_nseg, L.items_cap, cell_nseg, d.cells, S(L.item_seg0),
-                                    slot0, S(L.comb_cell), S(L.comb_slot0), L.n_occ, S(L.empty),
-                                    L.n_empty);
+  int4* cell_tot = reinterpret_cast<int4*>(ws + L.wl_cell_tot);
+  const int32_t nchunks = (int32_t)L.wl_cell_chunks;
+  k_ls_cell_totals<<<(unsigned)nchunks, kCT, 0, stream>>>(cell_nseg, d.cells, L.wl_cell_shift,
+                                                         cell_tot);
+  k_ls_cells<<<(unsigned)nchunks + 1, kCT, 0, stream>>>(
+      hdr, item_nseg, L.items_cap, cell_nseg, d.cells, L.wl_cell_shift, cell_tot, nchunks,
+      S(L.item_seg0), slot0, S(L.comb_cell), S(L.comb_slot0), L.n_occ, S(L.empty), L.n_empty);
   k_ls_segments<<<g_nv, 256, 0, stream>>>(hdr, reinterpret_cast<const uint32_t*>(S(L.pair_ln)),
                                           reinterpret_cast<const uint16_t*>(S(L.pair_seg)),
                                           head_cell, head_item, S(L.item_seg0), cell_nseg, slot0,
