@@ -67,6 +67,19 @@ def remove_stale_objects() -> list[str]:
     return removed
 
 
+def check_defined(lib: str) -> None:
+    """Fail when the library leaves one of its own symbols undefined (a
+    kernel whose launch stub the host pass did not emit links silently into
+    a shared library and only fails when the library is loaded)."""
+    res = subprocess.run(["nm", "-D", "--undefined-only", lib], stdout=subprocess.PIPE,
+                         stderr=subprocess.STDOUT, text=True)
+    if res.returncode != 0:
+        raise RuntimeError(f"nm failed on {lib}: {res.stdout}")
+    own = [l.split()[-1] for l in res.stdout.splitlines() if "bevpool" in l]
+    if own:
+        raise RuntimeError(f"{lib} leaves {len(own)} of its own symbols undefined, e.g. {own[0]}")
+
+
 def build(verbose: bool = False) -> str:
     os.makedirs(BUILD, exist_ok=True)
     for name in remove_stale_objects():
@@ -84,6 +97,7 @@ def build(verbose: bool = False) -> str:
         objs = list(ex.map(compile_one, SOURCES))
     tmp = LIB_PATH + ".tmp"
     _run([cc, "-shared", "-fPIC", f"--offload-arch={ARCH}", *objs, "-o", tmp], verbose)
+    check_defined(tmp)
     os.replace(tmp, LIB_PATH)
     # the measurement probe, a library of its own (bench.py loads it)
     pobj = os.path.join(BUILD, "stream_probe.o")

@@ -47,6 +47,14 @@ namespace bevpool {
 
 namespace {
 
+// 16 bytes per lane from memory straight into LDS (global_load_lds_dwordx4):
+// lane i of the wave writes at lds + 16 i, lds being the same for the wave.
+// (A plain device function: inside the kernel template the builtin keeps the
+// host pass from emitting the kernel's launch stub.)
+__device__ __forceinline__ void global_to_lds16(const void* g, void* lds) {
+  __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)lds, 16, 0, 0);
+}
+
 // One workgroup per CU: kLoadWaves waves fetch the next item into one LDS
 // buffer while the other waves walk the current item in the other.
 constexpr int kNT = 1024;
@@ -326,6 +334,45 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // can be, surplus lanes repeating an in-range address: a load under a branch
   // makes the compiler wait for it where the branch joins.
   const int lt = tid;
+  // Rows of 16-byte vectors, one per staged slot, go from memory straight into
+  // LDS (global_load_lds_dwordx4: lane i of a wave writes its 16 bytes at the
+  // wave's LDS address + 16 i, the staged layout).  They take no registers and
+  // are issued before the item's other loads, so that rows, records and
+  // destinations share one round trip to memory; a strip's vectors fill at
+  // most kStripBytes, so kStripBytes / 16 / NT rounds cover them.  The wait
+  // for the loads after them (memory loads complete in order) also waits for
+  // these.  Other widths go through registers.
+  constexpr bool kDirectRows = kNV == 1 && sizeof(RawT) == 16;
+  auto stage_rows_direct = [&](const Geo& g, int b, auto nt_tag) {
+    constexpr int NT = decltype(nt_tag)::value;
+    constexpr int kLoadRows = kStripBytes / 16 / NT;
+    static_assert(NT % kWave == 0 && kLoadRows * NT * 16 == kStripBytes, "whole waves and rounds");
+    const int nvec = g.npix * rowvec;
+    RawT* const s_rows = buf_rows(b);
+#pragma unroll
+    for (int r = 0; r < kLoadRows; ++r) {
+      const int idx = r * NT + lt;  // (a wave's lanes take consecutive slots)
+      global_to_lds16(vec_addr(g, min(idx, nvec - 1)), s_rows + (idx & ~(kWave - 1)));
+    }
+  };
+  // the depth scores of a pair's points kDepthBurst .. n - 1 added to sum in
+  // point order, four loads at a time (clamped indices; runs longer than
+  // kDepthBurst points are few)
+  auto depth_tail = [&](float& sum, int32_t rd0, int n, double lq) {
+    for (int j0 = kDepthBurst; j0 < n; j0 += 4) {
+      TIn x[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t p = (int64_t)rd0 + (int64_t)min(j0 + u, n - 1) * hw;
+        x[u] = depth[min(max(p, (int64_t)0), a.P - 1)];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const int64_t p = (int64_t)rd0 + (int64_t)(j0 + u) * hw;
+        if (j0 + u < n && p >= 0 && p < a.P) sum += score(x[u], lq);
+      }
+    }
+  };
   auto load_item = [&](const ItemHdr& h, int b, auto nt_tag) {
     constexpr int NT = decltype(nt_tag)::value;
     constexpr int kLoadRows = kStripBytes / 16 / NT;  // 16-byte row vectors per thread
@@ -338,22 +385,27 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     RawT* const s_rows = buf_rows(b);
     PairRec* const s_pr = buf_pr(b);
     int32_t* const s_dest = buf_dest(b);
-    // rows and destinations, kLoadRounds rounds of loads in flight
-    for (int r0 = 0; r0 < kLoadRows; r0 += kRB) {
-      RawT rv[kRB];
+    if constexpr (kDirectRows) {
+      stage_rows_direct(g, b, nt_tag);
+    } else {
+      // rows, kRB vectors per thread in flight
+      for (int r0 = 0; r0 < kLoadRows; r0 += kRB) {
+        RawT rv[kRB];
 #pragma unroll
-      for (int u = 0; u < kRB; ++u)
-        rv[u] = *vec_addr(g, min((r0 + u) * NT + lt, nvec - 1));
+        for (int u = 0; u < kRB; ++u)
+          rv[u] = *vec_addr(g, min((r0 + u) * NT + lt, nvec - 1));
 #pragma unroll
-      for (int u = 0; u < kRB; ++u) {
-        const int idx = (r0 + u) * NT + lt;
-        if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
+        for (int u = 0; u < kRB; ++u) {
+          const int idx = (r0 + u) * NT + lt;
+          if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
+        }
       }
+      for (int idx = kLoadRows * NT + lt; idx < nvec; idx += NT)
+        s_rows[vec_slot(idx)] = *vec_addr(g, idx);
     }
-    for (int idx = kLoadRows * NT + lt; idx < nvec; idx += NT)
-      s_rows[vec_slot(idx)] = *vec_addr(g, idx);
-    for (int j = lt; j < h.nseg; j += NT) s_dest[j] = a.seg_dest[h.g0 + j];
-    // pair records and their depth scores, kPB pairs per thread at a time
+    // pair records and their depth scores, kPB pairs per thread at a time;
+    // the destinations are loaded between a batch's records and its depth
+    // scores (the records have arrived once the destinations have)
     for (int q0 = 0; q0 < kLP; q0 += kPB) {
       int32_t rd0[kPB];
       uint32_t ln[kPB];
@@ -365,6 +417,8 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         ln[q] = a.pair_ln[k];
         sg[q] = a.pair_seg[k];
       }
+      if (q0 == 0)
+        for (int j = lt; j < h.nseg; j += NT) s_dest[j] = a.seg_dest[h.g0 + j];
       float dv[kPB][kDepthBurst];
       double lq[kPB];
 #pragma unroll
@@ -388,10 +442,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
           float sum = dv[q][0];
 #pragma unroll
           for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
-          for (int j = kDepthBurst; j < n; ++j) {
-            const int64_t p = (int64_t)rd0[q] + j * hw;
-            if (p >= 0 && p < a.P) sum += score(depth[p], lq[q]);
-          }
+          depth_tail(sum, rd0[q], n, lq[q]);
           const uint32_t lp = ln[q] & kPairPixel;
           const bool ok = lp < (uint32_t)g.npix;
           const uint32_t sgc = min(sg[q], (uint32_t)(h.nseg - 1));
@@ -403,6 +454,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         }
       }
     }
+    if constexpr (kDirectRows) __builtin_amdgcn_s_waitcnt(0);  // (the rows are in LDS)
   };
 
   // ---- the loading waves' item loads, with the item's pair records (depth
@@ -431,6 +483,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     RawT* const s_rows = buf_rows(b);
     PairRec* const s_pr = buf_pr(b);
     int32_t* const s_dest = buf_dest(b);
+    if constexpr (kDirectRows) stage_rows_direct(g, b, std::integral_constant<int, kLoadThreads>{});
     float dv[kLPL][kDepthBurst];
     double lq[kLPL];
 #pragma unroll
@@ -448,19 +501,21 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     uint32_t sg[kLPL];
 #pragma unroll
     for (int q = 0; q < kLPL; ++q) sg[q] = a.pair_seg[h.p0 + min(q * kLoadThreads + lt, max(h.np - 1, 0))];
+    if constexpr (!kDirectRows) {
 #pragma unroll
-    for (int r0 = 0; r0 < kRowsL; r0 += kRowsH) {
-      RawT rv[kRowsH];
+      for (int r0 = 0; r0 < kRowsL; r0 += kRowsH) {
+        RawT rv[kRowsH];
 #pragma unroll
-      for (int u = 0; u < kRowsH; ++u) rv[u] = *vec_addr(g, min((r0 + u) * kLoadThreads + lt, nvec - 1));
+        for (int u = 0; u < kRowsH; ++u) rv[u] = *vec_addr(g, min((r0 + u) * kLoadThreads + lt, nvec - 1));
 #pragma unroll
-      for (int u = 0; u < kRowsH; ++u) {
-        const int idx = (r0 + u) * kLoadThreads + lt;
-        if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
+        for (int u = 0; u < kRowsH; ++u) {
+          const int idx = (r0 + u) * kLoadThreads + lt;
+          if (idx < nvec) s_rows[vec_slot(idx)] = rv[u];
+        }
       }
+      for (int idx = kRowsL * kLoadThreads + lt; idx < nvec; idx += kLoadThreads)
+        s_rows[vec_slot(idx)] = *vec_addr(g, idx);
     }
-    for (int idx = kRowsL * kLoadThreads + lt; idx < nvec; idx += kLoadThreads)
-      s_rows[vec_slot(idx)] = *vec_addr(g, idx);
     for (int j = lt; j < h.nseg; j += kLoadThreads) s_dest[j] = a.seg_dest[h.g0 + j];
 #pragma unroll
     for (int q = 0; q < kLPL; ++q) {
@@ -471,10 +526,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         float sum = dv[q][0];
 #pragma unroll
         for (int j = 1; j < kDepthBurst; ++j) sum += dv[q][j];
-        for (int j = kDepthBurst; j < n; ++j) {
-          const int64_t p = (int64_t)pf.rd0[q] + j * hw;
-          if (p >= 0 && p < a.P) sum += score(depth[p], lq[q]);
-        }
+        depth_tail(sum, pf.rd0[q], n, lq[q]);
         const uint32_t lp = pf.ln[q] & kPairPixel;
         const bool ok = lp < (uint32_t)g.npix;
         const uint32_t sgc = min(sg[q], (uint32_t)(h.nseg - 1));
@@ -485,6 +537,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
         s_pr[k] = rec;
       }
     }
+    if constexpr (kDirectRows) __builtin_amdgcn_s_waitcnt(0);  // (the rows are in LDS)
   };
 
   // ---- walking waves: lane group lg of walking wave wv owns an equal range
