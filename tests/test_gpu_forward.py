@@ -290,6 +290,8 @@ def test_schedule_edge_shapes():
     ("12384 points per strip", dict(B=1, N=1, D=129, H=32, W=6, C=80, X=40, Y=40, Z=1)),
     ("32-bit keys", dict(B=1, N=1, D=128, H=32, W=3, C=80, X=512, Y=512, Z=1)),
     ("33-bit keys", dict(B=1, N=1, D=128, H=32, W=3, C=80, X=512, Y=512, Z=2)),
+    # 2^21 cells: the cell scans take chunks of 2048 cells (at most 1024 chunks)
+    ("2^21 cells", dict(B=1, N=1, D=8, H=32, W=6, C=80, X=1024, Y=1024, Z=2)),
 ])
 def test_schedule_local_bounds(label, shape):
     """Shapes on both sides of the bounds of the strip-local build give the
