@@ -15,9 +15,9 @@
 //                  chunk (up to 64 vectors), taking one share of the items
 //                  (a contiguous run of strips) and two LDS item buffers:
 //     1. loading waves fill one buffer with the next item: the strip's feature
-//        rows (this chunk, 16-byte loads), the item's pair records, each
-//        pair's weight (the sum of its points' depth scores, gathered) and
-//        the segment destinations;
+//        rows (this chunk; 16-byte vectors go straight from memory into
+//        LDS), the item's pair records, each pair's weight (the sum of its
+//        points' depth scores, gathered) and the segment destinations;
 //     2. meanwhile walking waves sum the current item from the other buffer:
 //        its pairs are cut into equal ranges, one per lane group (one lane per
 //        vector of the chunk); each group sums weight x feature row over its
