@@ -554,6 +554,7 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
   __shared__ int32_t s_scan[kLW];
   __shared__ int32_t s_items[kLItems + 1];
   __shared__ int32_t s_iseg[kLItems + 1];
+  __shared__ int32_t s_pix0[kLBuckets];  // first pixel-major pair of each pixel of the strip
   const int t = threadIdx.x;
   const int lane = lane_id();
   const int wid = t / kWave;
@@ -569,6 +570,10 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
   g.strip(s, bn, h0, w0, bhs, bws);
   const int32_t rb_base = (bn / g.N) * g.zyx;
   for (int k = t; k <= K; k += kLT) s_items[k] = item_pair0[it0 + k];
+  for (int lp = t; lp < bhs * bws; lp += kLT) {  // (at most kLBuckets pixels)
+    const int32_t hl = lp / bws;
+    s_pix0[lp] = pix_pair0[(int64_t)bn * g.hw + (int64_t)(h0 + hl) * g.W + w0 + (lp - hl * bws)];
+  }
   __syncthreads();
 
   const int span = ((np + kLT - 1) / kLT) * kWave;
@@ -639,9 +644,7 @@ __global__ __launch_bounds__(kLT) void k_ls_emit(
     const int e = wid * span + r * kWave + lane;
     if (e >= np) continue;
     const int32_t lp = (int32_t)digit[r];
-    const int32_t hl = lp / bws;
-    const int64_t row = (int64_t)bn * g.hw + (int64_t)(h0 + hl) * g.W + w0 + (lp - hl * bws);
-    const int32_t q = pix_pair0[row] + (dest[r] - cnt[0][lp]);
+    const int32_t q = s_pix0[lp] + (dest[r] - cnt[0][lp]);
     bp_cell[q] = rb_base + (int32_t)(key[r] >> rb_shift);
     bp_dn[q] = (key[r] & dmask) | ((uint32_t)npts[r] << 16);
   }
