@@ -30,7 +30,7 @@ def _lse_bound(ref):
     return 4 * 2.0 ** -24 + 1e-12 * np.abs(ref)
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large"])
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train"])
 def test_lse_matches_oracle(name):
     cfg = CONFIGS[name]
     _gpu.say(f"depth log-sum-exp: {name}")
@@ -59,7 +59,7 @@ def test_lse_depth_bins(D):
     assert worst <= 1.0, D
 
 
-@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "voxel3d"])
+@pytest.mark.parametrize("name", ["tiny", "bevdet", "headline", "large", "train", "voxel3d"])
 def test_fused_forward_every_element(name):
     cfg = CONFIGS[name]
     shape = cfg.shape()
