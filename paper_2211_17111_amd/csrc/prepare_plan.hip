@@ -68,12 +68,15 @@ __device__ __forceinline__ int32_t rank_or_drop(const int32_t* __restrict__ coor
 // tile's valid elements ordered by (digit, element), s_start[d] the first
 // place of digit d, *n_tile the number of valid elements.  cnt and match are
 // LDS scratch; all threads call it.  Its barriers order LDS only, so global
-// loads issued before it stay in flight.
-template <int R>
+// loads issued before it stay in flight.  The lanes of equal digit are found
+// with the LDS digit masks, or with BALLOT by one ballot per digit bit (the
+// later passes: their digits repeat within a wave much more, and the lanes
+// of one digit would queue their ORs on one mask word).
+template <int R, bool BALLOT = false>
 __device__ void tile_ranks(const uint32_t (&digit)[R], const bool (&valid)[R],
                            int32_t (*cnt)[kBuckets], uint32_t (*match)[kBuckets][2],
                            int32_t* s_start, int32_t* s_scan, int32_t (&pos)[R],
-                           int32_t* n_tile) {
+                           int32_t* n_tile, int bits = 8) {
   const int lane = lane_id();
   const int wid = threadIdx.x / kWave;
   const int t = threadIdx.x;
@@ -83,14 +86,28 @@ __device__ void tile_ranks(const uint32_t (&digit)[R], const bool (&valid)[R],
   // lanes with equal digits: each sets its bit in the wave's mask of its
   // digit, reads the mask back and clears it (LDS keeps one wave's order)
   uint2 m[R];
+  if constexpr (BALLOT) {
 #pragma unroll
-  for (int r = 0; r < R; ++r) {
-    uint32_t* w = match[wid][digit[r]];
-    m[r] = make_uint2(0u, 0u);
-    if (valid[r]) {
-      atomicOr(&w[lane >> 5], 1u << (lane & 31));
-      m[r] = *reinterpret_cast<const uint2*>(w);
-      *reinterpret_cast<uint2*>(w) = make_uint2(0u, 0u);
+    for (int r = 0; r < R; ++r) {
+      uint64_t same = wave_ballot(valid[r]);
+      for (int b = 0; b < bits; ++b) {
+        const bool on = (digit[r] >> b) & 1u;
+        const uint64_t x = wave_ballot(on);
+        same &= on ? x : ~x;
+      }
+      if (!valid[r]) same = 0;
+      m[r] = make_uint2((uint32_t)same, (uint32_t)(same >> 32));
+    }
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      uint32_t* w = match[wid][digit[r]];
+      m[r] = make_uint2(0u, 0u);
+      if (valid[r]) {
+        atomicOr(&w[lane >> 5], 1u << (lane & 31));
+        m[r] = *reinterpret_cast<const uint2*>(w);
+        *reinterpret_cast<uint2*>(w) = make_uint2(0u, 0u);
+      }
     }
   }
   // the lowest lane of each digit adds the digit's count to the wave's
@@ -259,7 +276,7 @@ struct ScatterOut {
 // (the run's first element adds -i, its last i + 1), so that every cell takes
 // a few adds.  (Counting per chunk of cells the same way puts thousands of
 // adds on a few addresses, which serialises them.)
-template <int R>
+template <int R, bool BALLOT = false>
 __device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t (&key)[R],
                                              const int32_t (&val)[R], const bool (&valid)[R],
                                              const uint32_t (&digit)[R], int32_t dstart,
@@ -268,7 +285,8 @@ __device__ __forceinline__ void scatter_tile(const ScatterLds& S, const int32_t 
   const int t = threadIdx.x;
   int32_t pos[R];
   int32_t n_valid_tile;
-  tile_ranks<R>(digit, valid, S.cnt, S.match, S.start, S.scan, pos, &n_valid_tile);
+  tile_ranks<R, BALLOT>(digit, valid, S.cnt, S.match, S.start, S.scan, pos, &n_valid_tile,
+                        __builtin_popcount(mask));
   S.delta[t] = dstart + tile_off - S.start[t];
   lds_barrier();  // (every rank read: the tile takes over the counters)
 #pragma unroll
@@ -360,7 +378,7 @@ __global__ __launch_bounds__(kPT) void k_pp_scatter_next(
   const int32_t tile_off = t <= (int)mask ? hist[(int64_t)t * ntiles + blockIdx.x] : 0;
   int32_t n_kept;
   const int32_t dstart = block_exclusive_scan<kPT, true>(dt, S.scan, &n_kept);
-  scatter_tile<kR1>(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
+  scatter_tile<kR1, true>(S, key, val, valid, digit, dstart, tile_off, shift, mask, g, o);
 }
 
 // The cells are taken in chunks of 2^chunk_shift >= kIChunk cells, at most
