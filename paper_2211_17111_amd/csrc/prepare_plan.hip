@@ -193,17 +193,19 @@ __global__ __launch_bounds__(kPT) void k_pp_hist0(const int32_t* __restrict__ co
   if (t <= (int)mask) hist[(int64_t)t * ntiles + blockIdx.x] = h[t];
 }
 
-// Later-pass histogram over the n kept points (tiles past n count nothing).
+// Later-pass histogram over the n kept points.  The grid is sized for all
+// frustum points; tiles past n return at once (no pass reads their counts).
 __global__ __launch_bounds__(kPT) void k_pp_hist(const int32_t* __restrict__ keys,
                                                  const int32_t* __restrict__ n_ptr, int shift,
                                                  int bits, int32_t* __restrict__ hist,
                                                  int64_t ntiles) {
   __shared__ int32_t h[kBuckets];
   const int t = threadIdx.x;
-  h[t] = 0;
-  __syncthreads();
   const int64_t n = *n_ptr;
   const int64_t base = (int64_t)blockIdx.x * kTile1;
+  if (base >= n) return;  // (uniform)
+  h[t] = 0;
+  __syncthreads();
   const uint32_t mask = (1u << bits) - 1u;
 #pragma unroll
   for (int k = 0; k < kR1; ++k) {
@@ -215,30 +217,44 @@ __global__ __launch_bounds__(kPT) void k_pp_hist(const int32_t* __restrict__ key
 }
 
 // One block per digit: exclusive scan of the digit's tile counts in place,
-// and the digit's total.
-__global__ __launch_bounds__(kPT) void k_pp_digit_scan(int32_t* __restrict__ hist, int64_t ntiles,
+// and the digit's total.  Later passes (n_ptr: the kept count) scan only the
+// tiles that hold kept points.
+__global__ __launch_bounds__(kPT) void k_pp_digit_scan(int32_t* __restrict__ hist, int64_t row,
+                                                       const int32_t* __restrict__ n_ptr,
                                                        int32_t* __restrict__ dtot) {
   __shared__ int32_t s_scan[kPW];
-  int32_t* a = hist + (int64_t)blockIdx.x * ntiles;
-  constexpr int kPer = 8;
+  int32_t* a = hist + (int64_t)blockIdx.x * row;
+  const int64_t ntiles =
+      n_ptr == nullptr ? row : min<int64_t>(row, ((int64_t)*n_ptr + kTile1 - 1) / kTile1);
+  // up to kChunks * kPT * kPer counts loaded at once, then scanned chunk by
+  // chunk (the scans' barriers order LDS only, so the loads stay in flight)
+  constexpr int kPer = 8, kChunks = 4;
+  constexpr int64_t kSpan = (int64_t)kPT * kPer;
   int32_t carry = 0;
-  for (int64_t b0 = 0; b0 < ntiles; b0 += (int64_t)kPT * kPer) {
-    const int64_t i0 = b0 + (int64_t)threadIdx.x * kPer;
-    int32_t v[kPer];
-    int32_t s = 0;
+  for (int64_t b0 = 0; b0 < ntiles; b0 += kSpan * kChunks) {
+    int32_t v[kChunks][kPer];
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      v[k] = i0 + k < ntiles ? a[i0 + k] : 0;
-      s += v[k];
-    }
-    int32_t tot;
-    int32_t off = carry + block_exclusive_scan<kPT>(s, s_scan, &tot);
+    for (int c = 0; c < kChunks; ++c) {
+      const int64_t i0 = b0 + c * kSpan + (int64_t)threadIdx.x * kPer;
 #pragma unroll
-    for (int k = 0; k < kPer; ++k) {
-      if (i0 + k < ntiles) a[i0 + k] = off;
-      off += v[k];
+      for (int k = 0; k < kPer; ++k) v[c][k] = i0 + k < ntiles ? a[i0 + k] : 0;
     }
-    carry += tot;
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+      if (b0 + c * kSpan >= ntiles) break;  // (uniform)
+      const int64_t i0 = b0 + c * kSpan + (int64_t)threadIdx.x * kPer;
+      int32_t s = 0;
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) s += v[c][k];
+      int32_t tot;
+      int32_t off = carry + block_exclusive_scan<kPT, true>(s, s_scan, &tot);
+#pragma unroll
+      for (int k = 0; k < kPer; ++k) {
+        if (i0 + k < ntiles) a[i0 + k] = off;
+        off += v[c][k];
+      }
+      carry += tot;
+    }
   }
   if (threadIdx.x == 0) dtot[blockIdx.x] = carry;
 }
@@ -549,7 +565,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
       k_pp_hist0<<<tiles0, kPT, 0, stream>>>(coor, g, vec, bits, hist, nt, cell_cnt, d.cells);
     else
       k_pp_hist<<<tiles, kPT, 0, stream>>>(keys_of(pass - 1), counts, shift, bits, hist, nt);
-    k_pp_digit_scan<<<1u << bits, kPT, 0, stream>>>(hist, nt, dtot);
+    k_pp_digit_scan<<<1u << bits, kPT, 0, stream>>>(hist, nt, pass == 0 ? nullptr : counts, dtot);
     if (pass == 0)
       k_pp_scatter_first<<<tiles0, kPT, 0, stream>>>(coor, g, shift, bits, hist, dtot, nt, o,
                                                      counts + 0);
