@@ -58,6 +58,14 @@ def test_prepare_edge_cases():
                                                rng.integers(-2**31, 2**31 - 1, P),
                                                rng.integers(0, 2, P)], axis=1).astype(np.int32),
     }
+    # kept counts at and beside a later-pass tile boundary (1024 points): the
+    # later passes histogram and scan only the tiles holding kept points
+    for kept in (1023, 1024, 1025, 2048, 2049):
+        coor = np.full((P, 3), 99, dtype=np.int32)
+        idx = np.sort(rng.choice(P, kept, replace=False))
+        coor[idx] = np.stack([rng.integers(0, 16, kept), rng.integers(0, 16, kept),
+                              rng.integers(0, 2, kept)], axis=1)
+        cases[f"{kept} kept points"] = coor
     for label, coor in cases.items():
         _gpu.say(f"prepare edge case: {label}")
         got = _gpu.plan_to_numpy(_gpu.run_prepare(coor, shape))
