@@ -249,8 +249,13 @@ struct ReduceScatter {
   }
 };
 
+// The large-launch form (UMAX 4) of one-part rows is held to 5 waves per
+// SIMD (96 VGPRs): float16 rows of 8 channels need 104 and would run 4 (large:
+// 251 -> 230 us, at most 4 registers spilled); wider rows (NV > 1) would spill
+// heavily and are left to the compiler.
 template <typename TIn, typename TG, int VEC, int NV, int GS, int UMAX, int MW>
-__global__ __launch_bounds__(kBwdThreads) void k_bwd_pixels(
+__global__ __launch_bounds__(kBwdThreads)
+__attribute__((amdgpu_waves_per_eu(UMAX == 4 && NV == 1 ? 5 : 1))) void k_bwd_pixels(
     const TG* __restrict__ grad_out, const TIn* __restrict__ depth, const TIn* __restrict__ feat,
     TIn* __restrict__ grad_depth, TIn* __restrict__ grad_feat, PixArgs a) {
   constexpr int G = kWave / GS;
