@@ -734,8 +734,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // ---- the pipeline: item i is walked from buffer b while the loading
   // waves add up the cut segments of item i - 1 (published in buffer b ^ 1)
   // and then fill buffer b ^ 1 with item i + 1
-  // (records are read ahead where the walk leaves the registers for them)
-  constexpr bool kPrefetch = VEC < 8;
+  // (records are read ahead where the walk leaves the registers for them;
+  // not in the fused softmax forms, whose per-pair lse already takes them)
+  constexpr bool kPrefetch = VEC < 8 && !SM;
   load_item(header(i_begin), 0, std::integral_constant<int, kNT>{});
   PairPf pf;  // the second item's records
   if (kPrefetch && !walker && i_begin + 1 < i_begin + n_my) fetch_pairs(header(i_begin + 1), pf);
