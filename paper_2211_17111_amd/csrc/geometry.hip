@@ -14,50 +14,66 @@
 // contraction into fused multiply-adds, so the indices are reproducible
 // bit for bit on any IEEE double implementation that takes the same order.
 //
-// One thread per point p = (((b N + n) D + d) H + h) W + w, writing its
-// three int32 indices; the 16 camera words of (b, n) are shared by the
-// threads of a view and come from cache.
+// Point p = (((b N + n) D + d) H + h) W + w gets its three int32 indices
+// from the thread of its pixel (h, w) in view (b, n) that takes depth bins
+// d0 .. d0 + kGeoBins - 1: blocks cover a view's H W pixels (grid x), the
+// runs of depth bins (y) and the views (z; larger counts are walked in
+// strides).  A thread finds (h, w) with one 32-bit division (64-bit
+// divisions of p cost more than the float64 arithmetic) and reuses its
+// pixel's (u, v) for every bin; the 16 camera words of (b, n) are shared by
+// the threads of a view and come from cache.
 
 #include "internal.h"
 
 #include <math.h>
+
+#include <algorithm>
 
 namespace bevpool {
 
 namespace {
 
 constexpr int kGeoThreads = 256;
+constexpr int kGeoMaxGrid = 65535;  // grid y and z limit
+constexpr int kGeoBins = 8;         // depth bins per thread
 
 struct GeoParams {
   double stride, depth_start, depth_step;
   double lo[3], res[3];
-  int64_t P;
+  int64_t views;  // B * N
   int32_t D, H, W;
 };
 
 __global__ __launch_bounds__(kGeoThreads) void k_geometry(const double* __restrict__ cams,
                                                           GeoParams g, int32_t* __restrict__ coor) {
 #pragma clang fp contract(off)
-  const int64_t p = (int64_t)blockIdx.x * kGeoThreads + threadIdx.x;
-  if (p >= g.P) return;
-  const int64_t hw = (int64_t)g.H * g.W;
-  const int w = (int)(p % g.W);
-  const int h = (int)((p / g.W) % g.H);
-  const int d = (int)((p / hw) % g.D);
-  const int64_t view = p / (hw * g.D);
-  const double* c = cams + view * kCameraWords;
+  const int32_t hw = g.H * g.W;  // (< 2^31: P is)
+  const int32_t t = (int32_t)blockIdx.x * kGeoThreads + (int32_t)threadIdx.x;
+  if (t >= hw) return;
+  const int32_t h = t / g.W;
+  const int32_t w = t - h * g.W;
   const double u = ((double)w + 0.5) * g.stride;
   const double v = ((double)h + 0.5) * g.stride;
-  const double dep = g.depth_start + (double)d * g.depth_step;
-  const double xc = ((u - c[2]) * dep) / c[0];
-  const double yc = ((v - c[3]) * dep) / c[1];
-  const double zc = dep;
+  for (int64_t view = blockIdx.z; view < g.views; view += gridDim.z) {
+    const double* c = cams + view * kCameraWords;
+    for (int32_t d0 = blockIdx.y * kGeoBins; d0 < g.D; d0 += gridDim.y * kGeoBins) {
+      const int32_t d_end = min(d0 + kGeoBins, g.D);
+      for (int32_t d = d0; d < d_end; ++d) {
+        const int64_t p = (view * g.D + d) * hw + t;
+        const double dep = g.depth_start + (double)d * g.depth_step;
+        const double xc = ((u - c[2]) * dep) / c[0];
+        const double yc = ((v - c[3]) * dep) / c[1];
+        const double zc = dep;
 #pragma unroll
-  for (int i = 0; i < 3; ++i) {
-    const double e = ((c[4 + 3 * i] * xc + c[5 + 3 * i] * yc) + c[6 + 3 * i] * zc) + c[13 + i];
-    double idx = floor((e - g.lo[i]) / g.res[i]);
-    idx = fmin(fmax(idx, -1073741824.0), 1073741824.0);  // (+-2^30; a NaN stays NaN)
-    coor[p * 3 + i] = idx == idx ? (int32_t)idx : (int32_t)-1073741824;
+        for (int i = 0; i < 3; ++i) {
+          const double e =
+              ((c[4 + 3 * i] * xc + c[5 + 3 * i] * yc) + c[6 + 3 * i] * zc) + c[13 + i];
+          double idx = floor((e - g.lo[i]) / g.res[i]);
+          idx = fmin(fmax(idx, -1073741824.0), 1073741824.0);  // (+-2^30; a NaN stays NaN)
+          coor[p * 3 + i] = idx == idx ? (int32_t)idx : (int32_t)-1073741824;
+        }
+      }
+    }
   }
 }
 
@@ -74,12 +90,14 @@ hipError_t launch_geometry(const Dims& d, const bevpool_frustum& f, const double
     g.lo[i] = f.lo[i];
     g.res[i] = f.res[i];
   }
-  g.P = d.P;
+  g.views = d.B * d.N;
   g.D = (int32_t)d.D;
   g.H = (int32_t)d.H;
   g.W = (int32_t)d.W;
-  k_geometry<<<dim3((unsigned)((d.P + kGeoThreads - 1) / kGeoThreads)), dim3(kGeoThreads), 0,
-               stream>>>(cams, g, coor);
+  const dim3 grid((unsigned)((d.hw + kGeoThreads - 1) / kGeoThreads),
+                  (unsigned)std::min<int64_t>((d.D + kGeoBins - 1) / kGeoBins, kGeoMaxGrid),
+                  (unsigned)std::min<int64_t>(g.views, kGeoMaxGrid));
+  k_geometry<<<grid, dim3(kGeoThreads), 0, stream>>>(cams, g, coor);
   return hipGetLastError();
 }
 

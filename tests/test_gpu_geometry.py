@@ -49,3 +49,19 @@ def test_jittered_geometry_then_prepare():
         assert np.array_equal(getattr(plan, k)[:nv].cpu().numpy(), ref[k][:nv]), k
     assert np.array_equal(plan.interval_starts[:ni].cpu().numpy(), ref["interval_starts"][:ni])
     assert np.array_equal(plan.interval_lengths[:ni].cpu().numpy(), ref["interval_lengths"][:ni])
+
+
+@pytest.mark.parametrize("dhw", [(3, 1, 1), (5, 1, 257), (2, 17, 15), (130, 2, 3)])
+def test_geometry_ragged_shapes(dhw):
+    """Views of one pixel, of 257 pixels (a block and one more), of an odd
+    pixel count, and of more depth bins than pixels: the grid covers each
+    view's pixels in blocks, its depth bins and its views."""
+    cfg = CONFIGS["tiny"]
+    D, H, W = dhw
+    shape = dict(cfg.shape(), D=D, H=H, W=W)
+    _gpu.say(f"geometry ragged shape D={D} H={H} W={W}")
+    cams = rig_cameras(cfg)
+    got = bp.geometry(torch.from_numpy(cams).to(_gpu.DEV), frustum_params(cfg), shape)
+    torch.cuda.synchronize()
+    want = oracle.geometry_ref(cams, frustum_params(cfg), shape)
+    assert np.array_equal(got.cpu().numpy(), want), dhw
