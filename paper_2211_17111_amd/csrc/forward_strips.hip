@@ -65,13 +65,17 @@ constexpr int kLoadThreads = kLoadWaves * kWave;
 constexpr int kDepthBurst = 2;  // depth scores per pair loaded before any is summed
 constexpr int kRowBatch = 8;    // row vectors per loading thread in flight
 constexpr int kPairBatch = 8;   // pair records per loading thread in flight
-constexpr int kBufBytes = kStripBytes + kItemPairs * 12;  // rows | pair records | destinations
+// LDS of one item buffer for items of up to ip pairs: rows | pair records |
+// destinations
+constexpr int buf_bytes(int ip) { return kStripBytes + ip * 12; }
 constexpr int kHdrCache = 128;  // item headers of a workgroup kept in LDS
 constexpr int kCombThreads = 256;
 static_assert(kStripBytes % (16 * kLoadThreads) == 0, "row vectors split evenly over the loading threads");
-static_assert(kItemPairs % kNT == 0 && kItemPairs % kLoadThreads == 0,
+static_assert(kItemPairs % kNT == 0 && kItemPairs % kLoadThreads == 0 &&
+                  kItemPairsBig % kNT == 0 && kItemPairsBig % kLoadThreads == 0,
               "pair records split evenly over the loading threads");
-static_assert(kItemPairs <= 65536, "segment index fits 16 bits");
+static_assert(kItemPairsBig <= 65536, "segment index fits 16 bits");
+static_assert(2 * buf_bytes(kItemPairsBig) + 16 * 1024 <= 160 * 1024, "two big item buffers fit LDS");
 static_assert(kShareItems <= kHdrCache, "a share's item headers fit the cache");
 
 struct StripArgs {
@@ -90,6 +94,7 @@ struct StripArgs {
   float* slots;
   int64_t slot_cap;  // slots the workspace holds
   int32_t n_valid, n_occ, n_slots, items_cap;  // counts the launch was sized from
+  int32_t item_pairs;  // the item size the launch's kernel holds (schedule_item_pairs)
   const double* lse;  // fused depth softmax: per-pixel log-sum-exp of the logits (else unused)
   int32_t dhw;       // D * H * W (points of one view)
   int32_t C, H, W, bh, bw, nhb, nwb, strips;
@@ -101,7 +106,7 @@ struct StripArgs {
 __device__ __forceinline__ bool header_ok(const StripArgs& a) {
   const int32_t* hdr = a.hdr;
   return hdr[kHdrOcc] == a.n_occ && hdr[kHdrOccFound] == a.n_occ && hdr[kHdrValid] == a.n_valid &&
-         hdr[kHdrSlots] == a.n_slots;
+         hdr[kHdrSlots] == a.n_slots && hdr[kHdrItemPairs] == a.item_pairs;
 }
 
 struct PairRec {
@@ -111,7 +116,7 @@ struct PairRec {
 constexpr uint32_t kRecHead = 1u << 31;  // first pair of a segment
 constexpr int kRecSegShift = 19;
 constexpr uint32_t kRecOff = (1u << kRecSegShift) - 1;
-static_assert(kItemPairs <= (1 << (31 - kRecSegShift)), "segment index fits its field");
+static_assert(kItemPairsBig <= (1 << (31 - kRecSegShift)), "segment index fits its field");
 static_assert(kStripBytes / 2 <= (int)kRecOff + 1, "row offset (in staged elements) fits its field");
 
 // Raw element vector moved between memory and LDS without conversion.
@@ -188,7 +193,7 @@ struct ItemHdr {
 // SM: `depth` holds depth logits, and a point's depth score is
 // exp(logit - lse[pixel]) (the softmax over the pixel's depth bins, with the
 // log-sum-exp from k_depth_lse), formed as the points are gathered.
-template <typename TIn, typename TOut, int VEC, bool SM>
+template <typename TIn, typename TOut, int VEC, bool SM, int IP>
 __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ depth,
                                                     const TIn* __restrict__ feat,
                                                     TOut* __restrict__ out, StripArgs a) {
@@ -197,17 +202,18 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   constexpr int kNV = raw_parts<TIn, VEC>();  // staged vectors per lane and row
   constexpr int kPer = VEC / kNV;            // elements per staged vector
   // two buffers of [rows, then partial sums | pair records | segment destinations]
+  constexpr int kBufBytes = buf_bytes(IP);
   __shared__ __attribute__((aligned(16))) char smem[2 * kBufBytes];
   __shared__ int32_t s_hdr[3][kHdrCache + 1];  // strip, first pair, first segment
   __shared__ int4 s_meta[kWalkWaves * kWave];  // each lane group's last walked range
   __shared__ int32_t s_lsync;                  // arrivals of the loading waves (loader_sync)
 
   static_assert((int64_t)kWaves * kWave * 8 * sizeof(float) <= kStripBytes, "partial sums fit the row area");
-  static_assert(kItemPairs <= 65535, "pair indices fit 16 bits");
+  static_assert(IP <= 65535, "pair indices fit 16 bits");
   auto buf_rows = [&](int b) { return reinterpret_cast<RawT*>(smem + b * kBufBytes); };
   auto buf_pr = [&](int b) { return reinterpret_cast<PairRec*>(smem + b * kBufBytes + kStripBytes); };
   auto buf_dest = [&](int b) {
-    return reinterpret_cast<int32_t*>(smem + b * kBufBytes + kStripBytes + kItemPairs * sizeof(PairRec));
+    return reinterpret_cast<int32_t*>(smem + b * kBufBytes + kStripBytes + IP * sizeof(PairRec));
   };
 
   // This workgroup's items.  Workgroup w = (die, slot) of a die-major
@@ -289,7 +295,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     h.nseg = __builtin_amdgcn_readfirstlane(v[4]) - h.g0;
     // (bitwise or: no branches)
     const bool bad = (h.strip < 0) | (h.strip >= a.strips) | (h.p0 < 0) | (h.np < 1) |
-                     (h.np > kItemPairs) | (h.p0 + h.np > n_pairs) | (h.g0 < 0) | (h.nseg < 1) |
+                     (h.np > IP) | (h.p0 + h.np > n_pairs) | (h.g0 < 0) | (h.nseg < 1) |
                      (h.nseg > h.np) | (h.g0 + h.nseg > n_segs);
     if (bad) h = ItemHdr{0, 0, 0, 0, 0};  // an inconsistent header becomes an empty item
     return h;
@@ -377,7 +383,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
     constexpr int NT = decltype(nt_tag)::value;
     constexpr int kLoadRows = kStripBytes / 16 / NT;  // 16-byte row vectors per thread
     constexpr int kRB = whole_batch(kLoadRows, kRowBatch);
-    constexpr int kLP = kItemPairs / NT;  // pairs per thread
+    constexpr int kLP = IP / NT;  // pairs per thread
     constexpr int kPB = whole_batch(kLP, kPairBatch);
     static_assert(kLoadRows % kRB == 0 && kLP % kPB == 0, "whole batches");
     const Geo g = geometry(h.strip);
@@ -461,7 +467,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // rank, pixel and run) read one item ahead into registers (fetch_pairs):
   // the depth gathers, which need them, then go out first, beside the row
   // loads, and the LDS stores follow.
-  constexpr int kLPL = kItemPairs / kLoadThreads;  // pairs per loading thread
+  constexpr int kLPL = IP / kLoadThreads;  // pairs per loading thread
   constexpr int kRowsL = kStripBytes / 16 / kLoadThreads;  // row vectors per loading thread
   constexpr int kRowsH = kRowsL / 2;  // row vectors per batch
   static_assert(kRowsL % 2 == 0, "two row batches");
@@ -662,7 +668,7 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // destinations), and a record of its range.  The loading waves add the
   // parts up while the walking waves go on to the next item.
   constexpr int kMetaPrev = 1, kMetaNext = 2, kMetaLast = 4, kMetaEmpty = 8;
-  static_assert((int64_t)kWalkWaves * kWave * 8 * sizeof(float) <= kItemPairs * 12,
+  static_assert((int64_t)kWalkWaves * kWave * 8 * sizeof(float) <= IP * 12,
                 "last parts fit the pair records and destinations");
   auto part_first = [&](int b) { return reinterpret_cast<float*>(smem + b * kBufBytes); };
   auto part_last = [&](int b) { return reinterpret_cast<float*>(smem + b * kBufBytes + kStripBytes); };
@@ -735,8 +741,9 @@ __global__ __launch_bounds__(kNT) void k_fwd_strips(const TIn* __restrict__ dept
   // waves add up the cut segments of item i - 1 (published in buffer b ^ 1)
   // and then fill buffer b ^ 1 with item i + 1
   // (records are read ahead where the walk leaves the registers for them;
-  // not in the fused softmax forms, whose per-pair lse already takes them)
-  constexpr bool kPrefetch = VEC < 8 && !SM;
+  // not in the fused softmax forms, whose per-pair lse already takes them,
+  // nor for big items, whose records would not fit)
+  constexpr bool kPrefetch = VEC < 8 && !SM && IP <= kItemPairs;
   load_item(header(i_begin), 0, std::integral_constant<int, kNT>{});
   PairPf pf;  // the second item's records
   if (kPrefetch && !walker && i_begin + 1 < i_begin + n_my) fetch_pairs(header(i_begin + 1), pf);
@@ -864,8 +871,12 @@ hipError_t run(const Dims& d, const StripDims& sd, const void* depth, const void
   const int64_t per_die_slots = std::max<int64_t>(forward_workgroups() / kXcds,
                                                   a.items_cap / ((int64_t)kXcds * kHdrCache) + 1);
   const int blocks = (int)(per_die_slots * kXcds);
-  k_fwd_strips<TIn, TOut, VEC, SM><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
-      static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
+  if (a.item_pairs == kItemPairsBig)
+    k_fwd_strips<TIn, TOut, VEC, SM, kItemPairsBig><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
+        static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
+  else
+    k_fwd_strips<TIn, TOut, VEC, SM, kItemPairs><<<dim3((unsigned)blocks, chunks), dim3(kNT), 0, stream>>>(
+        static_cast<const TIn*>(depth), static_cast<const TIn*>(feat), o, a);
   const int64_t gpw = kWave / (CV < kWave ? CV : kWave);
   const int64_t entries = (int64_t)a.n_occ + a.n_empty;
   const int64_t per_block = gpw * (kCombThreads / kWave);
@@ -961,6 +972,9 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.n_occ = n_intervals;
   a.n_slots = n_slots;
   a.items_cap = (int32_t)L.items_cap;
+  // (the item size the schedule builders choose on this device; a schedule
+  // cut otherwise fails the header check)
+  a.item_pairs = schedule_item_pairs(n_valid, std::min<int64_t>(forward_workgroups(), kMaxShares));
   a.C = (int32_t)d.C;
   a.H = (int32_t)d.H;
   a.W = (int32_t)d.W;

@@ -72,7 +72,8 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //            falls in when less than kMinPiece pairs from it
 //   item     a run of one strip's pairs inside one share: a strip is cut at
 //            the share boundaries inside it, and each piece of L pairs into
-//            K = ceil(L / kItemPairs) items, item j starting at pair
+//            K = ceil(L / I) items, I the schedule's item size
+//            (schedule_item_pairs, in the header), item j starting at pair
 //            floor(j * L / K) of the piece
 //   segment  maximal run of pairs of one cell inside one item
 //   slot     a float32 row of the forward workspace holding one segment's
@@ -97,14 +98,23 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //   share_item0[kMaxShares + 1] first item of each share (+ end sentinel:
 //                               items), for the shares in the header
 constexpr int kItemPairs = 2048;          // most pairs of one forward item
+constexpr int kItemPairsBig = 3072;       //   of a schedule whose shares hold many items
+constexpr int64_t kBigItemPoints = 16384; // kept points per share from which items are big
 constexpr int kStripBytes = 32 * 1024;    // staged feature bytes of a strip (4-byte elements)
 constexpr uint32_t kPairHead = 1u << 15;  // pair_ln: first pair of a segment
 constexpr uint32_t kPairPixel = kPairHead - 1;
 constexpr int kHdrPairs = 0, kHdrItems = 1, kHdrSegs = 2, kHdrValid = 3, kHdrOcc = 4,
               kHdrOccFound = 5, kHdrEmpty = 6, kHdrSlots = 7, kHdrComb = 8, kHdrStrips = 9,
               kHdrShares = 10,     // S, the shares the items are cut at
-              kHdrSharesOk = 11;   // 1 if no share has more than kShareItems items
+              kHdrSharesOk = 11,   // 1 if no share has more than kShareItems items
+              kHdrItemPairs = 12;  // the item size the pieces were cut at
 constexpr int kMaxShares = 1024;   // most shares (workgroups of the scheduled forward)
+// Item size of a schedule of n_valid kept points cut into `shares` shares:
+// big items where each share holds many (a workgroup then walks a dozen or
+// more items, and each item stages its strip's rows once), else kItemPairs.
+inline int schedule_item_pairs(int64_t n_valid, int64_t shares) {
+  return shares > 0 && n_valid >= kBigItemPoints * shares ? kItemPairsBig : kItemPairs;
+}
 constexpr int kShareItems = 128;   // most items of a share the forward takes as one
 constexpr int kMinPiece = 512;     // share boundaries closer to a strip end move to it
 static_assert(kHdrPairs == BEVPOOL_SCHEDULE_PAIRS && kHdrItems == BEVPOOL_SCHEDULE_ITEMS &&

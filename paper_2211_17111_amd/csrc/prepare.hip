@@ -462,13 +462,13 @@ __global__ void k_strips_end(const int32_t* __restrict__ hdr, int32_t* __restric
 // Items of every listed strip (0 past the last one, up to cap).
 __global__ __launch_bounds__(256) void k_item_counts(const int32_t* __restrict__ hdr,
                                                      const int32_t* __restrict__ strip_p0,
-                                                     int64_t cap, int64_t shares,
+                                                     int64_t cap, int64_t shares, int64_t ip,
                                                      int32_t* __restrict__ count) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= cap) return;
   int32_t k = 0;
   if (j < hdr[kHdrStrips])
-    k = (int32_t)strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares,
+    k = (int32_t)strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares, ip,
                              [](int64_t, int64_t) {});
   count[j] = k;
 }
@@ -480,14 +480,14 @@ __global__ __launch_bounds__(256) void k_item_scatter(const int32_t* __restrict_
                                                       const int32_t* __restrict__ strip_p0,
                                                       const int32_t* __restrict__ offset,
                                                       int64_t items_cap, int64_t shares,
-                                                      int32_t* __restrict__ item_strip,
+                                                      int64_t ip, int32_t* __restrict__ item_strip,
                                                       int32_t* __restrict__ item_pair0,
                                                       int32_t* __restrict__ item_flag) {
   const int64_t j = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
   if (j >= hdr[kHdrStrips]) return;
   const int32_t sid = strip_id[j];
   const int64_t off = offset[j];
-  strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares, [&](int64_t i, int64_t first) {
+  strip_items(strip_p0[j], strip_p0[j + 1], hdr[kHdrPairs], shares, ip, [&](int64_t i, int64_t first) {
     const int64_t item = off + i;
     if (item >= items_cap) return;
     item_strip[item] = sid;
@@ -504,6 +504,7 @@ __global__ __launch_bounds__(kShareThreads) void k_share_items(int32_t* __restri
                                                                const int32_t* __restrict__ strip_p0,
                                                                const int32_t* __restrict__ item_pair0,
                                                                int64_t items_cap, int32_t shares,
+                                                               int32_t ip,
                                                                int32_t* __restrict__ share_item0) {
   __shared__ int32_t s_bad;
   if (threadIdx.x == 0) s_bad = 0;
@@ -535,6 +536,7 @@ __global__ __launch_bounds__(kShareThreads) void k_share_items(int32_t* __restri
   if (threadIdx.x == 0) {
     hdr[kHdrShares] = shares;
     hdr[kHdrSharesOk] = s_bad ? 0 : 1;
+    hdr[kHdrItemPairs] = ip;
   }
 }
 
@@ -901,15 +903,16 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
     k_strips_end<<<1, 64, 0, stream>>>(hdr, strip_p0);
     const unsigned g_s = (unsigned)((scap + 255) / 256);
     const int32_t shares = (int32_t)std::min<int64_t>(forward_workgroups(), kMaxShares);
-    k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, shares, icount);
+    const int32_t ip = schedule_item_pairs(n_valid, shares);
+    k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, shares, ip, icount);
     scan_exclusive(icount, scap, sums, hdr + kHdrItems, stream);
     int32_t* item_flag = W(L.ws_flags);
     k_fill_i32<<<g_nv, 256, 0, stream>>>(item_flag, n_valid, 0);
     k_item_scatter<<<g_s, 256, 0, stream>>>(hdr, strip_id, strip_p0, icount, L.items_cap, shares,
-                                            S(L.item_strip), S(L.item_pair0), item_flag);
+                                            ip, S(L.item_strip), S(L.item_pair0), item_flag);
     k_items_end<<<1, 64, 0, stream>>>(hdr, L.items_cap, S(L.item_pair0));
     k_share_items<<<1, kShareThreads, 0, stream>>>(hdr, strip_p0, S(L.item_pair0), L.items_cap, shares,
-                                                   S(L.share_item0));
+                                                   ip, S(L.share_item0));
 
     // 5. segments and pair records
     ck = W(L.ws_ka); cv = W(L.ws_va); ak = W(L.ws_kb); av = W(L.ws_vb);

@@ -19,11 +19,11 @@ __device__ __forceinline__ int64_t snap_bound(int64_t c, int64_t a, int64_t b) {
 }
 
 // The items of a strip with pairs [a, b): cut at the (snapped) share
-// boundaries inside (a, b), and each piece of L pairs into ceil(L /
-// kItemPairs) items starting at floor(i * L / K) of the piece.  visit(i,
-// first) is called for every item start in order; returns the count.
+// boundaries inside (a, b), and each piece of L pairs into ceil(L / ip)
+// items starting at floor(i * L / K) of the piece (ip: the item size).
+// visit(i, first) is called for every item start in order; returns the count.
 template <typename F>
-__device__ int64_t strip_items(int64_t a, int64_t b, int64_t P, int64_t S, F visit) {
+__device__ int64_t strip_items(int64_t a, int64_t b, int64_t P, int64_t S, int64_t ip, F visit) {
   // shares w with a < floor(P w / S) < b: floor(P w / S) > a  <=>
   // w >= ceil((a + 1) S / P); floor(P w / S) < b  <=>  w < ceil(b S / P)
   const int64_t w_lo = ((a + 1) * S + P - 1) / P;
@@ -34,7 +34,7 @@ __device__ int64_t strip_items(int64_t a, int64_t b, int64_t P, int64_t S, F vis
     const int64_t e = w <= w_hi ? snap_bound((P * w) / S, a, b) : b;  // end of this piece
     const int64_t L = e - q;
     if (L > 0) {
-      const int64_t K = (L + kItemPairs - 1) / kItemPairs;
+      const int64_t K = (L + ip - 1) / ip;
       for (int64_t i = 0; i < K; ++i) visit(n + i, q + (i * L) / K);
       n += K;
       q = e;

@@ -389,7 +389,7 @@ constexpr int kPlanItems = 8192;   // item starts kept in LDS up to this many it
 // their strips and first pairs, the shares' first items, and the first
 // pixel-major pair of every feature row.
 __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ strip_np,
-                                                 int32_t strips, int32_t shares,
+                                                 int32_t strips, int32_t shares, int32_t ip,
                                                  int64_t items_cap, const int32_t* __restrict__ pix_count,
                                                  int64_t rows, int32_t* __restrict__ strip_p0,
                                                  int32_t* __restrict__ strip_it0,
@@ -449,7 +449,7 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
   int64_t isum = 0;
   for (int32_t s = s_lo; s < s_hi; ++s) {
     const int32_t a = sp0[s], v = sp0[s + 1] - a;
-    if (v > 0) isum += strip_items(a, a + v, P, shares, [](int64_t, int64_t) {});
+    if (v > 0) isum += strip_items(a, a + v, P, shares, ip, [](int64_t, int64_t) {});
   }
   int32_t n_items;
   int32_t ioff = block_exclusive_scan<kLT>((int32_t)isum, s_scan, &n_items);
@@ -459,7 +459,7 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
     strip_it0[s] = ioff;
     if (v > 0) {
       const int32_t first_item = ioff;
-      ioff += (int32_t)strip_items(a, a + v, P, shares, [&](int64_t i, int64_t first) {
+      ioff += (int32_t)strip_items(a, a + v, P, shares, ip, [&](int64_t i, int64_t first) {
         const int64_t item = first_item + i;
         if (item < items_cap) {
           item_strip[item] = s;
@@ -532,6 +532,7 @@ __global__ __launch_bounds__(kLT) void k_ls_plan(const int32_t* __restrict__ str
     pix_pair0[rows] = rtot;
     hdr[kHdrShares] = shares;
     hdr[kHdrSharesOk] = s_bad ? 0 : 1;
+    hdr[kHdrItemPairs] = ip;
   }
 }
 
@@ -945,7 +946,8 @@ hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t
   k_ls_map<<<g_nv, 256, 0, stream>>>(rd, rb, n_valid, d.P, d.cells, g, map);
   const unsigned strip_blocks = (unsigned)((L.sd.strips + kXcds - 1) / kXcds * kXcds);
   k_ls_strips<<<strip_blocks, kLT, 0, stream>>>(map, g, rkey, rnpts, strip_np, pix_count);
-  k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, L.items_cap, pix_count, d.rows,
+  k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, schedule_item_pairs(n_valid, shares),
+                                   L.items_cap, pix_count, d.rows,
                                    strip_p0, strip_it0, hdr, S(L.item_strip), S(L.item_pair0),
                                    S(L.share_item0), S(L.pix_pair0));
   k_ls_emit<<<strip_blocks, kLT, 0, stream>>>(

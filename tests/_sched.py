@@ -12,13 +12,20 @@ import numpy as np
 
 ALIGN = 256
 ITEM_PAIRS = 2048
+ITEM_PAIRS_BIG = 3072      # items of a schedule whose shares hold many kept points
+BIG_ITEM_POINTS = 16384    # kept points per share from which items are big
 STRIP_BYTES = 32 * 1024
 PAIR_HEAD = 1 << 15
 MAX_SHARES = 1024
 SHARE_ITEMS = 128
 MIN_PIECE = 512
 HDR = dict(pairs=0, items=1, segs=2, valid=3, occ=4, occ_found=5, empty=6, slots=7, comb=8, strips=9,
-           shares=10, shares_ok=11)
+           shares=10, shares_ok=11, item_pairs=12)
+
+
+def item_pairs(n_valid: int, shares: int) -> int:
+    """The item size a schedule of n_valid kept points in `shares` shares is cut at."""
+    return ITEM_PAIRS_BIG if shares > 0 and n_valid >= BIG_ITEM_POINTS * shares else ITEM_PAIRS
 
 
 def strip_dims(shape) -> dict:
@@ -88,16 +95,16 @@ def snap(c: int, a: int, b: int) -> int:
     return a if c - a < MIN_PIECE else (b if b - c < MIN_PIECE else c)
 
 
-def strip_items(a: int, b: int, P: int, S: int) -> list:
+def strip_items(a: int, b: int, P: int, S: int, ip: int = ITEM_PAIRS) -> list:
     """First pairs of the items of a strip with pairs [a, b): cut at the
     (snapped) share boundaries floor(P w / S) inside it, each piece of L pairs
-    into ceil(L / ITEM_PAIRS) items at floor(i L / K) of the piece."""
+    into ceil(L / ip) items at floor(i L / K) of the piece."""
     raw = [c for c in ((P * w) // S for w in range(1, S)) if a < c < b]
     cuts = sorted({snap(c, a, b) for c in raw} - {a, b})
     starts = []
     for q, e in zip([a] + cuts, cuts + [b]):
         L = e - q
-        K = -(-L // ITEM_PAIRS)
+        K = -(-L // ip)
         starts += [q + (i * L) // K for i in range(K)]
     return starts
 
@@ -127,12 +134,13 @@ def derive(plan: dict, shape, shares: int = 1) -> dict:
     p_rb, p_row, p_strip, p_lp, p_rd0 = rb[hp], row[hp], strip[hp], lp[hp], rd[hp]
     p_d0 = (p_rd0 % per_view) // hw
     npairs = hp.size
-    # items: strips cut at the shares, pieces cut into at most ITEM_PAIRS
+    # items: strips cut at the shares, pieces cut into at most ip pairs
+    ip = item_pairs(n, shares)
     s_head = np.r_[True, p_strip[1:] != p_strip[:-1]]
     s_p0 = np.r_[np.flatnonzero(s_head), npairs]
     item_strip, item_pair0 = [], []
     for j in range(s_p0.size - 1):
-        st = strip_items(int(s_p0[j]), int(s_p0[j + 1]), int(npairs), shares)
+        st = strip_items(int(s_p0[j]), int(s_p0[j + 1]), int(npairs), shares, ip)
         item_strip += [int(p_strip[s_p0[j]])] * len(st)
         item_pair0 += st
     item_start = np.zeros(npairs, dtype=bool)
@@ -181,7 +189,8 @@ def derive(plan: dict, shape, shares: int = 1) -> dict:
     return dict(
         n=dict(pairs=int(npairs), items=n_items, segs=int(nsegs), valid=n, occ=int(run_head.sum()),
                occ_found=int(run_head.sum()), empty=int(empty.size), slots=int(shared.sum()),
-               comb=int(comb.sum()), strips=int(s_p0.size - 1), shares=shares, shares_ok=shares_ok),
+               comb=int(comb.sum()), strips=int(s_p0.size - 1), shares=shares, shares_ok=shares_ok,
+               item_pairs=ip),
         pair_rd0=p_rd0, pair_ln=pair_ln, pair_seg=pair_seg, item_strip=np.array(item_strip, dtype=np.int64),
         item_pair0=np.r_[np.array(item_pair0, dtype=np.int64), npairs],
         item_seg0=np.r_[item_seg0, nsegs].astype(np.int64), seg_dest=seg_dest,

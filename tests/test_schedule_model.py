@@ -41,7 +41,7 @@ def _execute(sch, depth, feat, shape):
         rows = [(bn * H + h0 + lp // bws) * W + w0 + lp % bws for lp in range(npix)]
         p0, p1 = sch["item_pair0"][i], sch["item_pair0"][i + 1]
         g0, g1 = sch["item_seg0"][i], sch["item_seg0"][i + 1]
-        assert 1 <= p1 - p0 <= _sched.ITEM_PAIRS
+        assert 1 <= p1 - p0 <= sch["n"]["item_pairs"]
         seg = -1
         acc = {}
         for k in range(p0, p1):
@@ -120,7 +120,7 @@ def test_schedule_model_random(shape, shares):
 def test_shares_cut_items(shares):
     # every share boundary starts an item, so share w's items hold exactly its
     # pairs [floor(P w / S), floor(P (w + 1) / S)); items stay inside one strip
-    # and hold at most ITEM_PAIRS pairs
+    # and hold at most the schedule's item size in pairs
     cfg = CONFIGS["bevdet"]
     plan = oracle.prepare_ref(frustum_coor(cfg), cfg.shape())
     sch = _sched.derive(plan, cfg.shape(), shares=shares)
@@ -149,7 +149,7 @@ def test_shares_cut_items(shares):
         c = bound(w)
         j = np.searchsorted(s_p0, c, side="right") - 1
         assert c == s_p0[j] or min(c - s_p0[j], s_p0[j + 1] - c) >= _sched.MIN_PIECE
-    assert np.all(np.diff(ip0) >= 1) and np.all(np.diff(ip0) <= _sched.ITEM_PAIRS)
+    assert np.all(np.diff(ip0) >= 1) and np.all(np.diff(ip0) <= sch["n"]["item_pairs"])
     # every strip starts an item
     strip_p0 = ip0[:-1][np.r_[True, sch["item_strip"][1:] != sch["item_strip"][:-1]]]
     base = _sched.derive(plan, cfg.shape(), shares=1)
@@ -277,3 +277,21 @@ def test_walk_partition_model(G):
     ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, shape)
     ref = ref.reshape(out.shape)
     assert np.all(np.abs(out - ref) <= 1e-12 * mag.reshape(out.shape) + 1e-300)
+
+
+def test_item_size_rule():
+    """Items are big (ITEM_PAIRS_BIG) once the shares hold BIG_ITEM_POINTS
+    kept points each, else ITEM_PAIRS; a schedule's items respect its size,
+    and big items are used where pieces are long enough."""
+    assert _sched.item_pairs(4 * _sched.BIG_ITEM_POINTS, 4) == _sched.ITEM_PAIRS_BIG
+    assert _sched.item_pairs(4 * _sched.BIG_ITEM_POINTS - 1, 4) == _sched.ITEM_PAIRS
+    assert _sched.item_pairs(10**9, 0) == _sched.ITEM_PAIRS
+    cfg = CONFIGS["bevdet"]
+    plan = oracle.prepare_ref(frustum_coor(cfg), cfg.shape())
+    for shares, want in ((1, _sched.ITEM_PAIRS_BIG), (64, _sched.ITEM_PAIRS)):
+        sch = _sched.derive(plan, cfg.shape(), shares=shares)
+        assert sch["n"]["item_pairs"] == want
+        sizes = np.diff(sch["item_pair0"])
+        assert sizes.min() >= 1 and sizes.max() <= want
+        if want == _sched.ITEM_PAIRS_BIG:
+            assert sizes.max() > _sched.ITEM_PAIRS
