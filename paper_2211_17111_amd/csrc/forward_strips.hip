@@ -972,9 +972,9 @@ hipError_t launch_forward_scheduled(const Dims& d, int in_dtype, int out_dtype,
   a.n_occ = n_intervals;
   a.n_slots = n_slots;
   a.items_cap = (int32_t)L.items_cap;
-  // (the item size the schedule builders choose on this device; a schedule
-  // cut otherwise fails the header check)
-  a.item_pairs = schedule_item_pairs(n_valid, std::min<int64_t>(forward_workgroups(), kMaxShares));
+  // (the item size every schedule of n_valid kept points is cut at; a
+  // schedule cut otherwise fails the header check)
+  a.item_pairs = schedule_item_pairs(n_valid);
   a.C = (int32_t)d.C;
   a.H = (int32_t)d.H;
   a.W = (int32_t)d.W;

@@ -99,7 +99,7 @@ hipError_t launch_prepare(const Dims& d, const int32_t* coor, int32_t* ranks_dep
 //                               items), for the shares in the header
 constexpr int kItemPairs = 2048;          // most pairs of one forward item
 constexpr int kItemPairsBig = 3072;       //   of a schedule whose shares hold many items
-constexpr int64_t kBigItemPoints = 16384; // kept points per share from which items are big
+constexpr int64_t kBigItemPoints = 16384 * 256;  // kept points from which items are big
 constexpr int kStripBytes = 32 * 1024;    // staged feature bytes of a strip (4-byte elements)
 constexpr uint32_t kPairHead = 1u << 15;  // pair_ln: first pair of a segment
 constexpr uint32_t kPairPixel = kPairHead - 1;
@@ -109,11 +109,13 @@ constexpr int kHdrPairs = 0, kHdrItems = 1, kHdrSegs = 2, kHdrValid = 3, kHdrOcc
               kHdrSharesOk = 11,   // 1 if no share has more than kShareItems items
               kHdrItemPairs = 12;  // the item size the pieces were cut at
 constexpr int kMaxShares = 1024;   // most shares (workgroups of the scheduled forward)
-// Item size of a schedule of n_valid kept points cut into `shares` shares:
-// big items where each share holds many (a workgroup then walks a dozen or
-// more items, and each item stages its strip's rows once), else kItemPairs.
-inline int schedule_item_pairs(int64_t n_valid, int64_t shares) {
-  return shares > 0 && n_valid >= kBigItemPoints * shares ? kItemPairsBig : kItemPairs;
+// Item size of a schedule of n_valid kept points: big items where the
+// shares of a whole GPU hold many (16,384 kept points each over 256
+// workgroups: a workgroup then walks a dozen or more items, and each item
+// stages its strip's rows once), else kItemPairs.  It depends on n_valid
+// alone, so that a schedule built on one device runs on any other.
+inline int schedule_item_pairs(int64_t n_valid) {
+  return n_valid >= kBigItemPoints ? kItemPairsBig : kItemPairs;
 }
 constexpr int kShareItems = 128;   // most items of a share the forward takes as one
 constexpr int kMinPiece = 512;     // share boundaries closer to a strip end move to it

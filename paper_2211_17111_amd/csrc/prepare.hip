@@ -903,7 +903,7 @@ hipError_t launch_schedule(const Dims& d, const int32_t* rd, const int32_t* rb, 
     k_strips_end<<<1, 64, 0, stream>>>(hdr, strip_p0);
     const unsigned g_s = (unsigned)((scap + 255) / 256);
     const int32_t shares = (int32_t)std::min<int64_t>(forward_workgroups(), kMaxShares);
-    const int32_t ip = schedule_item_pairs(n_valid, shares);
+    const int32_t ip = schedule_item_pairs(n_valid);
     k_item_counts<<<g_s, 256, 0, stream>>>(hdr, strip_p0, scap, shares, ip, icount);
     scan_exclusive(icount, scap, sums, hdr + kHdrItems, stream);
     int32_t* item_flag = W(L.ws_flags);

@@ -946,7 +946,7 @@ hipError_t launch_schedule_local(const Dims& d, const int32_t* rd, const int32_t
   k_ls_map<<<g_nv, 256, 0, stream>>>(rd, rb, n_valid, d.P, d.cells, g, map);
   const unsigned strip_blocks = (unsigned)((L.sd.strips + kXcds - 1) / kXcds * kXcds);
   k_ls_strips<<<strip_blocks, kLT, 0, stream>>>(map, g, rkey, rnpts, strip_np, pix_count);
-  k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, schedule_item_pairs(n_valid, shares),
+  k_ls_plan<<<1, kLT, 0, stream>>>(strip_np, g.strips, shares, schedule_item_pairs(n_valid),
                                    L.items_cap, pix_count, d.rows,
                                    strip_p0, strip_it0, hdr, S(L.item_strip), S(L.item_pair0),
                                    S(L.share_item0), S(L.pix_pair0));

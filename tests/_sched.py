@@ -13,7 +13,7 @@ import numpy as np
 ALIGN = 256
 ITEM_PAIRS = 2048
 ITEM_PAIRS_BIG = 3072      # items of a schedule whose shares hold many kept points
-BIG_ITEM_POINTS = 16384    # kept points per share from which items are big
+BIG_ITEM_POINTS = 16384 * 256    # kept points from which items are big
 STRIP_BYTES = 32 * 1024
 PAIR_HEAD = 1 << 15
 MAX_SHARES = 1024
@@ -23,9 +23,9 @@ HDR = dict(pairs=0, items=1, segs=2, valid=3, occ=4, occ_found=5, empty=6, slots
            shares=10, shares_ok=11, item_pairs=12)
 
 
-def item_pairs(n_valid: int, shares: int) -> int:
-    """The item size a schedule of n_valid kept points in `shares` shares is cut at."""
-    return ITEM_PAIRS_BIG if shares > 0 and n_valid >= BIG_ITEM_POINTS * shares else ITEM_PAIRS
+def item_pairs(n_valid: int) -> int:
+    """The item size a schedule of n_valid kept points is cut at."""
+    return ITEM_PAIRS_BIG if n_valid >= BIG_ITEM_POINTS else ITEM_PAIRS
 
 
 def strip_dims(shape) -> dict:
@@ -135,7 +135,7 @@ def derive(plan: dict, shape, shares: int = 1) -> dict:
     p_d0 = (p_rd0 % per_view) // hw
     npairs = hp.size
     # items: strips cut at the shares, pieces cut into at most ip pairs
-    ip = item_pairs(n, shares)
+    ip = item_pairs(n)
     s_head = np.r_[True, p_strip[1:] != p_strip[:-1]]
     s_p0 = np.r_[np.flatnonzero(s_head), npairs]
     item_strip, item_pair0 = [], []

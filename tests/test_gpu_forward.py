@@ -384,11 +384,12 @@ def test_scheduled_workspace_checked():
     assert bool((out == 7.0).all())
 
 
-@pytest.mark.parametrize("case", ["slots", "unbuilt"])
+@pytest.mark.parametrize("case", ["slots", "unbuilt", "item size"])
 def test_scheduled_header_mismatch_nan(case):
     """A schedule whose header does not hold the counts of the call (another
-    slot count, or a buffer no build has written) gives NaN in every element
-    of `out`, never a partial or stale result."""
+    slot count, a buffer no build has written, or items cut at the other
+    size) gives NaN in every element of `out`, never a partial or stale
+    result."""
     cfg = CONFIGS["bevdet"]
     shape = cfg.shape()
     data = draw_inputs(cfg, with_grad=False)
@@ -399,6 +400,13 @@ def test_scheduled_header_mismatch_nan(case):
     buf = sched.buffer
     if case == "slots":
         n_slots += 1
+    elif case == "item size":
+        # a schedule cut at the other item size than this launch's rule gives
+        buf = sched.buffer.clone()
+        hdr = buf[:64].view(torch.int32)
+        want = _sched.item_pairs(plan.n_valid)
+        assert int(hdr[_sched.HDR["item_pairs"]]) == want
+        hdr[_sched.HDR["item_pairs"]] = _sched.ITEM_PAIRS_BIG + _sched.ITEM_PAIRS - want
     else:
         buf = torch.zeros_like(sched.buffer)
     ws = torch.empty(bp.bevpool_forward_scheduled_workspace_size(shape, n_slots) + 16, dtype=torch.uint8,

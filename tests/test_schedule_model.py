@@ -279,17 +279,19 @@ def test_walk_partition_model(G):
     assert np.all(np.abs(out - ref) <= 1e-12 * mag.reshape(out.shape) + 1e-300)
 
 
-def test_item_size_rule():
-    """Items are big (ITEM_PAIRS_BIG) once the shares hold BIG_ITEM_POINTS
-    kept points each, else ITEM_PAIRS; a schedule's items respect its size,
-    and big items are used where pieces are long enough."""
-    assert _sched.item_pairs(4 * _sched.BIG_ITEM_POINTS, 4) == _sched.ITEM_PAIRS_BIG
-    assert _sched.item_pairs(4 * _sched.BIG_ITEM_POINTS - 1, 4) == _sched.ITEM_PAIRS
-    assert _sched.item_pairs(10**9, 0) == _sched.ITEM_PAIRS
+def test_item_size_rule(monkeypatch):
+    """Items are big (ITEM_PAIRS_BIG) from BIG_ITEM_POINTS kept points on,
+    else ITEM_PAIRS; a schedule's items respect its size, and big items are
+    used where pieces are long enough (the threshold lowered here so that
+    bevdet's plan takes both sizes)."""
+    assert _sched.item_pairs(_sched.BIG_ITEM_POINTS) == _sched.ITEM_PAIRS_BIG
+    assert _sched.item_pairs(_sched.BIG_ITEM_POINTS - 1) == _sched.ITEM_PAIRS
     cfg = CONFIGS["bevdet"]
     plan = oracle.prepare_ref(frustum_coor(cfg), cfg.shape())
-    for shares, want in ((1, _sched.ITEM_PAIRS_BIG), (64, _sched.ITEM_PAIRS)):
-        sch = _sched.derive(plan, cfg.shape(), shares=shares)
+    n_valid = int(plan["n_valid"])
+    for limit, want in ((n_valid, _sched.ITEM_PAIRS_BIG), (n_valid + 1, _sched.ITEM_PAIRS)):
+        monkeypatch.setattr(_sched, "BIG_ITEM_POINTS", limit)
+        sch = _sched.derive(plan, cfg.shape(), shares=1)
         assert sch["n"]["item_pairs"] == want
         sizes = np.diff(sch["item_pair0"])
         assert sizes.min() >= 1 and sizes.max() <= want
