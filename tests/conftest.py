@@ -22,8 +22,8 @@ def _gpu_available() -> bool:
 
 
 def pytest_collection_modifyitems(config, items):
-    # GPU tests are skipped only when no GPU is visible at all; on a GPU machine a
-    # missing or broken library makes them fail loudly instead.
+    # GPU tests are skipped only when no GPU is visible at all; on a machine
+    # with a GPU a missing or broken library makes them fail loudly instead.
     if _gpu_available():
         return
     skip = pytest.mark.skip(reason="no GPU visible")
