@@ -3,7 +3,8 @@
 The headline (6 views, 40x100, D=118, C=80, fp32), large (4 samples,
 40x110, D=118, fp16 in and out, 256x256 grid), train (8 samples, 16x44,
 D=118, fp32) and voxel3d (the headline rig into a 128x128x16 voxel grid)
-workloads are compared over the whole output: the forward of
+workloads are compared over the whole output (and large's plan once more
+with float32 data, whose items are cut at the big size): the forward of
 both the interval-table path and the scheduled path, and grad_depth and
 grad_feat of both backward paths, each element within
 tol * sum|terms| + 1e-6 of the float64 oracle (section 2.1: the
@@ -115,3 +116,25 @@ def test_backward_every_element(name, path):
     scale = float((np.abs(g64) * c["mag"]).sum())
     tol = _gpu.TOL[cfg.dtype] * scale + 1e-6
     assert abs(r_d - lhs) <= tol and abs(r_f - lhs) <= tol, (lhs, r_d, r_f, tol)
+
+
+def test_big_items_float32():
+    """large's plan with float32 inputs and output: 6.45 M kept points, so
+    the schedule's items are cut at ITEM_PAIRS_BIG and the forward runs its
+    big-item float32 form (no record read-ahead); every output element
+    against the oracle."""
+    import dataclasses
+
+    import _sched
+    cfg = dataclasses.replace(CONFIGS["large"], dtype="f32", out_dtype="f32")
+    _gpu.say("[large, float32] inputs and oracle forward")
+    coor = frustum_coor(cfg)
+    data = draw_inputs(cfg, with_grad=False)
+    ref, mag = oracle.forward_ref(data["depth"], data["feat"], coor, cfg.shape())
+    plan = _gpu.run_prepare(coor, cfg.shape())
+    sched = bp.schedule(plan)
+    hdr = sched.buffer[:64].view(torch.int32).cpu()
+    assert int(hdr[_sched.HDR["item_pairs"]]) == _sched.ITEM_PAIRS_BIG
+    out = bp.forward_scheduled(_gpu.to_dev(data["depth"]), _gpu.to_dev(data["feat"]), sched)
+    torch.cuda.synchronize()
+    _gpu.assert_within(out.cpu().numpy(), ref, mag, "f32", label="large float32, big items", log=True)
